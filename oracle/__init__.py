@@ -1,0 +1,254 @@
+"""Plain CPU reference (the oracle) for the affine-recurrence hot path.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The product
+package never imports it, and it shares no code with the HIP sources.
+
+The arithmetic lives in ``sw_oracle.c`` (plain C, fp64 and uint32 loops).  This
+module only compiles that file with gcc and marshals numpy arrays to it.
+
+What each routine computes (see ``sw_oracle.c`` for the loops):
+
+* ``affine_scan`` / ``affine_scan_i32``: the recurrence of Sec. 3.1, Eq. (3),
+  ``h_t = a_t h_{t-1} + bx_t``, as a sequential loop; all inclusive states.
+* ``affine_prefix`` / ``affine_prefix_i32``: the inclusive prefix compositions
+  of Sec. 3.2 built with the operator of Eq. (7), and the state rebuilt from
+  them, ``h_t = A_{1:t} h_0 + U_{1:t}``.
+* ``compose`` / ``compose_u32``: Eq. (7) itself.
+* ``selective_scan``: the Mamba-style fused form (Sec. 1, Sec. 3.1) with
+  ``a = exp(delta A)``, ``u = delta B x``, ``y = sum_n C h + Dskip x``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sw_oracle.c")
+_HDR = os.path.join(_HERE, "sw_oracle.h")
+_LIB_PATH = os.path.join(_HERE, "libsw_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+_f32p = np.ctypeslib.ndpointer(dtype=np.float32, flags="C_CONTIGUOUS")
+_f64p = np.ctypeslib.ndpointer(dtype=np.float64, flags="C_CONTIGUOUS")
+_u32p = np.ctypeslib.ndpointer(dtype=np.uint32, flags="C_CONTIGUOUS")
+_i64p = np.ctypeslib.ndpointer(dtype=np.int64, flags="C_CONTIGUOUS")
+_vp = ctypes.c_void_p
+_i64 = ctypes.c_int64
+
+
+def build(force: bool = False) -> str:
+    """Compile sw_oracle.c into libsw_oracle.so (gcc, -O2, no fast-math)."""
+    stale = (not os.path.exists(_LIB_PATH)) or any(
+        os.path.getmtime(p) > os.path.getmtime(_LIB_PATH) for p in (_SRC, _HDR))
+    if force or stale:
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fno-fast-math", "-std=c11", "-Wall", "-Wextra", "-fPIC",
+               "-shared", "-pthread", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True, cwd=_HERE)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        lib.swo_threads_used.argtypes = [ctypes.c_int, _i64]
+        lib.swo_threads_used.restype = ctypes.c_int
+        lib.swo_compose_f64.argtypes = [ctypes.c_double] * 4 + [ctypes.POINTER(ctypes.c_double)] * 2
+        lib.swo_compose_f64.restype = None
+        lib.swo_compose_u32.argtypes = [ctypes.c_uint32] * 4 + [ctypes.POINTER(ctypes.c_uint32)] * 2
+        lib.swo_compose_u32.restype = None
+        lib.swo_affine_scan_f64.argtypes = [_vp] * 6 + [_i64, _i64, ctypes.c_int]
+        lib.swo_affine_scan_f64.restype = ctypes.c_int
+        lib.swo_affine_scan_u32.argtypes = [_vp] * 4 + [_i64, _i64, ctypes.c_int]
+        lib.swo_affine_scan_u32.restype = ctypes.c_int
+        lib.swo_affine_prefix_f64.argtypes = [_vp] * 6 + [_i64, _i64]
+        lib.swo_affine_prefix_f64.restype = ctypes.c_int
+        lib.swo_affine_prefix_u32.argtypes = [_vp] * 6 + [_i64, _i64]
+        lib.swo_affine_prefix_u32.restype = ctypes.c_int
+        lib.swo_selective_scan_f64.argtypes = [_vp] * 13 + [_i64, _i64, _i64, ctypes.c_int,
+                                                            ctypes.c_int]
+        lib.swo_selective_scan_f64.restype = ctypes.c_int
+        _lib = lib
+        return lib
+
+
+def _p(arr):
+    return None if arr is None else arr.ctypes.data_as(ctypes.c_void_p)
+
+
+def _as(arr, dtype):
+    return None if arr is None else np.ascontiguousarray(arr, dtype=dtype)
+
+
+def threads_used(requested: int, rows: int) -> int:
+    """Threads a call with ``requested`` threads (<=0: all CPUs) over ``rows`` uses."""
+    return int(_load().swo_threads_used(int(requested), int(rows)))
+
+
+def compose(p2, p1):
+    """Eq. (7) in fp64: ``(A2,U2) (+) (A1,U1) = (A2 A1, A2 U1 + U2)``."""
+    A = ctypes.c_double()
+    U = ctypes.c_double()
+    _load().swo_compose_f64(float(p2[0]), float(p2[1]), float(p1[0]), float(p1[1]),
+                            ctypes.byref(A), ctypes.byref(U))
+    return (A.value, U.value)
+
+
+def compose_u32(p2, p1):
+    """Eq. (7) in Z/2^32 (operands and results as uint32)."""
+    A = ctypes.c_uint32()
+    U = ctypes.c_uint32()
+    m = 0xFFFFFFFF
+    _load().swo_compose_u32(int(p2[0]) & m, int(p2[1]) & m, int(p1[0]) & m, int(p1[1]) & m,
+                            ctypes.byref(A), ctypes.byref(U))
+    return (A.value, U.value)
+
+
+def _rows_L(a):
+    L = a.shape[-1] if a.ndim else 0
+    rows = int(np.prod(a.shape[:-1])) if a.ndim > 1 else 1
+    return rows, L
+
+
+def affine_scan(a, bx, h0=None, bounds: bool = False, threads: int = 0):
+    """Sequential fp64 evaluation of Eq. (3) over the last axis.
+
+    ``a`` and ``bx`` are fp32 arrays of shape (..., L); ``h0`` has shape (...)
+    or is None (zero).  Returns ``h`` (fp64, same shape), and with
+    ``bounds=True`` also ``(mag, sens)`` (see sw_oracle.c).
+    """
+    a = _as(a, np.float32)
+    bx = _as(bx, np.float32)
+    if a.shape != bx.shape:
+        raise ValueError("a and bx must have the same shape")
+    rows, L = _rows_L(a)
+    h0 = _as(h0, np.float32)
+    if h0 is not None and h0.size != rows:
+        raise ValueError("h0 must hold one value per row")
+    h = np.empty(a.shape, np.float64)
+    mag = np.empty(a.shape, np.float64) if bounds else None
+    sens = np.empty(a.shape, np.float64) if bounds else None
+    rc = _load().swo_affine_scan_f64(_p(a), _p(bx), _p(h0), _p(h), _p(mag), _p(sens), rows, L,
+                                     int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return (h, mag, sens) if bounds else h
+
+
+def affine_scan_i32(a, bx, h0=None, threads: int = 0):
+    """Eq. (3) in the int32 wraparound ring; int32 in, int32 out."""
+    a = _as(a, np.int32).view(np.uint32)
+    bx = _as(bx, np.int32).view(np.uint32)
+    if a.shape != bx.shape:
+        raise ValueError("a and bx must have the same shape")
+    rows, L = _rows_L(a)
+    h0 = None if h0 is None else _as(h0, np.int32).view(np.uint32)
+    if h0 is not None and h0.size != rows:
+        raise ValueError("h0 must hold one value per row")
+    h = np.empty(a.shape, np.uint32)
+    rc = _load().swo_affine_scan_u32(_p(a), _p(bx), _p(h0), _p(h), rows, L, int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return h.view(np.int32)
+
+
+def affine_prefix(a, bx, h0=None):
+    """Sec. 3.2 prefix compositions (fp64): returns ``(A_pre, U_pre, h)``."""
+    a = _as(a, np.float32)
+    bx = _as(bx, np.float32)
+    rows, L = _rows_L(a)
+    h0 = _as(h0, np.float32)
+    A = np.empty(a.shape, np.float64)
+    U = np.empty(a.shape, np.float64)
+    h = np.empty(a.shape, np.float64)
+    if _load().swo_affine_prefix_f64(_p(a), _p(bx), _p(h0), _p(A), _p(U), _p(h), rows, L):
+        raise ValueError("oracle rejected the arguments")
+    return A, U, h
+
+
+def affine_prefix_i32(a, bx, h0=None):
+    """Sec. 3.2 prefix compositions in Z/2^32: returns int32 ``(A_pre, U_pre, h)``."""
+    a = _as(a, np.int32).view(np.uint32)
+    bx = _as(bx, np.int32).view(np.uint32)
+    rows, L = _rows_L(a)
+    h0 = None if h0 is None else _as(h0, np.int32).view(np.uint32)
+    A = np.empty(a.shape, np.uint32)
+    U = np.empty(a.shape, np.uint32)
+    h = np.empty(a.shape, np.uint32)
+    if _load().swo_affine_prefix_u32(_p(a), _p(bx), _p(h0), _p(A), _p(U), _p(h), rows, L):
+        raise ValueError("oracle rejected the arguments")
+    return A.view(np.int32), U.view(np.int32), h.view(np.int32)
+
+
+def selective_scan(x, delta, A, Bm, Cm, Dskip=None, rows=None, a_mode: int = 0,
+                   bounds: bool = False, threads: int = 0):
+    """Fused selective scan in fp64.
+
+    Shapes: ``x, delta`` (B, D, L); ``A`` (D, N); ``Bm, Cm`` (B, L, N);
+    ``Dskip`` (D,) or None.  All values are taken as given (fp32, or bf16
+    values already widened exactly to fp32).
+
+    ``rows``: optional 1-D array of flat row indices ``b*D + d``; only those
+    rows are evaluated and results have a leading axis of len(rows) instead
+    of (B, D).
+
+    Returns a dict with ``y`` and ``h_last``; with ``bounds=True`` also
+    ``y_mag, y_sens, h_mag, h_sens``.
+    """
+    x = np.asarray(x)
+    Bsz, D, L = x.shape
+    N = np.asarray(A).shape[1]
+    x2 = x.reshape(Bsz * D, L)
+    d2 = np.asarray(delta).reshape(Bsz * D, L)
+    if rows is None:
+        ridx = None
+        xs = _as(x2, np.float32)
+        ds = _as(d2, np.float32)
+        R = Bsz * D
+        row_b = np.repeat(np.arange(Bsz, dtype=np.int64), D)
+        As = _as(np.tile(np.asarray(A, np.float32), (Bsz, 1)), np.float32)
+        Ds = None if Dskip is None else _as(np.tile(np.asarray(Dskip, np.float32), Bsz),
+                                            np.float32)
+    else:
+        ridx = np.asarray(rows, dtype=np.int64).reshape(-1)
+        if ridx.size and (ridx.min() < 0 or ridx.max() >= Bsz * D):
+            raise ValueError("row index out of range")
+        R = ridx.size
+        xs = _as(x2[ridx], np.float32)
+        ds = _as(d2[ridx], np.float32)
+        row_b = np.ascontiguousarray(ridx // D, dtype=np.int64)
+        As = _as(np.asarray(A, np.float32)[ridx % D], np.float32)
+        Ds = None if Dskip is None else _as(np.asarray(Dskip, np.float32)[ridx % D], np.float32)
+    Bs = _as(Bm, np.float32)
+    Cs = _as(Cm, np.float32)
+    if Bs.shape != (Bsz, L, N) or Cs.shape != (Bsz, L, N):
+        raise ValueError("Bm and Cm must have shape (B, L, N)")
+    y = np.empty((R, L), np.float64)
+    h_last = np.empty((R, N), np.float64)
+    ym = np.empty((R, L), np.float64) if bounds else None
+    ys = np.empty((R, L), np.float64) if bounds else None
+    hm = np.empty((R, N), np.float64) if bounds else None
+    hs = np.empty((R, N), np.float64) if bounds else None
+    rc = _load().swo_selective_scan_f64(_p(xs), _p(ds), _p(As), _p(Bs), _p(Cs), _p(row_b),
+                                        _p(Ds), _p(y), _p(h_last), _p(ym), _p(ys), _p(hm),
+                                        _p(hs), R, N, L, int(a_mode), int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    out = {"y": y, "h_last": h_last}
+    if bounds:
+        out.update(y_mag=ym, y_sens=ys, h_mag=hm, h_sens=hs)
+    if ridx is None:
+        for k in list(out):
+            out[k] = out[k].reshape((Bsz, D) + out[k].shape[1:])
+    return out

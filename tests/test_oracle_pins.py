@@ -1,0 +1,420 @@
+"""Pins of the oracle to facts that do not come from the oracle itself.
+
+The paper prints no output values, so the oracle is pinned by:
+  * brute force of the unrolled closed form, Sec. 3.2 Eq. (5), in exact
+    rational arithmetic (fp inputs are exact binary fractions) and in exact
+    integers modulo 2^32;
+  * closed forms: constant a (geometric series), a = 1 (prefix sum), a = 0,
+    and in Z/2^32 a = 2 and a = -1;
+  * the algebra of Eq. (7): associativity, the identity pair, the
+    non-commutativity that fixes the operand order, and split invariance
+    (a segment's aggregate carries the state across a cut);
+  * the hand-worked four-leaf tree of Fig. 2 (tests/golden);
+  * for the fused form: exact rational brute force with a rounded to fp32,
+    reduction to the bare recurrence, and the closed forms A = 0, a = 0
+    (delta*A <= -800), B = 0 and a constant-parameter geometric series that
+    fixes exp(delta*A) (base e, sign as given).
+All of these run on the CPU.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+MASK = (1 << 32) - 1
+
+
+def _rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def _frac(v):
+    return Fraction(float(v))
+
+
+def _brute_eq5(a_row, u_row, h0):
+    """Eq. (5): h_t = (prod_{i<=t} a_i) h0 + sum_k (prod_{k<i<=t} a_i) u_k, exactly."""
+    a = [_frac(v) for v in a_row]
+    u = [_frac(v) for v in u_row]
+    out = []
+    for t in range(len(a)):
+        p = Fraction(1)
+        for i in range(t + 1):
+            p *= a[i]
+        s = p * _frac(h0)
+        for k in range(t + 1):
+            p = Fraction(1)
+            for i in range(k + 1, t + 1):
+                p *= a[i]
+            s += p * u[k]
+        out.append(s)
+    return out
+
+
+def _brute_eq5_int(a_row, u_row, h0):
+    a = [int(v) & MASK for v in a_row]
+    u = [int(v) & MASK for v in u_row]
+    out = []
+    for t in range(len(a)):
+        p = 1
+        for i in range(t + 1):
+            p = (p * a[i]) & MASK
+        s = (p * (int(h0) & MASK)) & MASK
+        for k in range(t + 1):
+            p = 1
+            for i in range(k + 1, t + 1):
+                p = (p * a[i]) & MASK
+            s = (s + p * u[k]) & MASK
+        out.append(s)
+    return np.array(out, dtype=np.uint64).astype(np.uint32).view(np.int32)
+
+
+# ---------------------------------------------------------------- bare, fp64
+
+@pytest.mark.parametrize("seed,L", [(101, 1), (102, 7), (103, 24)])
+def test_fp_matches_eq5_bruteforce(seed, L):
+    rng = _rng(seed)
+    rows = 3
+    a = rng.uniform(-1.2, 1.2, size=(rows, L)).astype(np.float32)
+    bx = rng.standard_normal(size=(rows, L)).astype(np.float32)
+    h0 = rng.standard_normal(size=(rows,)).astype(np.float32)
+    h, mag, sens = oracle.affine_scan(a, bx, h0, bounds=True)
+    for r in range(rows):
+        exact = _brute_eq5(a[r], bx[r], h0[r])
+        for t in range(L):
+            tol = 1e-14 * (mag[r, t] + sens[r, t]) + 1e-300
+            assert abs(h[r, t] - float(exact[t])) <= tol
+
+
+def test_bounds_match_their_definitions():
+    """mag_t is the abs-sum of the Eq. (5) terms; sens_t = sum (t-k)|prod a||u_k|."""
+    rng = _rng(7)
+    L = 12
+    a = rng.uniform(-1.1, 1.1, size=(1, L)).astype(np.float32)
+    bx = rng.standard_normal(size=(1, L)).astype(np.float32)
+    h0 = np.array([0.75], np.float32)
+    h, mag, sens = oracle.affine_scan(a, bx, h0, bounds=True)
+    av = [abs(_frac(v)) for v in a[0]]
+    uv = [abs(_frac(v)) for v in bx[0]]
+    for t in range(L):  # state index t is h_{t+1} in the 1-based notation
+        m = abs(_frac(h0[0]))
+        for i in range(t + 1):
+            m *= av[i]
+        s = m * (t + 1)
+        for k in range(t + 1):
+            p = Fraction(1)
+            for i in range(k + 1, t + 1):
+                p *= av[i]
+            m += p * uv[k]
+            s += p * uv[k] * (t - k)
+        assert abs(mag[0, t] - float(m)) <= 1e-14 * float(m)
+        assert abs(sens[0, t] - float(s)) <= 1e-14 * float(s) + 1e-300
+        assert abs(h[0, t]) <= mag[0, t] * (1 + 1e-15)
+
+
+def test_geometric_series_closed_form():
+    """Constant a = c, constant u = v: h_t = c^t h0 + v (1 - c^t) / (1 - c)."""
+    c, v, h0, L = np.float32(0.96875), np.float32(0.5), np.float32(2.0), 300
+    a = np.full((1, L), c, np.float32)
+    bx = np.full((1, L), v, np.float32)
+    h = oracle.affine_scan(a, bx, np.array([h0]))[0]
+    t = np.arange(1, L + 1, dtype=np.float64)
+    ref = float(c) ** t * float(h0) + float(v) * (1 - float(c) ** t) / (1 - float(c))
+    np.testing.assert_allclose(h, ref, rtol=1e-13, atol=0)
+
+
+def test_unit_a_is_prefix_sum_exact():
+    rng = _rng(8)
+    L = 5000
+    u = rng.integers(-1000, 1000, size=(2, L)).astype(np.float32)
+    h0 = np.array([3.0, -7.0], np.float32)
+    h = oracle.affine_scan(np.ones_like(u), u, h0)
+    ref = np.cumsum(u.astype(np.float64), axis=1) + h0[:, None]
+    assert np.array_equal(h, ref)
+
+
+def test_zero_a_forgets_state():
+    rng = _rng(9)
+    u = rng.standard_normal(size=(3, 50)).astype(np.float32)
+    h = oracle.affine_scan(np.zeros_like(u), u, np.array([5, 6, 7], np.float32))
+    assert np.array_equal(h, u.astype(np.float64))
+
+
+def test_empty_and_single_step():
+    h = oracle.affine_scan(np.zeros((3, 0), np.float32), np.zeros((3, 0), np.float32))
+    assert h.shape == (3, 0)
+    h = oracle.affine_scan(np.array([[0.5]], np.float32), np.array([[2.0]], np.float32),
+                           np.array([4.0], np.float32))
+    assert h[0, 0] == 0.5 * 4.0 + 2.0
+
+
+# ---------------------------------------------------------------- bare, int32
+
+@pytest.mark.parametrize("seed,L,variant", [(111, 1, "u"), (112, 9, "u"), (113, 33, "odd"),
+                                            (114, 40, "h0")])
+def test_int_matches_eq5_bruteforce(seed, L, variant):
+    rng = _rng(seed)
+    rows = 3
+    a = rng.integers(-2 ** 31, 2 ** 31, size=(rows, L), dtype=np.int64).astype(np.int32)
+    if variant == "odd":
+        a |= 1
+    bx = rng.integers(-2 ** 31, 2 ** 31, size=(rows, L), dtype=np.int64).astype(np.int32)
+    h0 = (rng.integers(-2 ** 31, 2 ** 31, size=(rows,), dtype=np.int64).astype(np.int32)
+          if variant == "h0" else None)
+    h = oracle.affine_scan_i32(a, bx, h0)
+    for r in range(rows):
+        ref = _brute_eq5_int(a[r], bx[r], 0 if h0 is None else h0[r])
+        assert np.array_equal(h[r], ref)
+
+
+def test_int_closed_forms():
+    rng = _rng(12)
+    L = 200
+    u = rng.integers(-2 ** 31, 2 ** 31, size=(1, L), dtype=np.int64).astype(np.int32)
+    uu = [int(v) & MASK for v in u[0]]
+    h0 = 123456789
+    # a = 1: prefix sum mod 2^32
+    h = oracle.affine_scan_i32(np.ones_like(u), u, np.array([h0], np.int32))[0]
+    acc, ref = h0, []
+    for v in uu:
+        acc = (acc + v) & MASK
+        ref.append(acc)
+    assert np.array_equal(h.view(np.uint32), np.array(ref, np.uint32))
+    # a = 2: h_t = 2^t h0 + sum_k 2^(t-k) u_k mod 2^32 (only the last 32 terms survive)
+    h = oracle.affine_scan_i32(np.full_like(u, 2), u, np.array([h0], np.int32))[0]
+    for t in range(L):
+        s = (pow(2, t + 1, 1 << 32) * h0) & MASK
+        for k in range(max(0, t - 40), t + 1):
+            s = (s + pow(2, t - k, 1 << 32) * uu[k]) & MASK
+        assert int(h.view(np.uint32)[t]) == s
+    # a = -1: alternating sum
+    h = oracle.affine_scan_i32(np.full_like(u, -1), u, np.array([h0], np.int32))[0]
+    for t in range(L):
+        s = ((-1) ** (t + 1) * h0) & MASK
+        for k in range(t + 1):
+            s = (s + (-1) ** (t - k) * uu[k]) & MASK
+        assert int(h.view(np.uint32)[t]) == s
+
+
+# ---------------------------------------------------------------- Eq. (7)
+
+def test_compose_associative_identity_noncommutative_u32():
+    rng = _rng(21)
+    p = rng.integers(0, 2 ** 32, size=(3000, 3, 2), dtype=np.uint64)
+    ident = (1, 0)
+    noncomm = 0
+    for (p1, p2, p3) in p:
+        left = oracle.compose_u32(oracle.compose_u32(p3, p2), p1)
+        right = oracle.compose_u32(p3, oracle.compose_u32(p2, p1))
+        assert left == right
+        assert oracle.compose_u32(ident, p1) == (int(p1[0]), int(p1[1]))
+        assert oracle.compose_u32(p1, ident) == (int(p1[0]), int(p1[1]))
+        if oracle.compose_u32(p2, p1) != oracle.compose_u32(p1, p2):
+            noncomm += 1
+    assert noncomm > 2900  # the operand order matters almost always
+
+
+def test_compose_associative_fp64():
+    rng = _rng(22)
+    for _ in range(2000):
+        p1, p2, p3 = rng.uniform(-2, 2, size=(3, 2))
+        l = oracle.compose(oracle.compose(p3, p2), p1)
+        r = oracle.compose(p3, oracle.compose(p2, p1))
+        scale = 1 + abs(p3[0] * p2[0] * p1[1]) + abs(p3[0] * p2[1]) + abs(p3[1])
+        assert abs(l[0] - r[0]) <= 4 * 2 ** -53 * (1 + abs(p1[0] * p2[0] * p3[0]))
+        assert abs(l[1] - r[1]) <= 8 * 2 ** -53 * scale
+    # the later segment is the left operand: (a2,u2)(+)(a1,u1) applied to h is a2(a1 h+u1)+u2
+    A, U = oracle.compose((3.0, 5.0), (2.0, 7.0))
+    h = 11.0
+    assert A * h + U == 3.0 * (2.0 * h + 7.0) + 5.0
+
+
+def test_fig2_four_leaf_tree_golden():
+    with open(os.path.join(GOLDEN, "fig2_four_leaf_tree.json")) as f:
+        g = json.load(f)
+    p1, p2, p3, p4 = [tuple(p) for p in g["pairs"]]
+    assert oracle.compose(p2, p1) == tuple(map(float, g["p2_p1"]))
+    assert oracle.compose(p4, p3) == tuple(map(float, g["p4_p3"]))
+    root = oracle.compose(oracle.compose(p4, p3), oracle.compose(p2, p1))
+    assert root == tuple(map(float, g["root"]))
+    a = np.array([[p[0] for p in g["pairs"]]], np.int32)
+    bx = np.array([[p[1] for p in g["pairs"]]], np.int32)
+    h0 = np.array([g["h0"]], np.int32)
+    A, U, h = oracle.affine_prefix_i32(a, bx, h0)
+    assert A[0].tolist() == [p[0] for p in g["inclusive_prefixes"]]
+    assert U[0].tolist() == [p[1] for p in g["inclusive_prefixes"]]
+    assert h[0].tolist() == g["states"]
+    assert oracle.affine_scan_i32(a, bx, h0)[0].tolist() == g["states"]
+    assert oracle.affine_scan(a.astype(np.float32), bx.astype(np.float32),
+                              h0.astype(np.float32))[0].tolist() == g["states"]
+
+
+def test_prefix_route_equals_sequential_route():
+    rng = _rng(23)
+    a = rng.integers(-2 ** 31, 2 ** 31, size=(4, 777), dtype=np.int64).astype(np.int32)
+    bx = rng.integers(-2 ** 31, 2 ** 31, size=(4, 777), dtype=np.int64).astype(np.int32)
+    h0 = rng.integers(-2 ** 31, 2 ** 31, size=(4,), dtype=np.int64).astype(np.int32)
+    _, _, h_pre = oracle.affine_prefix_i32(a, bx, h0)
+    assert np.array_equal(h_pre, oracle.affine_scan_i32(a, bx, h0))
+    af = rng.uniform(0.5, 1.0, size=(4, 777)).astype(np.float32)
+    bf = rng.standard_normal(size=(4, 777)).astype(np.float32)
+    h0f = rng.standard_normal(size=(4,)).astype(np.float32)
+    _, _, hp = oracle.affine_prefix(af, bf, h0f)
+    hs, mag, sens = oracle.affine_scan(af, bf, h0f, bounds=True)
+    assert np.all(np.abs(hp - hs) <= 1e-13 * (mag + sens))
+
+
+@pytest.mark.parametrize("cut", [1, 17, 500, 999])
+def test_split_invariance_u32(cut):
+    """h_L = A_{cut+1:L} h_cut + U_{cut+1:L}: the segment aggregate carries the state."""
+    rng = _rng(24 + cut)
+    L = 1000
+    a = (rng.integers(-2 ** 31, 2 ** 31, size=(1, L), dtype=np.int64).astype(np.int32) | 1)
+    bx = rng.integers(-2 ** 31, 2 ** 31, size=(1, L), dtype=np.int64).astype(np.int32)
+    h0 = np.array([987654321], np.int32)
+    h = oracle.affine_scan_i32(a, bx, h0)[0].view(np.uint32)
+    Aseg, Useg, _ = oracle.affine_prefix_i32(a[:, cut:], bx[:, cut:])
+    Aagg = int(Aseg[0, -1].view(np.uint32))
+    Uagg = int(Useg[0, -1].view(np.uint32))
+    assert (Aagg * int(h[cut - 1]) + Uagg) & MASK == int(h[-1])
+    # and every intermediate state after the cut, from the segment's prefixes
+    Ap = Aseg[0].view(np.uint32).astype(np.uint64)
+    Up = Useg[0].view(np.uint32).astype(np.uint64)
+    rebuilt = (Ap * np.uint64(int(h[cut - 1])) + Up) & np.uint64(MASK)
+    assert np.array_equal(rebuilt.astype(np.uint32), h[cut:])
+
+
+# ---------------------------------------------------------------- fused form
+
+def _fused_inputs(rng, B, D, N, L, dyadic=False):
+    if dyadic:  # small integers and powers of two: delta*x*B exact in fp32
+        x = rng.integers(-4, 5, size=(B, D, L)).astype(np.float32)
+        delta = (2.0 ** rng.integers(-6, -2, size=(B, D, L))).astype(np.float32)
+        Bm = rng.integers(-4, 5, size=(B, L, N)).astype(np.float32)
+        Cm = rng.integers(-4, 5, size=(B, L, N)).astype(np.float32)
+    else:
+        x = rng.standard_normal(size=(B, D, L)).astype(np.float32)
+        delta = np.logaddexp(0, 0.5 * rng.standard_normal(size=(B, D, L)) - 2).astype(np.float32)
+        Bm = rng.standard_normal(size=(B, L, N)).astype(np.float32)
+        Cm = rng.standard_normal(size=(B, L, N)).astype(np.float32)
+    A = -np.exp(rng.uniform(0, np.log(16), size=(D, N))).astype(np.float32)
+    Dskip = rng.standard_normal(size=(D,)).astype(np.float32)
+    return x, delta, A, Bm, Cm, Dskip
+
+
+def test_fused_bruteforce_with_fp32_a():
+    """a_mode=1 (a rounded to fp32) makes every quantity an exact binary
+    fraction, so Eq. (5) per (b,d,n) plus the projection is checked exactly."""
+    rng = _rng(31)
+    B, D, N, L = 2, 3, 3, 10
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L)
+    o = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, a_mode=1, bounds=True)
+    for b in range(B):
+        for d in range(D):
+            yref = [Fraction(float(Dskip[d])) * _frac(x[b, d, t]) for t in range(L)]
+            for n in range(N):
+                a32 = [np.float32(math.exp(float(delta[b, d, t]) * float(A[d, n])))
+                       for t in range(L)]
+                u = [_frac(delta[b, d, t]) * _frac(x[b, d, t]) * _frac(Bm[b, t, n])
+                     for t in range(L)]
+                h = Fraction(0)
+                for t in range(L):
+                    h = _frac(a32[t]) * h + u[t]
+                    yref[t] += _frac(Cm[b, t, n]) * h
+                tol = 1e-14 * o["h_mag"][b, d, n] + 1e-300
+                assert abs(o["h_last"][b, d, n] - float(h)) <= tol
+            for t in range(L):
+                assert abs(o["y"][b, d, t] - float(yref[t])) <= 1e-14 * o["y_mag"][b, d, t] + 1e-300
+
+
+def test_fused_reduces_to_bare_recurrence():
+    rng = _rng(32)
+    B, D, N, L = 2, 4, 5, 300
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L, dyadic=True)
+    o = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, a_mode=1)
+    for b in range(B):
+        for d in range(D):
+            y = Dskip[d].astype(np.float64) * x[b, d].astype(np.float64)
+            for n in range(N):
+                a32 = np.exp(delta[b, d].astype(np.float64) * float(A[d, n])).astype(np.float32)
+                u = (delta[b, d] * x[b, d] * Bm[b, :, n]).astype(np.float32)  # exact: dyadic
+                assert np.array_equal(u.astype(np.float64), delta[b, d].astype(np.float64)
+                                      * x[b, d] * Bm[b, :, n])
+                h = oracle.affine_scan(a32[None], u[None])[0]
+                assert abs(o["h_last"][b, d, n] - h[-1]) <= 1e-12 * (1 + abs(h).max())
+                y = y + Cm[b, :, n].astype(np.float64) * h
+            np.testing.assert_allclose(o["y"][b, d], y, rtol=1e-12, atol=1e-12)
+
+
+def test_fused_exp_parameterisation_geometric():
+    """N=1, constant delta and A, x=B=C=1, Dskip=0: a = e^{delta A} and
+    y_t = delta (1 - a^t) / (1 - a); fixes the base and sign of the exponent."""
+    L, dl, Av = 400, 0.0625, -1.5
+    x = np.ones((1, 1, L), np.float32)
+    delta = np.full((1, 1, L), dl, np.float32)
+    A = np.array([[Av]], np.float32)
+    ones = np.ones((1, L, 1), np.float32)
+    o = oracle.selective_scan(x, delta, A, ones, ones, np.zeros(1, np.float32))
+    a = math.exp(dl * Av)
+    t = np.arange(1, L + 1)
+    ref = dl * (1 - a ** t) / (1 - a)
+    np.testing.assert_allclose(o["y"][0, 0], ref, rtol=1e-12)
+    np.testing.assert_allclose(o["h_last"][0, 0, 0], ref[-1], rtol=1e-12)
+
+
+def test_fused_zero_A_is_prefix_sum():
+    rng = _rng(33)
+    B, D, N, L = 1, 2, 4, 1000
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L, dyadic=True)
+    A[:] = 0.0
+    o = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip)
+    for d in range(D):
+        y = Dskip[d].astype(np.float64) * x[0, d]
+        for n in range(N):
+            h = np.cumsum(delta[0, d].astype(np.float64) * x[0, d] * Bm[0, :, n])
+            y = y + Cm[0, :, n] * h
+            assert o["h_last"][0, d, n] == h[-1]
+        assert np.array_equal(o["y"][0, d], y)
+
+
+def test_fused_underflowed_a_and_zero_B():
+    rng = _rng(34)
+    B, D, N, L = 2, 3, 4, 64
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L, dyadic=True)
+    A2 = np.full_like(A, -1e6)  # delta*A <= -800 for every delta here: a == 0
+    o = oracle.selective_scan(x, delta, A2, Bm, Cm, Dskip)
+    for b in range(B):
+        for d in range(D):
+            u = delta[b, d, :, None].astype(np.float64) * x[b, d, :, None] * Bm[b]
+            ref = (Cm[b] * u).sum(axis=1) + Dskip[d].astype(np.float64) * x[b, d]
+            np.testing.assert_allclose(o["y"][b, d], ref, rtol=1e-15, atol=1e-15)
+            assert np.array_equal(o["h_last"][b, d], u[-1])
+    o = oracle.selective_scan(x, delta, A, np.zeros_like(Bm), Cm, Dskip)
+    assert np.array_equal(o["y"], Dskip[None, :, None].astype(np.float64) * x)
+    assert not np.any(o["h_last"])
+
+
+def test_fused_row_subset_matches_full():
+    rng = _rng(35)
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, 3, 5, 4, 37)
+    full = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip)
+    rows = np.array([14, 0, 7, 7, 3])
+    sub = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, rows=rows)
+    assert np.array_equal(sub["y"], full["y"].reshape(15, 37)[rows])
+    assert np.array_equal(sub["h_last"], full["h_last"].reshape(15, 4)[rows])
+
+
+def test_threads_do_not_change_results():
+    rng = _rng(36)
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, 2, 33, 4, 50)
+    one = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, threads=1)
+    many = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, threads=8)
+    assert np.array_equal(one["y"], many["y"])
+    assert oracle.threads_used(3, 100) == 3
+    assert oracle.threads_used(8, 2) == 2
