@@ -1,0 +1,128 @@
+/*
+ * scanweaver.h -- C ABI of libscanweaver.so, the MI355X (gfx950) library for
+ * the forward affine recurrence and the Mamba-style fused selective scan.
+ *
+ * The operation (ScanWeaver, Sec. 3.1-3.2): for every independent channel,
+ *
+ *     h_t = a_t * h_{t-1} + bx_t                                   Eq. (3)
+ *
+ * evaluated as a prefix scan over the affine pairs (A_t, U_t) = (a_t, bx_t)
+ * of Eq. (6) under the composition of Eq. (7),
+ *
+ *     (A2, U2) (+) (A1, U1) = (A2*A1, A2*U1 + U2)   (left = later segment),
+ *
+ * so that h_t = A_{1:t} h_0 + U_{1:t}.  The library returns the inclusive
+ * states h_1..h_L, i.e. exactly what a sequential traversal produces
+ * (Sec. 3.2), for every (b, d) row.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Arrays are caller-owned DEVICE pointers (hipMalloc / torch CUDA tensors)
+ *    on the current HIP device, dense and row-major; the library never frees
+ *    or keeps them.  Host pointers are rejected with SW_ERR_INVALID_ARG.
+ *  - Alignment: natural alignment of the element type is required (4 bytes for
+ *    fp32/int32, 2 bytes for bf16).  Wider vector loads are used when every
+ *    pointer is 16-byte aligned and L allows it; results do not depend on it.
+ *  - Calls are asynchronous: SW_OK means the work was enqueued on the stream
+ *    set with sw_set_stream() for the calling thread (default: the null
+ *    stream).  Faults surface at the caller's next synchronisation.
+ *  - Validation happens before anything is enqueued: on any non-OK return no
+ *    output has been written and nothing is launched.  sw_last_error() gives
+ *    a message for the last non-OK return on the calling thread.
+ *  - Negative sizes are SW_ERR_INVALID_ARG.  A call whose output is empty
+ *    (B*D == 0, or L == 0 for the bare scan) returns SW_OK and touches
+ *    nothing; pointers are not inspected in that case.
+ *  - Outputs must not overlap inputs or each other (SW_ERR_INVALID_ARG).
+ *  - Scratch memory (only for sequences split across workgroups) is taken
+ *    from the device's stream-ordered pool on the same stream and returned
+ *    to it before the call returns; SW_ERR_ALLOC if that fails.
+ *  - Threads using distinct streams may call concurrently.
+ */
+#ifndef SCANWEAVER_H
+#define SCANWEAVER_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sw_status {
+  SW_OK = 0,              /* enqueued */
+  SW_ERR_INVALID_ARG = 1, /* NULL / host / misaligned / overlapping pointer, negative size */
+  SW_ERR_UNSUPPORTED = 2, /* a size outside what the kernels handle (e.g. N > 64) */
+  SW_ERR_HIP = 3,         /* a HIP runtime call or launch failed */
+  SW_ERR_ALLOC = 4        /* scratch allocation failed */
+} sw_status;
+
+/* Version of this ABI, major*10000 + minor*100 + patch. */
+int sw_version(void);
+
+/*
+ * Bare affine scan, fp32 (Eq. (3); pairs Eq. (6); composition Eq. (7)).
+ *   a, bx, h_out : (B, D, L) fp32, L fastest.  h_out[b,d,t] is the state
+ *                  after step t, i.e. a[b,d,t]*h_out[b,d,t-1] + bx[b,d,t].
+ *   h0           : (B, D) fp32 initial state h[b,d,-1], or NULL for zero.
+ * Arithmetic is fp32 (the composition is evaluated in an order that differs
+ * from the sequential loop, so results are not bitwise equal to it; they
+ * agree to within the rounding of fp32 affine compositions).
+ */
+int sw_affine_scan(const float* a, const float* bx, const float* h0, float* h_out, int64_t B,
+                   int64_t D, int64_t L);
+
+/*
+ * Bare affine scan in the int32 wraparound ring Z/2^32: the same recurrence
+ * on two's-complement bit patterns with arithmetic modulo 2^32.  The ring is
+ * exact under any association order, so the result is bit-identical to the
+ * sequential loop for every schedule.
+ *   a, bx, h_out : (B, D, L) int32;  h0 : (B, D) int32 or NULL for zero.
+ */
+int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t* h0, int32_t* h_out,
+                       int64_t B, int64_t D, int64_t L);
+
+/*
+ * Fused selective scan, forward, fp32 inputs (the Mamba-style instance of
+ * Eq. (3) that motivates the method, Sec. 1 and Sec. 3.1), zero initial state:
+ *
+ *   a[b,d,t,n]  = exp(delta[b,d,t] * A[d,n])
+ *   u[b,d,t,n]  = delta[b,d,t] * Bm[b,t,n] * x[b,d,t]
+ *   h[b,d,t,n]  = a * h[b,d,t-1,n] + u                 (h[.,-1,.] = 0)
+ *   y[b,d,t]    = sum_n Cm[b,t,n] * h[b,d,t,n] + Dskip[d] * x[b,d,t]
+ *   h_last      = h[b,d,L-1,:]
+ *
+ *   x, delta : (B, D, L) fp32          A      : (D, N) fp32
+ *   Bm, Cm   : (B, L, N) fp32          Dskip  : (D) fp32, or NULL for no skip
+ *   y        : (B, D, L) fp32 output   h_last : (B, D, N) fp32 output or NULL
+ * 1 <= N <= 64, else SW_ERR_UNSUPPORTED.  State and accumulation are fp32.
+ * With L == 0 and B*D > 0, h_last (if given) is set to zero.
+ */
+int sw_selective_scan_fwd(const float* x, const float* delta, const float* A, const float* Bm,
+                          const float* Cm, const float* Dskip, float* y, float* h_last,
+                          int64_t B, int64_t D, int64_t N, int64_t L);
+
+/*
+ * As sw_selective_scan_fwd, with x, delta, Bm and Cm given as bf16 (raw
+ * uint16 bit patterns, widened exactly to fp32 inside the kernel).  A, Dskip,
+ * the state, y and h_last are fp32.
+ */
+int sw_selective_scan_fwd_bf16(const uint16_t* x, const uint16_t* delta, const float* A,
+                               const uint16_t* Bm, const uint16_t* Cm, const float* Dskip,
+                               float* y, float* h_last, int64_t B, int64_t D, int64_t N,
+                               int64_t L);
+
+/* Stream used by the calling thread's subsequent calls (a hipStream_t;
+ * NULL = the null stream).  Always SW_OK. */
+int sw_set_stream(void* hip_stream);
+void* sw_get_stream(void);
+
+/* Static text for a status code; never NULL. */
+const char* sw_status_string(int status);
+
+/* Message for the calling thread's last non-OK return ("" if none). */
+const char* sw_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCANWEAVER_H */

@@ -1,0 +1,117 @@
+"""MI355X-native forward affine scan and fused selective scan.
+
+Thin Python binding over libscanweaver.so (C ABI in include/scanweaver.h).
+Each function only checks and marshals its torch tensors (device, dtype,
+contiguity), hands the current HIP stream to the library and raises on a
+non-OK status; every step of the computation runs in the HIP kernels.
+
+* ``affine_scan(a, bx, h0=None)``: h_t = a_t h_{t-1} + bx_t over the last
+  axis of (B, D, L) fp32 tensors (ScanWeaver Sec. 3.1, Eq. (3)).
+* ``affine_scan_i32(a, bx, h0=None)``: the same in the int32 wraparound ring.
+* ``selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None)``: the Mamba-style
+  fused form, returning ``(y, h_last)``; x/delta/Bm/Cm may be fp32 or bf16.
+"""
+from __future__ import annotations
+
+import torch
+
+from ._lib import ScanWeaverError, check, last_error, lib, status_string  # noqa: F401
+
+__all__ = ["affine_scan", "affine_scan_i32", "selective_scan_fwd", "ScanWeaverError",
+           "version"]
+
+
+def version() -> int:
+    return int(lib().sw_version())
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _need(t, name, dtype, shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a GPU (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+
+
+def _bind_stream(device):
+    lib().sw_set_stream(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _affine(fn, where, dtype, a, bx, h0, out):
+    _need(a, "a", dtype)
+    if a.dim() != 3:
+        raise ValueError("a must have shape (B, D, L)")
+    B, D, L = a.shape
+    _need(bx, "bx", dtype, a.shape)
+    if h0 is not None:
+        _need(h0, "h0", dtype, (B, D))
+    if out is None:
+        out = torch.empty_like(a)
+    else:
+        _need(out, "out", dtype, a.shape)
+    with torch.cuda.device(a.device):
+        _bind_stream(a.device)
+        check(fn(_ptr(a), _ptr(bx), _ptr(h0), _ptr(out), B, D, L), where)
+    return out
+
+
+def affine_scan(a, bx, h0=None, out=None):
+    """Inclusive states of h_t = a_t h_{t-1} + bx_t (fp32, shape (B, D, L))."""
+    return _affine(lib().sw_affine_scan, "sw_affine_scan", torch.float32, a, bx, h0, out)
+
+
+def affine_scan_i32(a, bx, h0=None, out=None):
+    """The recurrence in Z/2^32 on int32 tensors (bit-exact for any schedule)."""
+    return _affine(lib().sw_affine_scan_i32, "sw_affine_scan_i32", torch.int32, a, bx, h0, out)
+
+
+def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
+                       want_h_last=True):
+    """Fused selective scan forward; returns ``(y, h_last)`` (h_last None if not wanted).
+
+    x, delta: (B, D, L); A: (D, N) fp32; Bm, Cm: (B, L, N); Dskip: (D,) fp32 or None.
+    x, delta, Bm, Cm are all fp32 or all bf16; y and h_last are fp32.
+    """
+    if not isinstance(x, torch.Tensor) or x.dim() != 3:
+        raise ValueError("x must be a (B, D, L) tensor")
+    dt = x.dtype
+    if dt not in (torch.float32, torch.bfloat16):
+        raise TypeError("x must be float32 or bfloat16")
+    B, D, L = x.shape
+    _need(x, "x", dt)
+    _need(delta, "delta", dt, (B, D, L))
+    _need(A, "A", torch.float32)
+    if A.dim() != 2 or A.shape[0] != D:
+        raise ValueError("A must have shape (D, N)")
+    N = A.shape[1]
+    _need(Bm, "Bm", dt, (B, L, N))
+    _need(Cm, "Cm", dt, (B, L, N))
+    if Dskip is not None:
+        _need(Dskip, "Dskip", torch.float32, (D,))
+    if y is None:
+        y = torch.empty((B, D, L), dtype=torch.float32, device=x.device)
+    else:
+        _need(y, "y", torch.float32, (B, D, L))
+    if want_h_last:
+        if h_last is None:
+            h_last = torch.empty((B, D, N), dtype=torch.float32, device=x.device)
+        else:
+            _need(h_last, "h_last", torch.float32, (B, D, N))
+    else:
+        h_last = None
+    fn = lib().sw_selective_scan_fwd if dt == torch.float32 else lib().sw_selective_scan_fwd_bf16
+    where = "sw_selective_scan_fwd" if dt == torch.float32 else "sw_selective_scan_fwd_bf16"
+    with torch.cuda.device(x.device):
+        _bind_stream(x.device)
+        check(fn(_ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(y),
+                 _ptr(h_last), B, D, N, L), where)
+    return y, h_last

@@ -1,0 +1,232 @@
+// affine_scan.hip -- bare affine scan h_t = a_t h_{t-1} + bx_t (Eq. (3)) on
+// gfx950, as a prefix scan over the affine pairs of Eq. (6) under the
+// composition of Eq. (7), for fp32 and for the int32 wraparound ring.
+//
+// One workgroup (4 wavefronts, 256 lanes) owns one chunk of K*256 consecutive
+// steps of one (b,d) row:
+//   1. each lane loads K consecutive (a, bx) with 16-byte vector loads
+//      (consecutive lanes read consecutive 16-byte pieces: fully coalesced) and
+//      composes them sequentially into its local inclusive prefixes;
+//   2. the 64 lane totals of a wavefront are scanned with DPP lane moves
+//      (wave_inclusive_scan) and shifted to exclusive prefixes;
+//   3. the four wavefront totals go through LDS and every lane folds the
+//      totals of the wavefronts before it;
+//   4. rows longer than one chunk pass carries between workgroups by
+//      decoupled look-back: a chunk publishes its aggregate pair, walks back
+//      over its predecessors' published aggregates until it meets a published
+//      inclusive state, and then publishes its own inclusive state;
+//   5. every lane rebuilds its states as h = A_pre * h_in + U_pre (Sec. 3.2)
+//      and stores them with 16-byte vector stores.
+// Chunks are handed out through an atomic ticket in chunk-major order (all
+// rows' chunk 0 first), so a chunk only ever waits on chunks that already
+// hold a ticket, which guarantees forward progress.
+#include "sw_internal.h"
+
+namespace sw {
+namespace {
+
+constexpr int AS_THREADS = 256;
+constexpr int AS_WAVES = AS_THREADS / 64;
+
+template <typename T, int K, bool VEC>
+__global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
+    const T* __restrict__ a, const T* __restrict__ bx, const T* __restrict__ h0,
+    T* __restrict__ h, int64_t R, int64_t L, int64_t nchunks, int64_t total,
+    unsigned long long* __restrict__ carry, uint32_t* __restrict__ ticket, uint32_t epoch) {
+  static_assert(K % 4 == 0, "K must be a multiple of 4");
+  constexpr int64_t CH = (int64_t)AS_THREADS * K;
+  using Rg = Ring<T>;
+  __shared__ T sA[AS_WAVES], sU[AS_WAVES];
+  __shared__ T s_hin;
+  __shared__ uint32_t s_id;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const uint32_t st_agg = carry_status(epoch, CARRY_AGG);
+  const uint32_t st_inc = carry_status(epoch, CARRY_INC);
+  int64_t id = blockIdx.x;
+
+  for (;;) {
+    if (nchunks > 1) {
+      if (tid == 0) s_id = atomicAdd(ticket, 1u);
+      __syncthreads();
+      id = s_id;
+    }
+    if (id >= total) break;  // uniform across the workgroup
+    const int64_t c = id / R;
+    const int64_t row = id - c * R;
+    const int64_t t0 = c * CH + (int64_t)tid * K;
+    const T* __restrict__ ar = a + row * L;
+    const T* __restrict__ br = bx + row * L;
+    T* __restrict__ hr = h + row * L;
+
+    // 1. load and local inclusive prefixes
+    T pa[K], pu[K];
+    if (VEC && t0 + K <= L) {
+#pragma unroll
+      for (int q = 0; q < K / 4; ++q) {
+        uint4 va = *reinterpret_cast<const uint4*>(ar + t0 + 4 * q);
+        uint4 vb = *reinterpret_cast<const uint4*>(br + t0 + 4 * q);
+        pa[4 * q + 0] = Rg::from_bits(va.x);
+        pa[4 * q + 1] = Rg::from_bits(va.y);
+        pa[4 * q + 2] = Rg::from_bits(va.z);
+        pa[4 * q + 3] = Rg::from_bits(va.w);
+        pu[4 * q + 0] = Rg::from_bits(vb.x);
+        pu[4 * q + 1] = Rg::from_bits(vb.y);
+        pu[4 * q + 2] = Rg::from_bits(vb.z);
+        pu[4 * q + 3] = Rg::from_bits(vb.w);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const bool ok = t0 + k < L;
+        pa[k] = ok ? ar[t0 + k] : Rg::one();
+        pu[k] = ok ? br[t0 + k] : Rg::zero();
+      }
+    }
+#pragma unroll
+    for (int k = 1; k < K; ++k) absorb_earlier(pa[k], pu[k], pa[k - 1], pu[k - 1]);
+
+    // 2. wavefront scan of the lane totals
+    T wA = pa[K - 1], wU = pu[K - 1];
+    wave_inclusive_scan(wA, wU);
+    if (lane == 63) {
+      sA[wave] = wA;
+      sU[wave] = wU;
+    }
+    wave_shift_exclusive(wA, wU);
+    __syncthreads();
+
+    // 3. fold the totals of earlier wavefronts; chunk total
+    T pA = Rg::one(), pU = Rg::zero();  // prefix of waves before this one
+    T cA = Rg::one(), cU = Rg::zero();  // running chunk total
+#pragma unroll
+    for (int w = 0; w < AS_WAVES; ++w) {
+      if (w == wave) {
+        pA = cA;
+        pU = cU;
+      }
+      T nA = sA[w], nU = sU[w];
+      absorb_earlier(nA, nU, cA, cU);
+      cA = nA;
+      cU = nU;
+    }
+    absorb_earlier(wA, wU, pA, pU);  // lane's exclusive prefix within the chunk
+
+    // 4. carry into the chunk
+    T hin;
+    if (c == 0) {
+      hin = h0 ? h0[row] : Rg::zero();
+      if (nchunks > 1 && tid == 0)
+        carry_put(carry + (row * nchunks) * 3, st_inc, Rg::bits(Rg::mad(cA, hin, cU)));
+    } else {
+      if (tid == 0) {
+        unsigned long long* base = carry + (row * nchunks) * 3;
+        if (c + 1 < nchunks) {
+          carry_put(base + c * 3 + 1, st_agg, Rg::bits(cA));
+          carry_put(base + c * 3 + 2, st_agg, Rg::bits(cU));
+        }
+        T accA = Rg::one(), accU = Rg::zero();
+        int64_t p = c - 1;
+        for (;;) {
+          const unsigned long long wi = carry_get(base + p * 3);
+          if ((uint32_t)(wi >> 32) == st_inc) {
+            hin = Rg::mad(accA, Rg::from_bits((uint32_t)wi), accU);
+            break;
+          }
+          const unsigned long long wa = carry_get(base + p * 3 + 1);
+          const unsigned long long wu = carry_get(base + p * 3 + 2);
+          if ((uint32_t)(wa >> 32) == st_agg && (uint32_t)(wu >> 32) == st_agg) {
+            absorb_earlier(accA, accU, Rg::from_bits((uint32_t)wa), Rg::from_bits((uint32_t)wu));
+            --p;  // chunk 0 always publishes an inclusive state, so p stays >= 0
+            continue;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
+        if (c + 1 < nchunks) carry_put(base + c * 3, st_inc, Rg::bits(Rg::mad(cA, hin, cU)));
+        s_hin = hin;
+      }
+      __syncthreads();
+      hin = s_hin;
+    }
+
+    // 5. rebuild the states and store
+    const T hs = Rg::mad(wA, hin, wU);
+    if (VEC && t0 + K <= L) {
+#pragma unroll
+      for (int q = 0; q < K / 4; ++q) {
+        uint4 o;
+        o.x = Rg::bits(Rg::mad(pa[4 * q + 0], hs, pu[4 * q + 0]));
+        o.y = Rg::bits(Rg::mad(pa[4 * q + 1], hs, pu[4 * q + 1]));
+        o.z = Rg::bits(Rg::mad(pa[4 * q + 2], hs, pu[4 * q + 2]));
+        o.w = Rg::bits(Rg::mad(pa[4 * q + 3], hs, pu[4 * q + 3]));
+        *reinterpret_cast<uint4*>(hr + t0 + 4 * q) = o;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+        if (t0 + k < L) hr[t0 + k] = Rg::mad(pa[k], hs, pu[k]);
+    }
+    if (nchunks <= 1) {
+      id += gridDim.x;
+    }
+    __syncthreads();  // LDS is reused by the next chunk
+  }
+}
+
+constexpr int AS_K = 8;
+
+template <typename T>
+int launch_affine(const T* a, const T* bx, const T* h0, T* h, int64_t R, int64_t L, bool vec) {
+  hipStream_t s = current_stream();
+  constexpr int64_t CH = (int64_t)AS_THREADS * AS_K;
+  const int64_t nchunks = (L + CH - 1) / CH;
+  const int64_t total = R * nchunks;
+  unsigned long long* carry = nullptr;
+  uint32_t* ticket = nullptr;
+  void* ws = nullptr;
+  int64_t grid;
+  if (nchunks > 1) {
+    // carry words (3 per chunk) + one ticket counter, zeroed before the launch
+    const size_t words = (size_t)total * 3;
+    const size_t bytes = words * 8 + 256;
+    int st = scratch_alloc(&ws, bytes, s);
+    if (st != SW_OK) return st;
+    carry = reinterpret_cast<unsigned long long*>(ws);
+    ticket = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + words * 8);
+    st = zero_words(reinterpret_cast<uint32_t*>(ws), bytes / 4, s);
+    if (st != SW_OK) {
+      scratch_free(ws, s);
+      return st;
+    }
+    grid = total < 65536 ? total : 65536;
+  } else {
+    grid = total < 65536 ? total : 65536;
+  }
+  if (vec)
+    hipLaunchKernelGGL((affine_scan_kernel<T, AS_K, true>), dim3((unsigned)grid),
+                       dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L, nchunks, total, carry, ticket,
+                       1u);
+  else
+    hipLaunchKernelGGL((affine_scan_kernel<T, AS_K, false>), dim3((unsigned)grid),
+                       dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L, nchunks, total, carry, ticket,
+                       1u);
+  int st = check_launch("affine_scan_kernel");
+  if (ws) scratch_free(ws, s);
+  return st;
+}
+
+}  // namespace
+
+int affine_scan_f32(const float* a, const float* bx, const float* h0, float* h, int64_t R,
+                    int64_t L, bool vec) {
+  return launch_affine<float>(a, bx, h0, h, R, L, vec);
+}
+
+int affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
+                    int64_t R, int64_t L, bool vec) {
+  return launch_affine<uint32_t>(a, bx, h0, h, R, L, vec);
+}
+
+}  // namespace sw

@@ -1,0 +1,282 @@
+// sw_api.hip -- the C ABI of libscanweaver.so: argument validation, the
+// per-thread stream, error reporting and dispatch to the kernels.
+// Declarations and the full contract are in include/scanweaver.h.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "sw_internal.h"
+
+namespace sw {
+
+int affine_scan_f32(const float* a, const float* bx, const float* h0, float* h, int64_t R,
+                    int64_t L, bool vec);
+int affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
+                    int64_t R, int64_t L, bool vec);
+int selective_fwd_f32(const float* x, const float* delta, const float* A, const float* Bm,
+                      const float* Cm, const float* Dskip, float* y, float* h_last, int64_t B,
+                      int64_t D, int64_t N, int64_t L, bool vec);
+int selective_fwd_bf16(const uint16_t* x, const uint16_t* delta, const float* A,
+                       const uint16_t* Bm, const uint16_t* Cm, const float* Dskip, float* y,
+                       float* h_last, int64_t B, int64_t D, int64_t N, int64_t L, bool vec);
+
+namespace {
+thread_local hipStream_t tls_stream = nullptr;
+thread_local char tls_msg[512] = "";
+std::mutex pool_mu;
+bool pool_ready[64] = {};
+
+__global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) p[i] = 0u;
+}
+
+// ------------------------------------------------------------ validation
+
+struct Span {
+  const void* p;
+  size_t bytes;
+  const char* name;
+};
+
+bool overlaps(const Span& a, const Span& b) {
+  if (!a.p || !b.p || a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a.p, b0 = (uintptr_t)b.p;
+  return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+// Multiply non-negative sizes; false on overflow of int64.
+bool mul_ok(int64_t a, int64_t b, int64_t* out) { return !__builtin_mul_overflow(a, b, out); }
+
+int check_ptr(const void* p, size_t align, const char* name, bool required, int device) {
+  if (!p) {
+    if (required) return fail(SW_ERR_INVALID_ARG, "%s is NULL", name);
+    return SW_OK;
+  }
+  if ((uintptr_t)p % align != 0)
+    return fail(SW_ERR_INVALID_ARG, "%s is not %zu-byte aligned", name, align);
+  hipPointerAttribute_t attr;
+  memset(&attr, 0, sizeof(attr));
+  hipError_t e = hipPointerGetAttributes(&attr, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();  // the query failure is not a sticky launch error
+    return fail(SW_ERR_INVALID_ARG, "%s is not device memory (%s)", name, hipGetErrorString(e));
+  }
+  if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged &&
+      attr.type != hipMemoryTypeUnified)
+    return fail(SW_ERR_INVALID_ARG, "%s is not device memory (memory type %d)", name,
+                (int)attr.type);
+  if (attr.device != device)
+    return fail(SW_ERR_INVALID_ARG, "%s lives on device %d, current device is %d", name,
+                attr.device, device);
+  return SW_OK;
+}
+
+int current_device(int* dev) {
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return fail(SW_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  return SW_OK;
+}
+
+int check_spans(const Span* outs, int nout, const Span* ins, int nin) {
+  for (int i = 0; i < nout; ++i) {
+    for (int j = 0; j < nin; ++j)
+      if (overlaps(outs[i], ins[j]))
+        return fail(SW_ERR_INVALID_ARG, "output %s overlaps input %s", outs[i].name,
+                    ins[j].name);
+    for (int j = i + 1; j < nout; ++j)
+      if (overlaps(outs[i], outs[j]))
+        return fail(SW_ERR_INVALID_ARG, "outputs %s and %s overlap", outs[i].name,
+                    outs[j].name);
+  }
+  return SW_OK;
+}
+
+bool all_aligned16(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (p && (uintptr_t)p % 16 != 0) return false;
+  return true;
+}
+
+template <typename T>
+int affine_common(const T* a, const T* bx, const T* h0, T* h_out, int64_t B, int64_t D,
+                  int64_t L, int (*run)(const T*, const T*, const T*, T*, int64_t, int64_t, bool)) {
+  if (B < 0 || D < 0 || L < 0)
+    return fail(SW_ERR_INVALID_ARG, "negative size (B=%lld D=%lld L=%lld)", (long long)B,
+                (long long)D, (long long)L);
+  int64_t R, n;
+  if (!mul_ok(B, D, &R) || !mul_ok(R, L, &n) || !mul_ok(n, (int64_t)sizeof(T), &n))
+    return fail(SW_ERR_UNSUPPORTED, "B*D*L overflows");
+  if (R == 0 || L == 0) return SW_OK;
+  int dev, st;
+  if ((st = current_device(&dev)) != SW_OK) return st;
+  if ((st = check_ptr(a, sizeof(T), "a", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(bx, sizeof(T), "bx", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(h0, sizeof(T), "h0", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(h_out, sizeof(T), "h_out", true, dev)) != SW_OK) return st;
+  const size_t big = (size_t)n, small = (size_t)R * sizeof(T);
+  Span outs[] = {{h_out, big, "h_out"}};
+  Span ins[] = {{a, big, "a"}, {bx, big, "bx"}, {h0, small, "h0"}};
+  if ((st = check_spans(outs, 1, ins, 3)) != SW_OK) return st;
+  const bool vec = L % 4 == 0 && all_aligned16({a, bx, h_out});
+  return run(a, bx, h0, h_out, R, L, vec);
+}
+
+template <typename IN>
+int selective_common(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
+                     const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int64_t N,
+                     int64_t L,
+                     int (*run)(const IN*, const IN*, const float*, const IN*, const IN*,
+                                const float*, float*, float*, int64_t, int64_t, int64_t, int64_t,
+                                bool)) {
+  if (B < 0 || D < 0 || L < 0 || N < 0)
+    return fail(SW_ERR_INVALID_ARG, "negative size (B=%lld D=%lld N=%lld L=%lld)",
+                (long long)B, (long long)D, (long long)N, (long long)L);
+  if (N < 1 || N > 64) return fail(SW_ERR_UNSUPPORTED, "N=%lld outside [1, 64]", (long long)N);
+  int64_t R, nx, nbc, nh, tmp;
+  if (!mul_ok(B, D, &R) || !mul_ok(R, L, &nx) || !mul_ok(nx, 4, &tmp) || !mul_ok(B, L, &nbc) ||
+      !mul_ok(nbc, N, &nbc) || !mul_ok(nbc, 4, &tmp) || !mul_ok(R, N, &nh))
+    return fail(SW_ERR_UNSUPPORTED, "sizes overflow");
+  if (R == 0) return SW_OK;
+  const int64_t blocks = B * ((D + 31) / 32);
+  if (blocks >= ((int64_t)1 << 24))
+    return fail(SW_ERR_UNSUPPORTED, "B*ceil(D/32)=%lld workgroups exceed the launch limit",
+                (long long)blocks);
+  int dev, st;
+  if ((st = current_device(&dev)) != SW_OK) return st;
+  if (L == 0) {
+    if (!h_last) return SW_OK;
+    if ((st = check_ptr(h_last, 4, "h_last", true, dev)) != SW_OK) return st;
+    return zero_words(reinterpret_cast<uint32_t*>(h_last), (size_t)nh, current_stream());
+  }
+  const size_t es = sizeof(IN);
+  if ((st = check_ptr(x, es, "x", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(delta, es, "delta", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(A, 4, "A", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(Bm, es, "Bm", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(Cm, es, "Cm", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(Dskip, 4, "Dskip", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(y, 4, "y", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(h_last, 4, "h_last", false, dev)) != SW_OK) return st;
+  Span outs[] = {{y, (size_t)nx * 4, "y"}, {h_last, (size_t)nh * 4, "h_last"}};
+  Span ins[] = {{x, (size_t)nx * es, "x"},          {delta, (size_t)nx * es, "delta"},
+                {A, (size_t)(D * N) * 4, "A"},      {Bm, (size_t)nbc * es, "Bm"},
+                {Cm, (size_t)nbc * es, "Cm"},       {Dskip, (size_t)D * 4, "Dskip"}};
+  if ((st = check_spans(outs, 2, ins, 6)) != SW_OK) return st;
+  const bool vec = L % 4 == 0 && all_aligned16({x, delta, y});
+  return run(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, vec);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------ host helpers
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(tls_msg, sizeof(tls_msg), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+hipStream_t current_stream() { return tls_stream; }
+
+int check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(SW_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return SW_OK;
+}
+
+int scratch_alloc(void** p, size_t bytes, hipStream_t s) {
+  int dev = 0;
+  if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
+    std::lock_guard<std::mutex> lk(pool_mu);
+    if (!pool_ready[dev]) {
+      // keep freed scratch in the pool instead of returning it at every sync
+      hipMemPool_t pool;
+      if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+        uint64_t keep = UINT64_MAX;
+        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+      }
+      (void)hipGetLastError();
+      pool_ready[dev] = true;
+    }
+  }
+  hipError_t e = hipMallocAsync(p, bytes, s);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(SW_ERR_ALLOC, "hipMallocAsync(%zu bytes): %s", bytes, hipGetErrorString(e));
+  }
+  return SW_OK;
+}
+
+void scratch_free(void* p, hipStream_t s) {
+  if (p) (void)hipFreeAsync(p, s);
+}
+
+int zero_words(uint32_t* p, size_t words, hipStream_t s) {
+  if (words == 0) return SW_OK;
+  size_t blocks = (words + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, words);
+  return check_launch("fill_zero_kernel");
+}
+
+}  // namespace sw
+
+// ------------------------------------------------------------------ C ABI
+
+SW_API int sw_version(void) { return 100; }
+
+SW_API int sw_affine_scan(const float* a, const float* bx, const float* h0, float* h_out,
+                          int64_t B, int64_t D, int64_t L) {
+  return sw::affine_common<float>(a, bx, h0, h_out, B, D, L, sw::affine_scan_f32);
+}
+
+SW_API int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t* h0,
+                              int32_t* h_out, int64_t B, int64_t D, int64_t L) {
+  return sw::affine_common<uint32_t>(reinterpret_cast<const uint32_t*>(a),
+                                     reinterpret_cast<const uint32_t*>(bx),
+                                     reinterpret_cast<const uint32_t*>(h0),
+                                     reinterpret_cast<uint32_t*>(h_out), B, D, L,
+                                     sw::affine_scan_u32);
+}
+
+SW_API int sw_selective_scan_fwd(const float* x, const float* delta, const float* A,
+                                 const float* Bm, const float* Cm, const float* Dskip, float* y,
+                                 float* h_last, int64_t B, int64_t D, int64_t N, int64_t L) {
+  return sw::selective_common<float>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L,
+                                     sw::selective_fwd_f32);
+}
+
+SW_API int sw_selective_scan_fwd_bf16(const uint16_t* x, const uint16_t* delta, const float* A,
+                                      const uint16_t* Bm, const uint16_t* Cm, const float* Dskip,
+                                      float* y, float* h_last, int64_t B, int64_t D, int64_t N,
+                                      int64_t L) {
+  return sw::selective_common<uint16_t>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L,
+                                        sw::selective_fwd_bf16);
+}
+
+SW_API int sw_set_stream(void* hip_stream) {
+  sw::tls_stream = reinterpret_cast<hipStream_t>(hip_stream);
+  return SW_OK;
+}
+
+SW_API void* sw_get_stream(void) { return reinterpret_cast<void*>(sw::tls_stream); }
+
+SW_API const char* sw_status_string(int status) {
+  switch (status) {
+    case SW_OK: return "SW_OK";
+    case SW_ERR_INVALID_ARG: return "SW_ERR_INVALID_ARG";
+    case SW_ERR_UNSUPPORTED: return "SW_ERR_UNSUPPORTED";
+    case SW_ERR_HIP: return "SW_ERR_HIP";
+    case SW_ERR_ALLOC: return "SW_ERR_ALLOC";
+    default: return "SW_ERR_UNKNOWN";
+  }
+}
+
+SW_API const char* sw_last_error(void) { return sw::tls_msg; }

@@ -1,0 +1,142 @@
+// sw_internal.h -- shared host/device helpers of libscanweaver (not installed).
+//
+// Holds: error bookkeeping and the per-thread stream of the C ABI, the exact
+// bf16 -> fp32 widening, the affine-pair arithmetic of Eq. (7) for fp32 and
+// for Z/2^32, the wavefront-level inclusive scan of pairs built on DPP, and
+// the status words used to pass chunk carries between workgroups.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "scanweaver.h"
+
+#define SW_API extern "C" __attribute__((visibility("default")))
+
+namespace sw {
+
+// ---------------------------------------------------------------- host side
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+hipStream_t current_stream();
+int check_launch(const char* what);  // hipGetLastError -> SW_ERR_HIP with a message
+
+// Scratch from the device's stream-ordered pool (released on the same stream).
+int scratch_alloc(void** p, size_t bytes, hipStream_t s);
+void scratch_free(void* p, hipStream_t s);
+// Zero `words` 32-bit words with a plain kernel (no memset node).
+int zero_words(uint32_t* p, size_t words, hipStream_t s);
+
+// ---------------------------------------------------------------- device side
+
+// bf16 bits -> fp32, exact.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_one(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// Affine-pair arithmetic.  combine(later, earlier) is Eq. (7):
+//   (A2,U2) (+) (A1,U1) = (A2*A1, A2*U1 + U2).
+template <typename T>
+struct Ring;
+
+template <>
+struct Ring<float> {
+  static constexpr float one() { return 1.0f; }
+  static constexpr float zero() { return 0.0f; }
+  static __device__ __forceinline__ float mul(float a, float b) { return a * b; }
+  static __device__ __forceinline__ float mad(float a, float b, float c) {
+    return __builtin_fmaf(a, b, c);
+  }
+  static __device__ __forceinline__ uint32_t bits(float v) { return __float_as_uint(v); }
+  static __device__ __forceinline__ float from_bits(uint32_t v) { return __uint_as_float(v); }
+};
+
+template <>
+struct Ring<uint32_t> {
+  static constexpr uint32_t one() { return 1u; }
+  static constexpr uint32_t zero() { return 0u; }
+  static __device__ __forceinline__ uint32_t mul(uint32_t a, uint32_t b) { return a * b; }
+  static __device__ __forceinline__ uint32_t mad(uint32_t a, uint32_t b, uint32_t c) {
+    return a * b + c;  // unsigned: wraps modulo 2^32
+  }
+  static __device__ __forceinline__ uint32_t bits(uint32_t v) { return v; }
+  static __device__ __forceinline__ uint32_t from_bits(uint32_t v) { return v; }
+};
+
+// (A,U) <- (A,U) (+) (Ap,Up)   where (Ap,Up) is the earlier segment.
+template <typename T>
+__device__ __forceinline__ void absorb_earlier(T& A, T& U, T Ap, T Up) {
+  U = Ring<T>::mad(A, Up, U);
+  A = Ring<T>::mul(A, Ap);
+}
+
+// DPP controls (GFX9 encoding).
+enum : int {
+  DPP_ROW_SHR1 = 0x111,
+  DPP_ROW_SHR2 = 0x112,
+  DPP_ROW_SHR4 = 0x114,
+  DPP_ROW_SHR8 = 0x118,
+  DPP_WAVE_SHR1 = 0x138,
+  DPP_ROW_BCAST15 = 0x142,
+  DPP_ROW_BCAST31 = 0x143,
+};
+
+// Move `v` across lanes with DPP; lanes without a valid source, or outside
+// row_mask, receive `ident`.
+template <int CTRL, int ROW_MASK, typename T>
+__device__ __forceinline__ T dpp_or(T v, T ident) {
+  uint32_t r = (uint32_t)__builtin_amdgcn_update_dpp((int)Ring<T>::bits(ident),
+                                                     (int)Ring<T>::bits(v), CTRL, ROW_MASK, 0xf,
+                                                     false);
+  return Ring<T>::from_bits(r);
+}
+
+template <int CTRL, int ROW_MASK, typename T>
+__device__ __forceinline__ void scan_step(T& A, T& U) {
+  T Ap = dpp_or<CTRL, ROW_MASK>(A, Ring<T>::one());
+  T Up = dpp_or<CTRL, ROW_MASK>(U, Ring<T>::zero());
+  absorb_earlier(A, U, Ap, Up);
+}
+
+// Inclusive scan of one affine pair per lane across the 64 lanes of a
+// wavefront (lane i ends with p_i (+) ... (+) p_0).  Kogge-Stone within each
+// 16-lane row (shifts 1, 2, 4, 8), then the row carries via row_bcast:15 and
+// row_bcast:31.  Lanes with no source keep the identity pair (1, 0).
+template <typename T>
+__device__ __forceinline__ void wave_inclusive_scan(T& A, T& U) {
+  scan_step<DPP_ROW_SHR1, 0xf>(A, U);
+  scan_step<DPP_ROW_SHR2, 0xf>(A, U);
+  scan_step<DPP_ROW_SHR4, 0xf>(A, U);
+  scan_step<DPP_ROW_SHR8, 0xf>(A, U);
+  scan_step<DPP_ROW_BCAST15, 0xa>(A, U);
+  scan_step<DPP_ROW_BCAST31, 0xc>(A, U);
+}
+
+// Inclusive -> exclusive: lane i receives lane i-1's pair, lane 0 the identity.
+template <typename T>
+__device__ __forceinline__ void wave_shift_exclusive(T& A, T& U) {
+  A = dpp_or<DPP_WAVE_SHR1, 0xf>(A, Ring<T>::one());
+  U = dpp_or<DPP_WAVE_SHR1, 0xf>(U, Ring<T>::zero());
+}
+
+// ------------------------------------------------------------- carry words
+// A carry word is 64 bits: status in the high half, a 32-bit payload in the
+// low half, written and read with single relaxed device-scope atomics, so a
+// reader either sees the whole word or the previous one.  Status encodes an
+// epoch and a kind; the scratch is zeroed before each launch (epoch 1).
+enum : uint32_t { CARRY_EMPTY = 0, CARRY_AGG = 1, CARRY_INC = 2 };
+
+__device__ __forceinline__ uint32_t carry_status(uint32_t epoch, uint32_t kind) {
+  return (epoch << 2) | kind;
+}
+
+__device__ __forceinline__ void carry_put(unsigned long long* w, uint32_t status, uint32_t payload) {
+  unsigned long long v = ((unsigned long long)status << 32) | payload;
+  __hip_atomic_store(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ unsigned long long carry_get(const unsigned long long* w) {
+  return __hip_atomic_load(const_cast<unsigned long long*>(w), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+}  // namespace sw

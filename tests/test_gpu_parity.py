@@ -1,0 +1,254 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Integer results must be bit-exact; fp32 results pass the gate of gate.py.
+Small cases are compared element by element over whole outputs, at sizes that
+span several workgroup tiles and a ragged tail; the full-size synthetic
+workloads are run at their real shapes in the launch configuration the bench
+uses and compared on seeded samples of rows that the oracle evaluates one by
+one.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from gate import assert_gate, fp_gate, rownorm_rel
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def sw():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_00601_amd as pkg
+    pkg.lib()  # raises if the HIP library is missing: no fallback
+    return pkg
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def bf16_dev(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to("cuda").view(
+        torch.bfloat16)
+
+
+# ------------------------------------------------------------ bare affine scan
+
+def _affine_check(sw, a, bx, h0=None):
+    h = sw.affine_scan(dev(a), dev(bx), None if h0 is None else dev(h0)).cpu().numpy()
+    ref, mag, sens = oracle.affine_scan(a, bx, h0, bounds=True)
+    return fp_gate(h, ref, mag, sens), h, ref
+
+
+def test_affine_f32_workload(sw):
+    w = wl.workload("affine_f32_b1_d64_l1024")
+    _say("case", w.name)
+    inp = w.inputs()
+    st, h, ref = _affine_check(sw, inp["a"], inp["bx"])
+    assert_gate(st, w.name)
+    assert st["n_ill"] == 0
+    assert rownorm_rel(h, ref) <= 1e-4
+
+
+@pytest.mark.parametrize("variant", ["uniform", "odd", "h0"])
+def test_affine_i32_workload_bitexact(sw, variant):
+    _say("case affine i32", variant)
+    inp = wl.affine_inputs_i32(1, 64, 1024, wl.INT_SEEDS[variant], variant)
+    h = sw.affine_scan_i32(dev(inp["a"]), dev(inp["bx"]),
+                           None if inp["h0"] is None else dev(inp["h0"])).cpu().numpy()
+    assert np.array_equal(h, oracle.affine_scan_i32(inp["a"], inp["bx"], inp["h0"]))
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 63, 64, 65, 2047, 2048, 2049, 4097, 10007, 65536,
+                               100003])
+def test_affine_i32_ragged_and_multichunk_bitexact(sw, L):
+    _say("case affine i32 L", L)
+    inp = wl.affine_inputs_i32(2, 3, L, 1000 + L, "odd")
+    h0 = wl.affine_inputs_i32(2, 3, 1, 2000 + L, "h0")["h0"]
+    h = sw.affine_scan_i32(dev(inp["a"]), dev(inp["bx"]), dev(h0)).cpu().numpy()
+    assert np.array_equal(h, oracle.affine_scan_i32(inp["a"], inp["bx"], h0))
+
+
+def test_affine_i32_long_single_row_repeatable(sw):
+    """One long row: every chunk carry crosses workgroups by look-back.  The
+    ring is exact, so any lost or misordered carry shows as a bit difference;
+    20 repeats must agree bit for bit."""
+    _say("case affine i32 long row repeat")
+    inp = wl.affine_inputs_i32(1, 1, 1 << 21, 77, "odd")
+    a, bx = dev(inp["a"]), dev(inp["bx"])
+    ref = oracle.affine_scan_i32(inp["a"], inp["bx"])
+    first = sw.affine_scan_i32(a, bx)
+    assert np.array_equal(first.cpu().numpy(), ref)
+    for _ in range(20):
+        assert torch.equal(sw.affine_scan_i32(a, bx), first)
+
+
+@pytest.mark.parametrize("B,D,L", [(1, 1, 1), (2, 3, 5), (1, 4, 2049), (3, 5, 6151),
+                                   (1, 2, 100001), (2, 2, 65536)])
+def test_affine_f32_ragged(sw, B, D, L):
+    _say("case affine f32", B, D, L)
+    inp = wl.affine_inputs(B, D, L, 3000 + L, with_h0=True)
+    st, _, _ = _affine_check(sw, inp["a"], inp["bx"], inp["h0"])
+    assert_gate(st, f"affine f32 {B}x{D}x{L}")
+
+
+def test_affine_weighted_prefix(sw):
+    """Sec. 6.6, Eq. (10): h_t = alpha_t h_{t-1} + beta_t through the same scan
+    (alpha -> a, beta -> b with x = 1)."""
+    rng = np.random.Generator(np.random.PCG64(66))
+    alpha = rng.uniform(0.0, 1.0, size=(2, 7, 3000)).astype(np.float32)
+    beta = rng.uniform(0.0, 1.0, size=(2, 7, 3000)).astype(np.float32)
+    st, _, _ = _affine_check(sw, alpha, beta)
+    assert_gate(st, "weighted prefix")
+
+
+def test_affine_empty(sw):
+    e = torch.empty((2, 3, 0), device="cuda")
+    assert sw.affine_scan(e, e).shape == (2, 3, 0)
+    e = torch.empty((0, 3, 5), device="cuda")
+    assert sw.affine_scan(e, e).shape == (0, 3, 5)
+
+
+# ------------------------------------------------------------ fused selective scan
+
+def _run_selective(sw, inp, dtype, with_dskip=True, want_h_last=True):
+    if dtype == "bf16":
+        x, dl = bf16_dev(inp["x_bf16"]), bf16_dev(inp["delta_bf16"])
+        Bm, Cm = bf16_dev(inp["Bm_bf16"]), bf16_dev(inp["Cm_bf16"])
+    else:
+        x, dl, Bm, Cm = dev(inp["x"]), dev(inp["delta"]), dev(inp["Bm"]), dev(inp["Cm"])
+    Dk = dev(inp["Dskip"]) if with_dskip else None
+    y, hl = sw.selective_scan_fwd(x, dl, dev(inp["A"]), Bm, Cm, Dk, want_h_last=want_h_last)
+    torch.cuda.synchronize()
+    return y, hl
+
+
+def _selective_check(sw, inp, dtype, rows=None, with_dskip=True):
+    y, hl = _run_selective(sw, inp, dtype, with_dskip)
+    Bsz, D, L = inp["x"].shape
+    N = inp["A"].shape[1]
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                              inp["Dskip"] if with_dskip else None, rows=rows, bounds=True)
+    if rows is None:
+        yg, hg = y.cpu().numpy(), hl.cpu().numpy()
+    else:
+        ridx = torch.as_tensor(np.asarray(rows), device="cuda")
+        yg = y.reshape(Bsz * D, L).index_select(0, ridx).cpu().numpy()
+        hg = hl.reshape(Bsz * D, N).index_select(0, ridx).cpu().numpy()
+    sy = fp_gate(yg, o["y"], o["y_mag"], o["y_sens"])
+    sh = fp_gate(hg, o["h_last"], o["h_mag"], o["h_sens"])
+    return sy, sh, yg, o, y
+
+
+@pytest.mark.parametrize("B,D,N,L", [(1, 1, 1, 1), (2, 70, 16, 200), (1, 33, 3, 37),
+                                     (3, 31, 8, 64), (1, 40, 17, 33), (2, 9, 32, 129),
+                                     (1, 5, 64, 100), (2, 64, 16, 31), (1, 3, 16, 5000)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_selective_small_full_compare(sw, B, D, N, L, dtype):
+    _say("case selective", dtype, B, D, N, L)
+    inp = wl.selective_inputs(B, D, N, L, 4000 + B * 7 + D * 13 + N * 17 + L, dtype)
+    sy, sh, yg, o, _ = _selective_check(sw, inp, dtype)
+    assert_gate(sy, f"y {dtype} {B}x{D}x{N}x{L}")
+    assert_gate(sh, f"h_last {dtype} {B}x{D}x{N}x{L}")
+    assert rownorm_rel(yg, o["y"]) <= 1e-4
+
+
+def test_selective_no_dskip_no_hlast(sw):
+    inp = wl.selective_inputs(2, 40, 16, 77, 4999, "f32")
+    y, hl = _run_selective(sw, inp, "f32", with_dskip=False, want_h_last=False)
+    assert hl is None
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"], None,
+                              bounds=True)
+    assert_gate(fp_gate(y.cpu().numpy(), o["y"], o["y_mag"], o["y_sens"]), "no dskip")
+
+
+def test_selective_L0_zeroes_h_last(sw):
+    x = torch.empty((2, 3, 0), device="cuda")
+    A = torch.randn((3, 16), device="cuda")
+    Bm = torch.empty((2, 0, 16), device="cuda")
+    hl = torch.full((2, 3, 16), 7.0, device="cuda")
+    y, hl2 = sw.selective_scan_fwd(x, x, A, Bm, Bm, None, h_last=hl)
+    torch.cuda.synchronize()
+    assert y.shape == (2, 3, 0) and torch.all(hl2 == 0)
+
+
+def test_selective_reduces_to_bare_scan(sw):
+    """N=1, C=1, Dskip=0: y is the state itself, so the fused kernel must agree
+    with the bare scan on a = exp(delta*A), bx = delta*B*x (oracle-checked)."""
+    rng = np.random.Generator(np.random.PCG64(5150))
+    B, D, L = 2, 37, 999
+    inp = wl.selective_inputs(B, D, 1, L, 5151, "f32")
+    inp["Cm"] = np.ones_like(inp["Cm"])
+    inp["Dskip"] = np.zeros_like(inp["Dskip"])
+    y, _ = _run_selective(sw, inp, "f32")
+    a = np.exp(inp["delta"].astype(np.float64) * inp["A"][None, :, :1]).astype(np.float32)
+    bx = (inp["delta"].astype(np.float64) * inp["x"] * inp["Bm"][:, None, :, 0]).astype(
+        np.float32)
+    h, mag, sens = oracle.affine_scan(a, bx, bounds=True)
+    # a and bx are rounded to fp32 here, so allow the rounding of those inputs too
+    st = fp_gate(y.cpu().numpy(), h, mag, sens, rel=2e-4)
+    assert_gate(st, "fused vs bare")
+    del rng
+
+
+# ------------------------------------------------------------ full-size workloads
+
+def _sample_rows(n_rows, k, seed):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    pick = rng.choice(n_rows, size=min(k, n_rows), replace=False)
+    # always include the first and last row (edges of the row tiling)
+    return np.unique(np.concatenate([pick, [0, n_rows - 1]])).astype(np.int64)
+
+
+@pytest.mark.parametrize("name,k", [("selective_f32_b2_d256_n16_l512", None),
+                                    ("selective_bf16_b8_d1536_n16_l2048", 768),
+                                    ("selective_f32_b1_d5120_n16_l65536", 48),
+                                    ("selective_f32_b4_d2048_n16_l8192_stress", 384)])
+def test_selective_workloads(sw, name, k):
+    w = wl.workload(name)
+    _say("case", name)
+    inp = w.inputs()
+    rows = None if k is None else _sample_rows(w.B * w.D, k, 99)
+    sy, sh, yg, o, y = _selective_check(sw, inp, w.dtype, rows=rows)
+    _say("  y:", {k_: v for k_, v in sy.items() if k_ != "first_bad"})
+    _say("  h_last:", {k_: v for k_, v in sh.items() if k_ != "first_bad"})
+    assert_gate(sy, name + " y")
+    assert_gate(sh, name + " h_last")
+    assert bool(torch.isfinite(y).all())
+    if not w.stress:
+        assert sy["n_ill"] == 0
+        assert rownorm_rel(yg, o["y"]) <= 1e-4
+
+
+# ------------------------------------------------------------ ABI error paths on the GPU
+
+def test_abi_rejects_bad_pointers(sw):
+    lib = sw.lib()
+    a = torch.zeros((1, 2, 8), device="cuda")
+    h = torch.zeros((1, 2, 8), device="cuda")
+    host = np.zeros(16, np.float32)
+    rc = lib.sw_affine_scan(host.ctypes.data, a.data_ptr(), None, h.data_ptr(), 1, 2, 8)
+    assert rc == 1 and "device memory" in sw.last_error()
+    rc = lib.sw_affine_scan(a.data_ptr() + 2, a.data_ptr(), None, h.data_ptr(), 1, 2, 8)
+    assert rc == 1 and "aligned" in sw.last_error()
+    rc = lib.sw_affine_scan(a.data_ptr(), a.data_ptr(), None, a.data_ptr() + 16, 1, 2, 8)
+    assert rc == 1 and "overlaps" in sw.last_error()
+    rc = lib.sw_affine_scan(a.data_ptr(), a.data_ptr(), None, None, 1, 2, 8)
+    assert rc == 1
+    assert torch.all(h == 0)  # nothing was written
+    x = torch.zeros((1, 2, 8), device="cuda")
+    A = torch.zeros((2, 65), device="cuda")
+    rc = lib.sw_selective_scan_fwd(x.data_ptr(), x.data_ptr(), A.data_ptr(), x.data_ptr(),
+                                   x.data_ptr(), None, h.data_ptr(), None, 1, 2, 65, 8)
+    assert rc == 2
