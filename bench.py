@@ -1,0 +1,207 @@
+"""Benchmark of the fused selective scan forward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+
+One step is one call of the fused selective scan (every step of the hot path:
+bf16 widening, exp discretisation, the recurrence, the C contraction, the
+D skip and the h_last write) over one batch of synthetic input that is already
+resident in HBM.  Several input sets are rotated so that the working set is
+larger than the 256 MB MALL and each step streams its inputs from HBM.
+
+Prints one JSON line: throughput in B*L*D*N elements/s over exactly K timed
+steps, the roofline of the kernel (per-launch duration from HIP events on the
+launch stream), the HBM bandwidth it reaches, and the CPU oracle timed on the
+host cores over a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads as wl  # noqa: E402
+
+DEFAULT_WORKLOAD = "selective_bf16_b8_d1536_n16_l2048"
+
+# MI355X figures used for the roofline
+HBM_PEAK_GBS = 8000.0            # HBM3E, 8 TB/s
+N_CU, SIMD_PER_CU, LANES_PER_SIMD, CLOCK_HZ = 256, 4, 16, 2.4e9
+# fp32 VALU issue peak without packed math: lane-instructions per second
+VALU_PEAK = N_CU * SIMD_PER_CU * LANES_PER_SIMD * CLOCK_HZ  # 3.93e13
+# issue slots the method needs per (b,d,t,n) element: delta*A' mul, exp2
+# (half rate: 2 slots), (delta*x)*B mul, state FMA, C FMA
+SLOTS_PER_ELEM = 6.0
+MALL_BYTES = 256 << 20
+
+
+def algorithmic_bytes(w) -> int:
+    """Each input read once, each output written once (fp32 y and h_last)."""
+    es = 2 if w.dtype == "bf16" else 4
+    x_dl = 2 * w.B * w.D * w.L * es
+    bc = 2 * w.B * w.L * w.N * es
+    a_d = w.D * w.N * 4 + w.D * 4
+    out = w.B * w.D * w.L * 4 + w.B * w.D * w.N * 4
+    return x_dl + bc + a_d + out
+
+
+def cpu_baseline(w, inp, target_s: float = 12.0, max_rows: int | None = None):
+    """Time the fp64 oracle (as it stands) on all host cores over a sample of rows."""
+    import oracle
+    cores = len(os.sched_getaffinity(0))
+    R = w.B * w.D
+    rows = 64
+
+    def run(nrows):
+        # rows 0..nrows-1 of the flattened (B*D) rows: a contiguous prefix
+        b_hi = (nrows + w.D - 1) // w.D
+        x = inp["x"][:b_hi].reshape(-1, w.L)[:nrows]
+        dl = inp["delta"][:b_hi].reshape(-1, w.L)[:nrows]
+        # present the sample as (1, nrows, L) rows of batch 0 when it lies in batch 0
+        if nrows <= w.D:
+            args = (x[None], dl[None], inp["A"][:nrows], inp["Bm"][:1], inp["Cm"][:1],
+                    inp["Dskip"][:nrows])
+            t = time.perf_counter()
+            oracle.selective_scan(*args, threads=cores)
+            return time.perf_counter() - t
+        ridx = np.arange(nrows)
+        t = time.perf_counter()
+        oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                              inp["Dskip"], rows=ridx, threads=cores)
+        return time.perf_counter() - t
+
+    dt = run(rows)
+    while dt < target_s / 4 and rows < R and (max_rows is None or rows < max_rows):
+        rows = min(R, rows * 4, max_rows or R)
+        dt = run(rows)
+    elems = rows * w.L * w.N
+    import oracle as _o
+    return {
+        "value": elems / dt, "unit": "elems/s", "cores": _o.threads_used(cores, rows),
+        "kind": "oracle",
+        "sample": f"{rows} of {R} (b,d) rows x L={w.L} x N={w.N} of {w.name}, fp64, "
+                  f"{dt:.1f} s wall",
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(wl.WORKLOADS))
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--sets", type=int, default=0,
+                    help="input sets rotated through (default: enough to exceed the MALL)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(rows shard across GPUs without communication; see the design notes).",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2606_00601_amd as sw
+    w = wl.workload(args.workload)
+    if w.path != "selective":
+        raise SystemExit("bench.py times the fused selective scan workloads")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sw.lib()  # the HIP library must be present: no fallback
+
+    inp = w.inputs()
+    abytes = algorithmic_bytes(w)
+    nsets = args.sets or max(2, int(np.ceil(2 * MALL_BYTES / abytes)) + 1)
+    nsets = min(nsets, 8)
+
+    def to_dev(k):
+        if w.dtype == "bf16" and k in ("x", "delta", "Bm", "Cm"):
+            return torch.from_numpy(inp[k + "_bf16"].view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(inp[k]).to(dev)
+
+    base = {k: to_dev(k) for k in ("x", "delta", "A", "Bm", "Cm", "Dskip")}
+    sets = []
+    for i in range(nsets):
+        s = {k: (v if i == 0 else v.clone()) for k, v in base.items()}
+        s["y"] = torch.empty((w.B, w.D, w.L), dtype=torch.float32, device=dev)
+        s["h"] = torch.empty((w.B, w.D, w.N), dtype=torch.float32, device=dev)
+        sets.append(s)
+    torch.cuda.synchronize()
+
+    def step(i):
+        s = sets[i % nsets]
+        sw.selective_scan_fwd(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"], s["Dskip"],
+                              y=s["y"], h_last=s["h"])
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream(dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([a.elapsed_time(b) * 1e-3 for a, b in ev])  # seconds per launch
+
+    elems = w.elems
+    value = elems * args.steps / wall
+    kern = float(per.mean())
+    hbm_gbs = abytes / kern / 1e9
+    alu_achieved = SLOTS_PER_ELEM * elems / kern
+    out = {
+        "metric": "selective-scan fwd B*L*D*N elems/s (+ achieved HBM GB/s vs peak), 1 GPU",
+        "value": value,
+        "unit": "elems/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "B": w.B, "D": w.D, "N": w.N, "L": w.L,
+            "inputs": ("bf16 x/delta/Bm/Cm, fp32 A/Dskip" if w.dtype == "bf16" else "fp32"),
+            "state_and_output": "fp32", "input_sets_rotated": nsets,
+        },
+        "roofline": {
+            "bound": "alu",
+            "achieved": alu_achieved / 1e12,
+            "peak": VALU_PEAK / 1e12,
+            "unit": "TVALU-slot/s",
+            "frac": alu_achieved / VALU_PEAK,
+            "traffic": None,
+            "kernel": "selective_fwd_kernel",
+            "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
+                              "median": float(np.median(per)) * 1e6},
+            "slots_per_elem": SLOTS_PER_ELEM,
+        },
+        "hbm": {"algorithmic_bytes": abytes, "achieved_GBs": hbm_gbs, "peak_GBs": HBM_PEAK_GBS,
+                "frac": hbm_gbs / HBM_PEAK_GBS},
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(w, inp)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -32,7 +32,8 @@ template <typename T, int K, bool VEC>
 __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
     const T* __restrict__ a, const T* __restrict__ bx, const T* __restrict__ h0,
     T* __restrict__ h, int64_t R, int64_t L, int64_t nchunks, int64_t total,
-    unsigned long long* __restrict__ carry, uint32_t* __restrict__ ticket, uint32_t epoch) {
+    unsigned long long* __restrict__ carry, uint32_t* __restrict__ ticket, uint32_t tbase,
+    uint32_t epoch) {
   static_assert(K % 4 == 0, "K must be a multiple of 4");
   constexpr int64_t CH = (int64_t)AS_THREADS * K;
   using Rg = Ring<T>;
@@ -49,7 +50,7 @@ __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
 
   for (;;) {
     if (nchunks > 1) {
-      if (tid == 0) s_id = atomicAdd(ticket, 1u);
+      if (tid == 0) s_id = atomicAdd(ticket, 1u) - tbase;
       __syncthreads();
       id = s_id;
     }
@@ -183,37 +184,25 @@ int launch_affine(const T* a, const T* bx, const T* h0, T* h, int64_t R, int64_t
   constexpr int64_t CH = (int64_t)AS_THREADS * AS_K;
   const int64_t nchunks = (L + CH - 1) / CH;
   const int64_t total = R * nchunks;
-  unsigned long long* carry = nullptr;
-  uint32_t* ticket = nullptr;
-  void* ws = nullptr;
-  int64_t grid;
+  const int64_t grid = total < 65536 ? total : 65536;
+  ScratchSession ss;
   if (nchunks > 1) {
-    // carry words (3 per chunk) + one ticket counter, zeroed before the launch
-    const size_t words = (size_t)total * 3;
-    const size_t bytes = words * 8 + 256;
-    int st = scratch_alloc(&ws, bytes, s);
+    if (total >= ((int64_t)1 << 31))
+      return fail(SW_ERR_UNSUPPORTED, "%lld chunks exceed the ticket range", (long long)total);
+    // 3 carry words per chunk; every workgroup takes one ticket past the end
+    int st = ss.reserve((size_t)total * 3, (uint32_t)(total + grid), s);
     if (st != SW_OK) return st;
-    carry = reinterpret_cast<unsigned long long*>(ws);
-    ticket = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + words * 8);
-    st = zero_words(reinterpret_cast<uint32_t*>(ws), bytes / 4, s);
-    if (st != SW_OK) {
-      scratch_free(ws, s);
-      return st;
-    }
-    grid = total < 65536 ? total : 65536;
-  } else {
-    grid = total < 65536 ? total : 65536;
   }
   if (vec)
     hipLaunchKernelGGL((affine_scan_kernel<T, AS_K, true>), dim3((unsigned)grid),
-                       dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L, nchunks, total, carry, ticket,
-                       1u);
+                       dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L, nchunks, total, ss.carry,
+                       ss.ticket, ss.ticket_base, ss.epoch);
   else
     hipLaunchKernelGGL((affine_scan_kernel<T, AS_K, false>), dim3((unsigned)grid),
-                       dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L, nchunks, total, carry, ticket,
-                       1u);
+                       dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L, nchunks, total, ss.carry,
+                       ss.ticket, ss.ticket_base, ss.epoch);
   int st = check_launch("affine_scan_kernel");
-  if (ws) scratch_free(ws, s);
+  if (st != SW_OK) ss.invalidate();
   return st;
 }
 

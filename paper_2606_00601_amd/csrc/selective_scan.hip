@@ -4,243 +4,436 @@
 //   a_{t,n} = exp(delta_t A_n),  u_{t,n} = delta_t B_{t,n} x_t,
 //   h_{t,n} = a_{t,n} h_{t-1,n} + u_{t,n}                       Eq. (3)
 //   y_t     = sum_n C_{t,n} h_{t,n} + Dskip x_t
-// computed as a sequential traversal over t of the independent (b,d,n)
-// recurrences, which reconstructs the same states as any associative
-// evaluation of Eq. (6)-(7) (Sec. 3.2).
+// evaluated as a sequential traversal over t of the independent (b,d,n)
+// recurrences inside each chunk of the sequence; chunks of a row are chained
+// through the exact inclusive state (the Eq. (7) composition of the chunk
+// with its carry, Sec. 3.2), so the result is the sequential one.
 //
 // Work per (b,d,t,n) is one exp2 plus four fp32 VALU operations against about
-// half a byte of HBM traffic, so the kernel is bound by the VALU issue rate,
-// not by HBM.  The layout is chosen to spend as few VALU slots per element
-// as possible:
-//   * G = 8 lanes share one (b,d) row, each lane owning NPL = N/8 states, so
-//     a workgroup of 256 lanes covers 32 rows and all N states;
-//   * per tile of T steps the workgroup stages delta, delta*x and Dskip*x
-//     (fp32, widened once from bf16 when needed) and B_t, C_t in LDS; lanes
-//     read them with LDS broadcast loads;
-//   * the per-lane loop does exp2(delta * A*log2e), delta*x*B, the state
-//     FMA and the C FMA into a per-lane partial of y_t;
-//   * the G partials of each y_t meet in LDS and are summed by the lane that
-//     stores y, together with Dskip*x (coalesced 16-byte stores along t);
-//   * the next tile's global loads are issued before the current tile is
-//     computed, so HBM latency hides behind the VALU work.
-#include "sw_internal.h"
+// half a byte of HBM traffic: the kernel is bound by the VALU issue rate, not
+// by HBM, and is laid out to spend as few VALU slots per element as possible
+// and to keep the SIMDs issuing:
+//   * one wavefront is one independent unit of work: 8 (b,d) rows x 8 lanes,
+//     each lane owning NPL = N/8 states of its row; there is no workgroup
+//     barrier anywhere;
+//   * per tile of T = 32 steps the wavefront stages delta and delta*x (fp32,
+//     widened once from bf16) and B_t, C_t in its own slice of LDS and reads
+//     them back with 16-byte LDS loads;
+//   * the per-lane loop does exp2(delta * A*log2e), (delta*x)*B, the state FMA
+//     and the C FMA into a per-lane partial of y_t;
+//   * the 8 partials of each y_t meet in LDS and are summed, with Dskip*x kept
+//     in registers, by the lane that stores y (16-byte stores along t);
+//   * global loads run two tiles ahead: raw bits go to registers and are
+//     widened only when staged; only the last, partial tile of a row takes the
+//     clamped and masked path.
+// Load balance: the work is cut into tasks (8-row block, sequence chunk)
+// handed out by an atomic ticket in chunk-major order to a persistent grid of
+// wavefronts.  A task waits for the final state of the same rows' previous
+// chunk, published as self-validating 64-bit words; that chunk holds an
+// earlier ticket, so it is running or done, which guarantees forward
+// progress.  A SIMD that runs fewer wavefronts finishes its tasks sooner and
+// takes more, so the work spreads evenly over the machine.
+#include <stdlib.h>
+
+#include <type_traits>
+
+#include "selective_common.h"
 
 namespace sw {
+
 namespace {
 
-constexpr int SS_THREADS = 256;
-constexpr int SS_G = 8;                     // lanes per (b,d) row
-constexpr int SS_RPB = SS_THREADS / SS_G;   // rows per workgroup
-constexpr int SS_T = 32;                    // time steps per tile
+constexpr int SS_G = 8;            // lanes per (b,d) row
+constexpr int SS_RPW = 64 / SS_G;  // rows per wavefront: 8
+constexpr int SS_T = 32;           // steps per tile
+constexpr int SS_TS = SS_T + 4;    // padded LDS row stride (16-byte aligned)
+// B/C tile in LDS: per step t a row of 8 slots [B_{g*NPL..}, C_{g*NPL..}] of
+// 2*NPL floats, rows padded by 4 floats so that the staging writes of the 64
+// lanes (2 lanes per step) spread over all banks; a row itself is contiguous,
+// so the compute-loop reads (8 slots of one step) are conflict-free too.
+template <int NPL>
+constexpr int bc_stride() { return SS_G * 2 * NPL + 4; }
 constexpr float LOG2E = 1.4426950408889634f;
 
+// One lane's share of one tile's global inputs.
+template <typename IN, int NPL>
+struct TileRaw {
+  RawVec<IN, 4> dl, xv;        // its row, steps tq .. tq+3
+  RawVec<IN, 4 * NPL> bb, cc;  // elements lane*4*NPL .. +4*NPL-1 of the (T, 8*NPL) tile
+};
+
+// Per-task, per-lane addressing of one wavefront's inputs and outputs.
 template <typename IN>
-struct In;
-
-template <>
-struct In<float> {
-  static __device__ __forceinline__ float get(const float* p, int64_t i) { return p[i]; }
-  // four consecutive values from a 16-byte aligned address
-  static __device__ __forceinline__ void get4(const float* p, int64_t i, float* v) {
-    float4 q = *reinterpret_cast<const float4*>(p + i);
-    v[0] = q.x;
-    v[1] = q.y;
-    v[2] = q.z;
-    v[3] = q.w;
-  }
+struct LanePtrs {
+  const IN* dl;  // delta row of this lane's staging row, at step tq
+  const IN* xv;  // x row, at step tq
+  int64_t bc;    // element offset of this lane's B/C slice in tile 0 (vector path)
+  int64_t row;   // element offset of the staging row (element path)
 };
 
-template <>
-struct In<uint16_t> {
-  static __device__ __forceinline__ float get(const uint16_t* p, int64_t i) {
-    return bf16_one(p[i]);
-  }
-  // four consecutive bf16 from an 8-byte aligned address
-  static __device__ __forceinline__ void get4(const uint16_t* p, int64_t i, float* v) {
-    uint2 q = *reinterpret_cast<const uint2*>(p + i);
-    v[0] = bf16_lo(q.x);
-    v[1] = bf16_hi(q.x);
-    v[2] = bf16_lo(q.y);
-    v[3] = bf16_hi(q.y);
-  }
-};
-
-// Registers holding one tile's worth of global inputs for one thread.
-template <int NPL>
-struct TileRegs {
-  float dl[4], xv[4];
-  float bv[NPL], cv[NPL];
-};
-
-template <typename IN, int NPL, bool VEC>
-__device__ __forceinline__ void load_tile(TileRegs<NPL>& r, const IN* __restrict__ x,
-                                          const IN* __restrict__ delta,
+// Fill `r` with tile [t0, t0+T).  FULL (uniform): the tile lies inside the
+// sequence and vector loads are allowed, so addresses need no clamping.
+// Otherwise elements are gathered one by one with steps clamped to L-1 and
+// padded states to N-1; the caller masks them when staging.
+template <bool FULL, bool NPADDED, typename IN, int NPL>
+__device__ __forceinline__ void load_tile(TileRaw<IN, NPL>& r, const LanePtrs<IN>& lp,
+                                          const IN* __restrict__ x, const IN* __restrict__ delta,
                                           const IN* __restrict__ Bm, const IN* __restrict__ Cm,
-                                          int64_t b, int64_t d0, int64_t D, int N, int64_t L,
-                                          int64_t t0, int tid) {
-  // delta and x: row tid/8, steps (tid%8)*4 .. +3 of the tile
-  const int rr = tid / 8;
-  const int tq = (tid % 8) * 4;
-  const int64_t d = d0 + rr;
-  const int64_t t = t0 + tq;
-  if (d < D) {
-    const int64_t base = (b * D + d) * L + t;
-    if (VEC && t + 4 <= L) {
-      In<IN>::get4(delta, base, r.dl);
-      In<IN>::get4(x, base, r.xv);
-    } else {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const bool ok = t + k < L;
-        r.dl[k] = ok ? In<IN>::get(delta, base + k) : 0.0f;
-        r.xv[k] = ok ? In<IN>::get(x, base + k) : 0.0f;
-      }
-    }
+                                          int64_t bc_off, int N, int64_t L, int64_t t0,
+                                          int lane) {
+  constexpr int NPAD = SS_G * NPL;
+  constexpr int PER = 4 * NPL;  // B (and C) elements per lane per tile
+  if constexpr (FULL) {
+    r.dl.load_vec(lp.dl + t0);
+    r.xv.load_vec(lp.xv + t0);
   } else {
+    const int tq = (lane % 8) * 4;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      r.dl[k] = 0.0f;
-      r.xv[k] = 0.0f;
+      const int64_t t = imin(t0 + tq + k, L - 1);
+      r.dl.set(k, Elt<IN>::raw(delta, lp.row + t));
+      r.xv.set(k, Elt<IN>::raw(x, lp.row + t));
     }
   }
-  // B and C: element e = tid + 256*m of the (T, G*NPL) tile
-  constexpr int NPAD = SS_G * NPL;
+  if constexpr (FULL && !NPADDED) {
+    // N == NPAD: the tile is T*N consecutive elements starting at (b, t0, 0)
+    r.bb.load_vec(Bm + lp.bc + t0 * N);
+    r.cc.load_vec(Cm + lp.bc + t0 * N);
+  } else {
 #pragma unroll
-  for (int m = 0; m < NPL; ++m) {
-    const int e = tid + SS_THREADS * m;
-    const int tt = e / NPAD;
-    const int n = e % NPAD;
-    const int64_t tg = t0 + tt;
-    const bool ok = n < N && tg < L;
-    const int64_t off = (b * L + tg) * N + n;
-    r.bv[m] = ok ? In<IN>::get(Bm, off) : 0.0f;
-    r.cv[m] = ok ? In<IN>::get(Cm, off) : 0.0f;
+    for (int i = 0; i < PER; ++i) {
+      const int e = lane * PER + i;
+      const int64_t t = imin(t0 + e / NPAD, L - 1);
+      const int n = (e % NPAD) < N ? (e % NPAD) : N - 1;
+      r.bb.set(i, Elt<IN>::raw(Bm, bc_off + t * N + n));
+      r.cc.set(i, Elt<IN>::raw(Cm, bc_off + t * N + n));
+    }
   }
 }
 
-template <typename IN, int NPL, bool VEC>
-__global__ __launch_bounds__(SS_THREADS) void selective_fwd_kernel(
+// Order LDS writes and reads of different lanes of one wavefront: LDS
+// instructions of a wavefront complete in order, so this only keeps the
+// compiler from moving memory operations across the point.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <bool B_>
+using Flag = std::integral_constant<bool, B_>;
+
+template <typename IN, int NPL, bool VEC, bool NPADDED>
+__global__ __launch_bounds__(64) void selective_fwd_kernel(
     const IN* __restrict__ x, const IN* __restrict__ delta, const float* __restrict__ A,
     const IN* __restrict__ Bm, const IN* __restrict__ Cm, const float* __restrict__ Dskip,
-    float* __restrict__ y, float* __restrict__ h_last, int64_t D, int N, int64_t L) {
-  constexpr int NPAD = SS_G * NPL;
+    float* __restrict__ y, float* __restrict__ h_last, int64_t D, int N, int64_t L, int64_t ndb,
+    int64_t nrb, int64_t Lc, int64_t nchunks, uint32_t ntasks,
+    unsigned long long* __restrict__ carry, uint32_t* __restrict__ ticket, uint32_t tbase,
+    uint32_t epoch) {
   constexpr int T = SS_T;
-  __shared__ float sDl[SS_RPB][T + 1];
-  __shared__ float sDx[SS_RPB][T + 1];
-  __shared__ float sYd[SS_RPB][T + 1];
-  __shared__ __align__(16) float sBC[T][SS_G][2 * NPL];
-  __shared__ float sP[SS_RPB][SS_G][T + 1];  // +1: lanes of 4 rows x 8 groups hit 32 banks
+  constexpr int TS = SS_TS;
+  constexpr int PER = 4 * NPL;
+  __shared__ __align__(16) float sDl[SS_RPW * TS];
+  __shared__ __align__(16) float sDx[SS_RPW * TS];
+  __shared__ __align__(16) float sBC[T * bc_stride<NPL>()];
+  __shared__ __align__(16) float sP[SS_RPW * SS_G * TS];
 
-  const int tid = threadIdx.x;
-  const int64_t ndb = (D + SS_RPB - 1) / SS_RPB;  // row blocks per batch
-  const int64_t b = (int64_t)blockIdx.x / ndb;
-  const int64_t d0 = ((int64_t)blockIdx.x - b * ndb) * SS_RPB;
+  const int lane = threadIdx.x;
+  const int r = lane / SS_G;      // row of this lane within the wavefront
+  const int g = lane % SS_G;      // state group: states g*NPL .. g*NPL+NPL-1
+  const int tq = (lane % 8) * 4;  // staging and reduce: steps tq .. tq+3 of a tile
+  const int btt = lane / 2;       // staging of B/C: step btt of a tile, slots 4*(lane%2)..+3
+  const uint32_t st_inc = carry_status(epoch, CARRY_INC);
+  float* const sDl_w = &sDl[r * TS + tq];
+  float* const sDx_w = &sDx[r * TS + tq];
+  float* const sBC_w = &sBC[btt * bc_stride<NPL>() + 4 * (lane % 2) * (2 * NPL)];
+  float* const sP_w = &sP[(r * SS_G + g) * TS];
+  const float* const sP_r = &sP[(r * SS_G) * TS + tq];
 
-  // compute-phase identity of this lane: row r, lane-group g, states g*NPL+j
-  const int r = tid / SS_G;
-  const int g = tid % SS_G;
-  const int64_t d = d0 + r;
-  float Al[NPL], hs[NPL];
-#pragma unroll
-  for (int j = 0; j < NPL; ++j) {
-    const int n = g * NPL + j;
-    Al[j] = (d < D && n < N) ? A[d * N + n] * LOG2E : 0.0f;
-    hs[j] = 0.0f;
-  }
-  // staging identity: row tid/8, steps (tid%8)*4..+3
-  const int rr = tid / 8;
-  const int tq = (tid % 8) * 4;
-  const float dsk = (Dskip && d0 + rr < D) ? Dskip[d0 + rr] : 0.0f;
+  for (;;) {
+    uint32_t tk = 0;
+    if (lane == 0) tk = atomicAdd(ticket, 1u) - tbase;
+    const uint32_t id = __builtin_amdgcn_readfirstlane(tk);
+    if (id >= ntasks) break;
+    const int64_t c = (int64_t)id / nrb;
+    const int64_t rb = (int64_t)id - c * nrb;
+    const int64_t b = rb / ndb;
+    const int64_t d0 = (rb - b * ndb) * SS_RPW;
+    const int64_t tb = c * Lc;
+    const int64_t te = imin(L, tb + Lc);
+    const int ntile = (int)((te - tb + T - 1) / T);
 
-  TileRegs<NPL> cur;
-  load_tile<IN, NPL, VEC>(cur, x, delta, Bm, Cm, b, d0, D, N, L, 0, tid);
-
-  for (int64_t t0 = 0; t0 < L; t0 += T) {
-    // stage the tile held in registers
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      sDl[rr][tq + k] = cur.dl[k];
-      sDx[rr][tq + k] = cur.dl[k] * cur.xv[k];
-      sYd[rr][tq + k] = dsk * cur.xv[k];
-    }
-#pragma unroll
-    for (int m = 0; m < NPL; ++m) {
-      const int e = tid + SS_THREADS * m;
-      const int tt = e / NPAD;
-      const int n = e % NPAD;
-      sBC[tt][n / NPL][n % NPL] = cur.bv[m];
-      sBC[tt][n / NPL][NPL + n % NPL] = cur.cv[m];
-    }
-    __syncthreads();
-    // prefetch the next tile while this one is computed
-    if (t0 + T < L) load_tile<IN, NPL, VEC>(cur, x, delta, Bm, Cm, b, d0, D, N, L, t0 + T, tid);
-
-    // recurrence over the tile
-#pragma unroll 4
-    for (int t = 0; t < T; ++t) {
-      const float dl = sDl[r][t];
-      const float dx = sDx[r][t];
-      float bc[2 * NPL];
-#pragma unroll
-      for (int j = 0; j < 2 * NPL; ++j) bc[j] = sBC[t][g][j];
-      float p = 0.0f;
-#pragma unroll
-      for (int j = 0; j < NPL; ++j) {
-        const float a = __builtin_amdgcn_exp2f(dl * Al[j]);
-        hs[j] = __builtin_fmaf(a, hs[j], dx * bc[j]);
-        p = __builtin_fmaf(bc[NPL + j], hs[j], p);
-      }
-      sP[r][g][t] = p;
-    }
-    __syncthreads();
-
-    // y = Dskip*x + sum of the G partials, stored along t
-    {
-      const int64_t dd = d0 + rr;
-      const int64_t tt = t0 + tq;
-      float yv[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        float s = sYd[rr][tq + k];
-#pragma unroll
-        for (int gg = 0; gg < SS_G; ++gg) s += sP[rr][gg][tq + k];
-        yv[k] = s;
-      }
-      if (dd < D) {
-        float* yr = y + (b * D + dd) * L;
-        if (VEC && tt + 4 <= L) {
-          *reinterpret_cast<float4*>(yr + tt) = make_float4(yv[0], yv[1], yv[2], yv[3]);
-        } else {
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            if (tt + k < L) yr[tt + k] = yv[k];
-        }
-      }
-    }
-    __syncthreads();
-  }
-
-  if (h_last && d < D) {
+    const int64_t d = d0 + r;
+    const bool dok = d < D;
+    const int64_t dcl = dok ? d : D - 1;  // rows past D compute a copy of row D-1, never stored
+    const int64_t bc_off = b * L * N;
+    LanePtrs<IN> lp;
+    lp.row = (b * D + dcl) * L;
+    lp.dl = delta + lp.row + tq;
+    lp.xv = x + lp.row + tq;
+    lp.bc = bc_off + lane * PER;
+    float* const y_row = y + (b * D + dcl) * L + tq;
+    float Al[NPL], hs[NPL];
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
       const int n = g * NPL + j;
-      if (n < N) h_last[(b * D + d) * N + n] = hs[j];
+      const float av = A[dcl * N + (n < N ? n : N - 1)];
+      Al[j] = n < N ? av * LOG2E : 0.0f;  // padded states: a = 1, u = 0 (B masked to 0)
+      hs[j] = 0.0f;
+    }
+    const float dsk = Dskip ? Dskip[dcl] : 0.0f;
+
+    if (c > 0) {  // state entering the chunk: the previous chunk's final state
+      const unsigned long long* cw = carry + ((c - 1) * nrb + rb) * (64 * NPL) + lane * NPL;
+#pragma unroll
+      for (int j = 0; j < NPL; ++j) {
+        unsigned long long w;
+        while ((uint32_t)((w = carry_get(cw + j)) >> 32) != st_inc) __builtin_amdgcn_s_sleep(2);
+        hs[j] = __uint_as_float((uint32_t)w);
+      }
+    }
+
+    auto fetch = [&](TileRaw<IN, NPL>& rr, int kt) {
+      const int64_t t0 = tb + (int64_t)kt * T;
+      if (VEC && t0 + T <= L)
+        load_tile<true, NPADDED>(rr, lp, x, delta, Bm, Cm, bc_off, N, L, t0, lane);
+      else
+        load_tile<false, NPADDED>(rr, lp, x, delta, Bm, Cm, bc_off, N, L, t0, lane);
+    };
+    TileRaw<IN, NPL> ra, rbuf;
+    fetch(ra, 0);
+    if (ntile > 1) fetch(rbuf, 1);
+    float ydp[4] = {0.f, 0.f, 0.f, 0.f};  // Dskip*x of the tile awaiting its reduce
+
+    // y = Dskip*x + sum of the 8 partials of tile kt, stored along t
+    auto reduce = [&](int kt, auto full) {
+      const int64_t t = tb + (int64_t)kt * T + tq;
+      float4 s = make_float4(ydp[0], ydp[1], ydp[2], ydp[3]);
+#pragma unroll
+      for (int gg = 0; gg < SS_G; ++gg) {
+        const float4 p = *reinterpret_cast<const float4*>(sP_r + gg * TS);
+        s.x += p.x;
+        s.y += p.y;
+        s.z += p.z;
+        s.w += p.w;
+      }
+      if (dok) {
+        float* yr = y_row + (t - tq);
+        if constexpr (decltype(full)::value && VEC) {
+          *reinterpret_cast<float4*>(yr) = s;
+        } else {
+          const float sv[4] = {s.x, s.y, s.z, s.w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (t + q < te) yr[q] = sv[q];
+        }
+      }
+    };
+
+    auto tile = [&](int kt, TileRaw<IN, NPL>& rr, auto full, bool prev_full) {
+      constexpr bool FULL = decltype(full)::value;
+      const int64_t t0 = tb + (int64_t)kt * T;
+      // stage: widen (and, in a tail tile, mask) and write this wavefront's LDS
+      float dl4[4], dx4[4], yd4[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float dv = rr.dl.get(q), xv = rr.xv.get(q);
+        if constexpr (!FULL) {
+          if (t0 + tq + q >= te) dv = xv = 0.0f;  // identity step: a = 1, u = 0
+        }
+        dl4[q] = dv;
+        dx4[q] = dv * xv;
+        yd4[q] = dsk * xv;
+      }
+      *reinterpret_cast<float4*>(sDl_w) = make_float4(dl4[0], dl4[1], dl4[2], dl4[3]);
+      *reinterpret_cast<float4*>(sDx_w) = make_float4(dx4[0], dx4[1], dx4[2], dx4[3]);
+      {
+        // this lane holds step btt = lane/2, states (lane%2)*4*NPL .. +4*NPL-1,
+        // i.e. slots 4*(lane%2) .. +3; one slot [B.., C..] is written at a time
+        const bool tmask = !FULL && t0 + btt >= te;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          float v[2 * NPL];
+#pragma unroll
+          for (int j = 0; j < NPL; ++j) {
+            float bv = rr.bb.get(k * NPL + j), cv = rr.cc.get(k * NPL + j);
+            if constexpr (NPADDED) {
+              if ((4 * (lane % 2) + k) * NPL + j >= N) bv = cv = 0.0f;
+            }
+            if constexpr (!FULL) {
+              if (tmask) bv = cv = 0.0f;
+            }
+            v[j] = bv;
+            v[NPL + j] = cv;
+          }
+          float* dst = sBC_w + k * (2 * NPL);
+          if constexpr (NPL == 1) {
+            *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
+          } else {
+#pragma unroll
+            for (int j = 0; j < 2 * NPL; j += 4)
+              *reinterpret_cast<float4*>(dst + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+          }
+        }
+      }
+      // the registers are free again: fetch the tile two ahead
+      if (kt + 2 < ntile) fetch(rr, kt + 2);
+      if (kt > 0) {
+        if (prev_full)
+          reduce(kt - 1, Flag<true>());
+        else
+          reduce(kt - 1, Flag<false>());
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) ydp[q] = yd4[q];
+      wave_sync();
+
+      // recurrence over the tile
+#pragma unroll
+      for (int t4 = 0; t4 < T; t4 += 4) {
+        const float4 dlv = *reinterpret_cast<const float4*>(&sDl[r * TS + t4]);
+        const float4 dxv = *reinterpret_cast<const float4*>(&sDx[r * TS + t4]);
+        const float dls[4] = {dlv.x, dlv.y, dlv.z, dlv.w};
+        const float dxs[4] = {dxv.x, dxv.y, dxv.z, dxv.w};
+        float p4[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float bc[2 * NPL];
+          const float* src = &sBC[(t4 + q) * bc_stride<NPL>() + g * (2 * NPL)];
+          if constexpr (NPL == 1) {
+            const float2 v = *reinterpret_cast<const float2*>(src);
+            bc[0] = v.x;
+            bc[1] = v.y;
+          } else {
+#pragma unroll
+            for (int j = 0; j < 2 * NPL; j += 4) {
+              const float4 v = *reinterpret_cast<const float4*>(src + j);
+              bc[j] = v.x;
+              bc[j + 1] = v.y;
+              bc[j + 2] = v.z;
+              bc[j + 3] = v.w;
+            }
+          }
+          float p = 0.0f;
+#pragma unroll
+          for (int j = 0; j < NPL; ++j) {
+            const float a = __builtin_amdgcn_exp2f(dls[q] * Al[j]);
+            hs[j] = __builtin_fmaf(a, hs[j], dxs[q] * bc[j]);
+            p = __builtin_fmaf(bc[NPL + j], hs[j], p);
+          }
+          p4[q] = p;
+        }
+        *reinterpret_cast<float4*>(sP_w + t4) = make_float4(p4[0], p4[1], p4[2], p4[3]);
+      }
+      wave_sync();
+    };
+
+    // a tile is full when it lies inside both the chunk and the sequence
+    auto is_full = [&](int kt) { return tb + (int64_t)(kt + 1) * T <= te; };
+    for (int kt = 0; kt < ntile; kt += 2) {
+      if (is_full(kt))
+        tile(kt, ra, Flag<true>(), kt > 0 && is_full(kt - 1));
+      else
+        tile(kt, ra, Flag<false>(), kt > 0 && is_full(kt - 1));
+      if (kt + 1 < ntile) {
+        if (is_full(kt + 1))
+          tile(kt + 1, rbuf, Flag<true>(), is_full(kt));
+        else
+          tile(kt + 1, rbuf, Flag<false>(), is_full(kt));
+      }
+    }
+    if (is_full(ntile - 1))
+      reduce(ntile - 1, Flag<true>());
+    else
+      reduce(ntile - 1, Flag<false>());
+    wave_sync();  // the next task rewrites this wavefront's LDS
+
+    if (c + 1 < nchunks) {
+      unsigned long long* out = carry + (c * nrb + rb) * (64 * NPL) + lane * NPL;
+#pragma unroll
+      for (int j = 0; j < NPL; ++j) carry_put(out + j, st_inc, __float_as_uint(hs[j]));
+    } else if (h_last && dok) {
+#pragma unroll
+      for (int j = 0; j < NPL; ++j) {
+        const int n = g * NPL + j;
+        if (n < N) h_last[(b * D + d) * N + n] = hs[j];
+      }
     }
   }
+}
+
+struct Plan {
+  int64_t ndb, nrb, Lc, nchunks, grid;
+  uint32_t ntasks;
+};
+
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  return (v && *v) ? atoi(v) : dflt;
+}
+
+// Persistent grid size and chunking for a launch.
+int make_plan(int64_t B, int64_t D, int64_t L, Plan* p) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  int cus = 0;
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess || cus <= 0)
+    return fail(SW_ERR_HIP, "device query failed: %s", hipGetErrorString(e));
+  // resident wavefronts per CU and tasks per wavefront (tuning knobs)
+  static const int waves_per_cu = env_int("SW_SS_WAVES_PER_CU", 6);
+  static const int tasks_per_wave = env_int("SW_SS_TASKS_PER_WAVE", 4);
+  p->ndb = (D + SS_RPW - 1) / SS_RPW;
+  p->nrb = B * p->ndb;
+  int64_t slots = (int64_t)cus * (waves_per_cu > 0 ? waves_per_cu : 6);
+  if (slots > p->nrb) slots = p->nrb;  // no more wavefronts than independent chains
+  const int64_t tiles = (L + SS_T - 1) / SS_T;
+  int64_t want = (slots * (tasks_per_wave > 0 ? tasks_per_wave : 4) + p->nrb - 1) / p->nrb;
+  const int64_t max_chunks = (tiles + 3) / 4;  // a chunk keeps at least 4 tiles
+  if (want > max_chunks) want = max_chunks;
+  if (want < 1) want = 1;
+  const int64_t tiles_per_chunk = (tiles + want - 1) / want;
+  p->Lc = tiles_per_chunk * SS_T;
+  p->nchunks = (L + p->Lc - 1) / p->Lc;
+  const int64_t ntasks = p->nrb * p->nchunks;
+  if (ntasks >= ((int64_t)1 << 31))
+    return fail(SW_ERR_UNSUPPORTED, "%lld tasks exceed the ticket range", (long long)ntasks);
+  p->ntasks = (uint32_t)ntasks;
+  p->grid = ntasks < slots ? ntasks : slots;
+  return SW_OK;
+}
+
+template <typename IN, int NPL, bool VEC, bool NPADDED>
+int launch_cfg(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
+               const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int N,
+               int64_t L, hipStream_t s) {
+  Plan p;
+  int st = make_plan(B, D, L, &p);
+  if (st != SW_OK) return st;
+  ScratchSession ss;
+  const size_t words = (size_t)(p.nchunks - 1) * p.nrb * 64 * NPL;
+  st = ss.reserve(words, p.ntasks + (uint32_t)p.grid, s);
+  if (st != SW_OK) return st;
+  hipLaunchKernelGGL((selective_fwd_kernel<IN, NPL, VEC, NPADDED>), dim3((unsigned)p.grid),
+                     dim3(64), 0, s, x, delta, A, Bm, Cm, Dskip, y, h_last, D, N, L, p.ndb,
+                     p.nrb, p.Lc, p.nchunks, p.ntasks, ss.carry, ss.ticket, ss.ticket_base,
+                     ss.epoch);
+  st = check_launch("selective_fwd_kernel");
+  if (st != SW_OK) ss.invalidate();
+  return st;
 }
 
 template <typename IN, int NPL>
 int launch_npl(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
                const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int N,
                int64_t L, bool vec, hipStream_t s) {
-  dim3 grid((unsigned)(B * ((D + SS_RPB - 1) / SS_RPB)));
+  const bool padded = N != SS_G * NPL;
+  if (vec && !padded)
+    return launch_cfg<IN, NPL, true, false>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, s);
   if (vec)
-    hipLaunchKernelGGL((selective_fwd_kernel<IN, NPL, true>), grid, dim3(SS_THREADS), 0, s, x,
-                       delta, A, Bm, Cm, Dskip, y, h_last, D, N, L);
-  else
-    hipLaunchKernelGGL((selective_fwd_kernel<IN, NPL, false>), grid, dim3(SS_THREADS), 0, s, x,
-                       delta, A, Bm, Cm, Dskip, y, h_last, D, N, L);
-  return check_launch("selective_fwd_kernel");
+    return launch_cfg<IN, NPL, true, true>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, s);
+  return launch_cfg<IN, NPL, false, true>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, s);
 }
 
 template <typename IN>
@@ -249,10 +442,12 @@ int launch_selective(const IN* x, const IN* delta, const float* A, const IN* Bm,
                      int64_t N, int64_t L, bool vec) {
   hipStream_t s = current_stream();
   const int n = (int)N;
-  if (n <= 8) return launch_npl<IN, 1>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, vec, s);
-  if (n <= 16) return launch_npl<IN, 2>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, vec, s);
-  if (n <= 32) return launch_npl<IN, 4>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, vec, s);
-  return launch_npl<IN, 8>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, vec, s);
+  // vector B/C loads need 16-byte aligned B and C (tile starts are then aligned)
+  const bool v = vec && ((uintptr_t)Bm % 16 == 0) && ((uintptr_t)Cm % 16 == 0);
+  if (n <= 8) return launch_npl<IN, 1>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
+  if (n <= 16) return launch_npl<IN, 2>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
+  if (n <= 32) return launch_npl<IN, 4>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
+  return launch_npl<IN, 8>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
 }
 
 }  // namespace

@@ -5,7 +5,9 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <map>
 #include <mutex>
+#include <utility>
 
 #include "sw_internal.h"
 
@@ -25,8 +27,7 @@ int selective_fwd_bf16(const uint16_t* x, const uint16_t* delta, const float* A,
 namespace {
 thread_local hipStream_t tls_stream = nullptr;
 thread_local char tls_msg[512] = "";
-std::mutex pool_mu;
-bool pool_ready[64] = {};
+bool pool_ready[64] = {};  // guarded by scratch_mu
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -190,32 +191,78 @@ int check_launch(const char* what) {
   return SW_OK;
 }
 
-int scratch_alloc(void** p, size_t bytes, hipStream_t s) {
-  int dev = 0;
-  if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
-    std::lock_guard<std::mutex> lk(pool_mu);
-    if (!pool_ready[dev]) {
-      // keep freed scratch in the pool instead of returning it at every sync
-      hipMemPool_t pool;
-      if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-        uint64_t keep = UINT64_MAX;
-        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
-      }
-      (void)hipGetLastError();
-      pool_ready[dev] = true;
-    }
+namespace {
+
+struct StreamScratch {
+  void* base = nullptr;   // [0, 256): ticket counter; [256, bytes): carry words
+  size_t bytes = 0;
+  uint32_t next_ticket = 0;
+  uint32_t epoch = 0;
+};
+
+std::mutex scratch_mu;
+std::map<std::pair<int, hipStream_t>, StreamScratch> scratch_map;
+
+void keep_pool_memory(int dev) {
+  if (dev < 0 || dev >= 64 || pool_ready[dev]) return;
+  // keep freed blocks in the stream-ordered pool instead of returning them at every sync
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+    uint64_t keep = UINT64_MAX;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
   }
-  hipError_t e = hipMallocAsync(p, bytes, s);
-  if (e != hipSuccess) {
-    (void)hipGetLastError();
-    *p = nullptr;
-    return fail(SW_ERR_ALLOC, "hipMallocAsync(%zu bytes): %s", bytes, hipGetErrorString(e));
-  }
-  return SW_OK;
+  (void)hipGetLastError();
+  pool_ready[dev] = true;
 }
 
-void scratch_free(void* p, hipStream_t s) {
-  if (p) (void)hipFreeAsync(p, s);
+}  // namespace
+
+ScratchSession::ScratchSession() {}
+
+void ScratchSession::invalidate() {
+  if (!locked_ || dev_ < 0) return;
+  StreamScratch& ws = scratch_map[std::make_pair(dev_, stream_)];
+  ws.bytes = 0;  // the next reserve() reallocates and zeroes
+}
+
+ScratchSession::~ScratchSession() {
+  if (locked_) scratch_mu.unlock();
+}
+
+int ScratchSession::reserve(size_t carry_words, uint32_t tickets, hipStream_t s) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SW_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (!locked_) {
+    scratch_mu.lock();
+    locked_ = true;
+  }
+  dev_ = dev;
+  stream_ = s;
+  StreamScratch& ws = scratch_map[std::make_pair(dev, s)];
+  const size_t need = 256 + carry_words * 8;
+  if (ws.bytes < need || ws.epoch + 1 >= (1u << 30)) {
+    if (ws.base) (void)hipFreeAsync(ws.base, s);
+    ws = StreamScratch();
+    keep_pool_memory(dev);
+    size_t bytes = need < ((size_t)1 << 20) ? ((size_t)1 << 20) : need + need / 4;
+    e = hipMallocAsync(&ws.base, bytes, s);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      ws.base = nullptr;
+      return fail(SW_ERR_ALLOC, "hipMallocAsync(%zu bytes): %s", bytes, hipGetErrorString(e));
+    }
+    int st = zero_words(reinterpret_cast<uint32_t*>(ws.base), bytes / 4, s);
+    if (st != SW_OK) return st;
+    ws.bytes = bytes;
+  }
+  ws.epoch += 1;
+  epoch = ws.epoch;
+  ticket = reinterpret_cast<uint32_t*>(ws.base);
+  ticket_base = ws.next_ticket;
+  ws.next_ticket += tickets;  // wraps modulo 2^32 together with the device counter
+  carry = reinterpret_cast<unsigned long long*>(reinterpret_cast<char*>(ws.base) + 256);
+  return SW_OK;
 }
 
 int zero_words(uint32_t* p, size_t words, hipStream_t s) {

@@ -20,11 +20,38 @@ int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)))
 hipStream_t current_stream();
 int check_launch(const char* what);  // hipGetLastError -> SW_ERR_HIP with a message
 
-// Scratch from the device's stream-ordered pool (released on the same stream).
-int scratch_alloc(void** p, size_t bytes, hipStream_t s);
-void scratch_free(void* p, hipStream_t s);
 // Zero `words` 32-bit words with a plain kernel (no memset node).
 int zero_words(uint32_t* p, size_t words, hipStream_t s);
+
+// Persistent scratch of one (device, stream): carry words passed between
+// workgroups and a ticket counter.  It is zeroed once when (re)allocated and
+// never again: each launch tags the carry words it writes with a fresh
+// epoch, so words left by earlier launches never match, and the ticket
+// counter only grows (a launch knows the value it starts from).  The session
+// holds a lock from reserve() until it is destroyed, so the order in which
+// launches are enqueued on the stream is the order in which epochs and ticket
+// ranges were handed out.
+struct ScratchSession {
+  ScratchSession();
+  ~ScratchSession();
+  ScratchSession(const ScratchSession&) = delete;
+  ScratchSession& operator=(const ScratchSession&) = delete;
+  // Make room for `carry_words` 64-bit words on stream `s`; the launch will
+  // consume exactly `tickets` tickets.  Fills carry / ticket / ticket_base /
+  // epoch.  Returns SW_OK or an error status.
+  int reserve(size_t carry_words, uint32_t tickets, hipStream_t s);
+  // The launch that reserved could not be enqueued: the ticket count handed
+  // out no longer matches the device counter, so start afresh next time.
+  void invalidate();
+  unsigned long long* carry = nullptr;
+  uint32_t* ticket = nullptr;
+  uint32_t ticket_base = 0;
+  uint32_t epoch = 0;  // in [1, 2^30)
+ private:
+  bool locked_ = false;
+  int dev_ = -1;
+  hipStream_t stream_ = nullptr;
+};
 
 // ---------------------------------------------------------------- device side
 
@@ -121,8 +148,9 @@ __device__ __forceinline__ void wave_shift_exclusive(T& A, T& U) {
 // ------------------------------------------------------------- carry words
 // A carry word is 64 bits: status in the high half, a 32-bit payload in the
 // low half, written and read with single relaxed device-scope atomics, so a
-// reader either sees the whole word or the previous one.  Status encodes an
-// epoch and a kind; the scratch is zeroed before each launch (epoch 1).
+// reader either sees the whole word or the previous one, and no fence is
+// needed between payload and flag.  Status encodes the launch's epoch and a
+// kind; words from earlier launches carry older epochs and never match.
 enum : uint32_t { CARRY_EMPTY = 0, CARRY_AGG = 1, CARRY_INC = 2 };
 
 __device__ __forceinline__ uint32_t carry_status(uint32_t epoch, uint32_t kind) {
