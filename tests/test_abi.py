@@ -1,0 +1,96 @@
+"""The C ABI: the library loads, exports every symbol the header declares (and
+nothing else), and its host-side validation answers without a GPU."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "scanweaver.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sw_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2606_00601_amd as pkg
+    return pkg.lib()
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for n in ("sw_affine_scan", "sw_affine_scan_i32", "sw_selective_scan_fwd",
+              "sw_selective_scan_fwd_bf16", "sw_set_stream", "sw_status_string",
+              "sw_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for n in _declared():
+        assert hasattr(lib, n), n
+
+
+def test_library_exports_nothing_else():
+    from paper_2606_00601_amd._lib import LIB_PATH
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    syms = {ln.split()[-1] for ln in out.splitlines() if " T " in ln}
+    assert syms == set(_declared())
+
+
+def test_binding_signatures_match_header():
+    from paper_2606_00601_amd._lib import SIGNATURES
+    assert set(SIGNATURES) == set(_declared())
+
+
+def test_validation_without_gpu(lib):
+    # negative sizes: invalid argument, before any HIP call
+    assert lib.sw_affine_scan(None, None, None, None, -1, 2, 3) == 1
+    assert "negative" in lib.sw_last_error().decode()
+    assert lib.sw_affine_scan_i32(None, None, None, None, 1, -2, 3) == 1
+    assert lib.sw_selective_scan_fwd(*([None] * 8), 1, 1, -1, 4) == 1
+    # N outside [1, 64]: unsupported
+    assert lib.sw_selective_scan_fwd(*([None] * 8), 1, 1, 65, 4) == 2
+    assert lib.sw_selective_scan_fwd_bf16(*([None] * 8), 1, 1, 0, 4) == 2
+    # empty outputs: nothing to do, pointers not inspected
+    assert lib.sw_affine_scan(None, None, None, None, 0, 5, 7) == 0
+    assert lib.sw_affine_scan(None, None, None, None, 3, 5, 0) == 0
+    assert lib.sw_selective_scan_fwd(*([None] * 8), 2, 0, 16, 9) == 0
+    # overflowing sizes are refused
+    big = 1 << 40
+    assert lib.sw_affine_scan(None, None, None, None, big, big, 4) == 2
+
+
+def test_status_strings(lib):
+    assert lib.sw_status_string(0) == b"SW_OK"
+    assert lib.sw_status_string(1) == b"SW_ERR_INVALID_ARG"
+    assert lib.sw_status_string(2) == b"SW_ERR_UNSUPPORTED"
+    assert lib.sw_status_string(3) == b"SW_ERR_HIP"
+    assert lib.sw_status_string(4) == b"SW_ERR_ALLOC"
+    assert lib.sw_status_string(99) == b"SW_ERR_UNKNOWN"
+
+
+def test_stream_is_per_thread(lib):
+    import threading
+    lib.sw_set_stream(ctypes.c_void_p(0x1234))
+    seen = []
+    t = threading.Thread(target=lambda: seen.append(lib.sw_get_stream()))
+    t.start()
+    t.join()
+    assert lib.sw_get_stream() == 0x1234
+    assert seen == [None]
+    lib.sw_set_stream(None)
+
+
+def test_binding_rejects_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    import paper_2606_00601_amd as pkg
+    a = torch.zeros((1, 2, 3))
+    with pytest.raises(ValueError):
+        pkg.affine_scan(a, a)
