@@ -115,6 +115,73 @@ def cpu_baseline(w, inp, target_s: float = 12.0, max_rows: int | None = None):
     }
 
 
+def time_launches(step, steps, warmup):
+    """Run warmup steps, then `steps` timed ones; returns (wall seconds, per-launch seconds)."""
+    import torch
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        step(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([a.elapsed_time(b) * 1e-3 for a, b in ev])
+    return wall, per
+
+
+def bench_affine(w, args):
+    """The bare affine scan (fp32): an HBM-bound kernel, 12 bytes per element."""
+    import torch
+
+    import paper_2606_00601_amd as sw
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sw.lib()
+    inp = w.inputs()
+    abytes = 12 * w.elems
+    nsets = args.sets or max(1, min(4, int(np.ceil(2 * MALL_BYTES / abytes)) + 1))
+    sets = []
+    for i in range(nsets):
+        a = torch.from_numpy(inp["a"]).to(dev)
+        bx = torch.from_numpy(inp["bx"]).to(dev)
+        sets.append((a, bx, torch.empty_like(a)))
+    del inp
+
+    def step(i):
+        a, bx, h = sets[i % nsets]
+        sw.affine_scan(a, bx, out=h)
+
+    wall, per = time_launches(step, args.steps, args.warmup)
+    kern = float(per.mean())
+    gbs = abytes / kern / 1e9
+    # the library walks each row in one workgroup once the rows alone fill the
+    # GPU (>= 8 per CU) and a row is longer than one 2048-step chunk
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    kname = ("affine_rows_kernel" if w.L > 2048 and w.B * w.D >= 8 * cus
+             else "affine_scan_kernel")
+    out = {
+        "metric": "affine-scan fwd B*L*D elems/s (+ achieved HBM GB/s vs peak), 1 GPU",
+        "value": w.elems * args.steps / wall, "unit": "elems/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "D": w.D, "L": w.L, "input_sets_rotated": nsets},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None, "kernel": kname,
+                     "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
+                                       "median": float(np.median(per)) * 1e6}},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -150,8 +217,8 @@ def main(argv=None):
 
     import paper_2606_00601_amd as sw
     w = wl.workload(args.workload)
-    if w.path != "selective":
-        raise SystemExit("bench.py times the fused selective scan workloads")
+    if w.path == "affine":
+        return bench_affine(w, args)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     sw.lib()  # the HIP library must be present: no fallback

@@ -19,7 +19,9 @@
 //      and stores them with 16-byte vector stores.
 // Chunks are handed out through an atomic ticket in chunk-major order (all
 // rows' chunk 0 first), so a chunk only ever waits on chunks that already
-// hold a ticket, which guarantees forward progress.
+// hold a ticket, which guarantees forward progress.  When the rows alone fill
+// the GPU, affine_rows_kernel below walks each row in one workgroup instead
+// and no carry leaves the chip.
 #include "sw_internal.h"
 
 namespace sw {
@@ -178,10 +180,149 @@ __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
 
 constexpr int AS_K = 8;
 
+// Row-serial variant for many rows: one workgroup owns one (b,d) row and walks
+// it chunk by chunk, keeping the carry in registers (every lane folds the four
+// wavefront totals, so every lane knows the state leaving the chunk).  No
+// cross-workgroup traffic, no scratch; the next chunk's loads are in flight
+// while the current one is scanned.  Used when the rows alone fill the GPU.
+template <typename T, int K, bool VEC>
+struct ChunkRegs {
+  T a[K], u[K];
+};
+
+// Branch-free loads (clamped addresses, identity pairs past the end): the
+// prefetch then never forces a wait, and the register buffer is never written
+// from two control-flow paths.  Requires L >= 4; with VEC, L is a multiple of
+// 4, so every 4-element piece is wholly inside or wholly outside the row.
+template <typename T, int K, bool VEC>
+__device__ __forceinline__ void load_chunk(ChunkRegs<T, K, VEC>& r, const T* __restrict__ ar,
+                                           const T* __restrict__ br, int64_t t0, int64_t L) {
+  using Rg = Ring<T>;
+  if (VEC) {
+#pragma unroll
+    for (int q = 0; q < K / 4; ++q) {
+      const int64_t tq = t0 + 4 * q;
+      const bool ok = tq < L;
+      const int64_t at = ok ? tq : L - 4;
+      const uint4 va = *reinterpret_cast<const uint4*>(ar + at);
+      const uint4 vb = *reinterpret_cast<const uint4*>(br + at);
+      r.a[4 * q + 0] = ok ? Rg::from_bits(va.x) : Rg::one();
+      r.a[4 * q + 1] = ok ? Rg::from_bits(va.y) : Rg::one();
+      r.a[4 * q + 2] = ok ? Rg::from_bits(va.z) : Rg::one();
+      r.a[4 * q + 3] = ok ? Rg::from_bits(va.w) : Rg::one();
+      r.u[4 * q + 0] = ok ? Rg::from_bits(vb.x) : Rg::zero();
+      r.u[4 * q + 1] = ok ? Rg::from_bits(vb.y) : Rg::zero();
+      r.u[4 * q + 2] = ok ? Rg::from_bits(vb.z) : Rg::zero();
+      r.u[4 * q + 3] = ok ? Rg::from_bits(vb.w) : Rg::zero();
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const bool ok = t0 + k < L;
+      const int64_t at = ok ? t0 + k : L - 1;
+      const T va = ar[at], vb = br[at];
+      r.a[k] = ok ? va : Rg::one();
+      r.u[k] = ok ? vb : Rg::zero();
+    }
+  }
+}
+
+template <typename T, int K, bool VEC>
+__global__ __launch_bounds__(AS_THREADS) void affine_rows_kernel(
+    const T* __restrict__ a, const T* __restrict__ bx, const T* __restrict__ h0,
+    T* __restrict__ h, int64_t R, int64_t L) {
+  constexpr int64_t CH = (int64_t)AS_THREADS * K;
+  using Rg = Ring<T>;
+  __shared__ T sA[2][AS_WAVES], sU[2][AS_WAVES];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t nch = (L + CH - 1) / CH;
+
+  for (int64_t row = blockIdx.x; row < R; row += gridDim.x) {
+    const T* __restrict__ ar = a + row * L;
+    const T* __restrict__ br = bx + row * L;
+    T* __restrict__ hr = h + row * L;
+    T carry = h0 ? h0[row] : Rg::zero();
+    ChunkRegs<T, K, VEC> cur, nxt;
+    load_chunk(cur, ar, br, (int64_t)tid * K, L);
+    for (int64_t c = 0; c < nch; ++c) {
+      const int64_t t0 = c * CH + (int64_t)tid * K;
+      if (c + 1 < nch) load_chunk(nxt, ar, br, t0 + CH, L);  // in flight during the scan
+      T pa[K], pu[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        pa[k] = cur.a[k];
+        pu[k] = cur.u[k];
+      }
+#pragma unroll
+      for (int k = 1; k < K; ++k) absorb_earlier(pa[k], pu[k], pa[k - 1], pu[k - 1]);
+      T wA = pa[K - 1], wU = pu[K - 1];
+      wave_inclusive_scan(wA, wU);
+      const int buf = (int)(c & 1);
+      if (lane == 63) {
+        sA[buf][wave] = wA;
+        sU[buf][wave] = wU;
+      }
+      wave_shift_exclusive(wA, wU);
+      __syncthreads();  // one barrier per chunk: the totals alternate between two buffers
+      T pA = Rg::one(), pU = Rg::zero(), cA = Rg::one(), cU = Rg::zero();
+#pragma unroll
+      for (int w = 0; w < AS_WAVES; ++w) {
+        if (w == wave) {
+          pA = cA;
+          pU = cU;
+        }
+        T nA = sA[buf][w], nU = sU[buf][w];
+        absorb_earlier(nA, nU, cA, cU);
+        cA = nA;
+        cU = nU;
+      }
+      absorb_earlier(wA, wU, pA, pU);
+      const T hs = Rg::mad(wA, carry, wU);
+      if (VEC) {
+#pragma unroll
+        for (int q = 0; q < K / 4; ++q) {
+          uint4 o;
+          o.x = Rg::bits(Rg::mad(pa[4 * q + 0], hs, pu[4 * q + 0]));
+          o.y = Rg::bits(Rg::mad(pa[4 * q + 1], hs, pu[4 * q + 1]));
+          o.z = Rg::bits(Rg::mad(pa[4 * q + 2], hs, pu[4 * q + 2]));
+          o.w = Rg::bits(Rg::mad(pa[4 * q + 3], hs, pu[4 * q + 3]));
+          if (t0 + 4 * q < L) *reinterpret_cast<uint4*>(hr + t0 + 4 * q) = o;
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+          if (t0 + k < L) hr[t0 + k] = Rg::mad(pa[k], hs, pu[k]);
+      }
+      carry = Rg::mad(cA, carry, cU);
+      cur = nxt;
+    }
+    __syncthreads();  // the totals buffers are reused by the next row
+  }
+}
+
 template <typename T>
 int launch_affine(const T* a, const T* bx, const T* h0, T* h, int64_t R, int64_t L, bool vec) {
   hipStream_t s = current_stream();
   constexpr int64_t CH = (int64_t)AS_THREADS * AS_K;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    cus = 256;
+  }
+  if (L > CH && R >= 8 * (int64_t)cus) {
+    // enough rows to fill the machine: one workgroup per row, carries stay on chip
+    const int64_t grid = R < ((int64_t)1 << 30) ? R : ((int64_t)1 << 30);
+    if (vec)
+      hipLaunchKernelGGL((affine_rows_kernel<T, AS_K, true>), dim3((unsigned)grid),
+                         dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L);
+    else
+      hipLaunchKernelGGL((affine_rows_kernel<T, AS_K, false>), dim3((unsigned)grid),
+                         dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L);
+    return check_launch("affine_rows_kernel");
+  }
   const int64_t nchunks = (L + CH - 1) / CH;
   const int64_t total = R * nchunks;
   const int64_t grid = total < 65536 ? total : 65536;

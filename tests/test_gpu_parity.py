@@ -103,6 +103,44 @@ def test_affine_f32_ragged(sw, B, D, L):
     assert_gate(st, f"affine f32 {B}x{D}x{L}")
 
 
+# Shapes with at least 2048 rows and rows longer than one 2048-step chunk run
+# the row-per-workgroup kernel (carry kept on chip); fewer rows run the
+# chunk-parallel look-back kernel.  L % 4 == 0 takes the 16-byte path.
+@pytest.mark.parametrize("L", [2 * 2048 + 4, 2 * 2048 + 37, 3 * 2048])
+def test_affine_i32_many_rows_bitexact(sw, L):
+    _say("case affine i32 many rows L", L)
+    inp = wl.affine_inputs_i32(2, 1100, L, 4000 + L, "odd")
+    h0 = wl.affine_inputs_i32(2, 1100, 1, 5000 + L, "h0")["h0"]
+    h = sw.affine_scan_i32(dev(inp["a"]), dev(inp["bx"]), dev(h0)).cpu().numpy()
+    assert np.array_equal(h, oracle.affine_scan_i32(inp["a"], inp["bx"], h0))
+    h = sw.affine_scan_i32(dev(inp["a"]), dev(inp["bx"])).cpu().numpy()
+    assert np.array_equal(h, oracle.affine_scan_i32(inp["a"], inp["bx"]))
+
+
+@pytest.mark.parametrize("L", [3 * 2048 + 4, 2048 + 1])
+def test_affine_f32_many_rows(sw, L):
+    _say("case affine f32 many rows L", L)
+    inp = wl.affine_inputs(3, 700, L, 6000 + L, with_h0=True)
+    st, _, _ = _affine_check(sw, inp["a"], inp["bx"], inp["h0"])
+    assert_gate(st, f"affine f32 3x700x{L}")
+
+
+def test_affine_long_workload_sampled(sw):
+    w = wl.workload("affine_f32_b1_d5120_l65536")
+    _say("case", w.name)
+    inp = w.inputs()
+    h = sw.affine_scan(dev(inp["a"]), dev(inp["bx"]))
+    rows = _sample_rows(w.B * w.D, 64, 98)
+    a2 = inp["a"].reshape(-1, w.L)[rows]
+    b2 = inp["bx"].reshape(-1, w.L)[rows]
+    got = h.reshape(-1, w.L)[torch.from_numpy(rows).to("cuda")].cpu().numpy()
+    ref, mag, sens = oracle.affine_scan(a2, b2, bounds=True)
+    st = fp_gate(got, ref, mag, sens)
+    _say("  h:", {k_: v for k_, v in st.items() if k_ != "first_bad"})
+    assert_gate(st, w.name)
+    assert bool(torch.isfinite(h).all())
+
+
 def test_affine_weighted_prefix(sw):
     """Sec. 6.6, Eq. (10): h_t = alpha_t h_{t-1} + beta_t through the same scan
     (alpha -> a, beta -> b with x = 1)."""

@@ -58,4 +58,4 @@ def test_workload_table():
     w = wl.workload("selective_bf16_b8_d1536_n16_l2048")
     assert (w.B, w.D, w.N, w.L, w.dtype) == (8, 1536, 16, 2048, "bf16")
     assert w.elems == 8 * 1536 * 16 * 2048
-    assert len(wl.WORKLOADS) == 5
+    assert len(wl.WORKLOADS) == 6
