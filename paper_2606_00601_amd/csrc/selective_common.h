@@ -1,5 +1,4 @@
-// selective_common.h -- helpers shared by the two layouts of the fused
-// selective scan (selective_scan.hip, selective_scan_rows.hip): raw-bits
+// selective_common.h -- helpers of the fused selective scan kernels: raw-bits
 // registers for fp32 / bf16 inputs and their exact widening to fp32.
 #pragma once
 
@@ -50,6 +49,30 @@ struct RawVec {
       }
     }
   }
+  // from a raw buffer resource at byte offset `off` (16- or 8-byte aligned);
+  // bytes outside the resource's range read as zero
+  __device__ __forceinline__ void load_buf(__amdgpu_buffer_rsrc_t rs, int32_t off) {
+    if constexpr (W % 4 == 0) {
+#pragma unroll
+      for (int q = 0; q < W / 4; ++q) {
+        const uint4 v =
+            __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 * q, 0, 0));
+        w[4 * q] = v.x;
+        w[4 * q + 1] = v.y;
+        w[4 * q + 2] = v.z;
+        w[4 * q + 3] = v.w;
+      }
+    } else {
+      static_assert(W % 2 == 0, "8-byte granularity");
+#pragma unroll
+      for (int q = 0; q < W / 2; ++q) {
+        const uint2 v =
+            __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs, off + 8 * q, 0, 0));
+        w[2 * q] = v.x;
+        w[2 * q + 1] = v.y;
+      }
+    }
+  }
   // element i as fp32 (bf16 widened exactly)
   __device__ __forceinline__ float get(int i) const {
     if constexpr (sizeof(IN) == 4) {
@@ -69,5 +92,13 @@ struct RawVec {
     }
   }
 };
+
+// Raw buffer resource over `bytes` bytes from `base` (stride 0, the gfx9
+// default data format): loads at byte offsets past the range return zero
+// instead of faulting.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
 
 }  // namespace sw

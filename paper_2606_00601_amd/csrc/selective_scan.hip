@@ -11,28 +11,36 @@
 //
 // Work per (b,d,t,n) is one exp2 plus four fp32 VALU operations against about
 // half a byte of HBM traffic: the kernel is bound by the VALU issue rate, not
-// by HBM, and is laid out to spend as few VALU slots per element as possible
-// and to keep the SIMDs issuing:
+// by HBM.  With at most two states per lane there are only about 1.5
+// wavefronts of independent work per SIMD at Mamba shapes, so every
+// wavefront has to keep its own SIMD issuing: the kernel is a software
+// pipeline in which nothing waits on a load issued shortly before.
 //   * one wavefront is one independent unit of work: 8 (b,d) rows x 8 lanes,
 //     each lane owning NPL = N/8 states of its row; there is no workgroup
 //     barrier anywhere;
-//   * per tile of T = 32 steps the wavefront stages delta and delta*x (fp32,
-//     widened once from bf16) and B_t, C_t in its own slice of LDS and reads
-//     them back with 16-byte LDS loads;
-//   * the per-lane loop does exp2(delta * A*log2e), (delta*x)*B, the state FMA
-//     and the C FMA into a per-lane partial of y_t;
-//   * the 8 partials of each y_t meet in LDS and are summed, with Dskip*x kept
-//     in registers, by the lane that stores y (16-byte stores along t);
-//   * global loads run two tiles ahead: raw bits go to registers and are
-//     widened only when staged; only the last, partial tile of a row takes the
-//     clamped and masked path.
+//   * a tile is T = 32 steps.  The wavefront widens the tile's delta, x, B
+//     and C (bf16 -> fp32 by a 16-bit shift, exact) and writes delta,
+//     delta*x and the [B, C] slot of every state group into its own LDS, in
+//     two alternating buffers: tile k+1 is staged while tile k is computed;
+//   * global loads run three tiles ahead (two raw register sets), so a load
+//     has two tiles of compute to arrive;
+//   * the compute runs over 4-step blocks and reads the operands of the
+//     block LA blocks ahead (across the tile boundary into the other
+//     buffer), so LDS latency is hidden behind the current block;
+//   * per step a lane does exp2(delta * A*log2e), (delta*x)*B, the state FMA
+//     and the C FMA into a per-lane partial of y_t, written to LDS per block;
+//   * the 8 partials of each y_t are summed, with Dskip*x, by the lane that
+//     stores y (16-byte stores along t) one tile later: the reads are issued
+//     before the next tile's first block and consumed after it.
+// LDS instructions of one wavefront execute in order, so the cross-lane
+// hand-offs through LDS need no hardware wait; compiler fences keep the
+// compiler from reordering them.
 // Load balance: the work is cut into tasks (8-row block, sequence chunk)
 // handed out by an atomic ticket in chunk-major order to a persistent grid of
 // wavefronts.  A task waits for the final state of the same rows' previous
 // chunk, published as self-validating 64-bit words; that chunk holds an
 // earlier ticket, so it is running or done, which guarantees forward
-// progress.  A SIMD that runs fewer wavefronts finishes its tasks sooner and
-// takes more, so the work spreads evenly over the machine.
+// progress.
 #include <stdlib.h>
 
 #include <type_traits>
@@ -47,6 +55,7 @@ constexpr int SS_G = 8;            // lanes per (b,d) row
 constexpr int SS_RPW = 64 / SS_G;  // rows per wavefront: 8
 constexpr int SS_T = 32;           // steps per tile
 constexpr int SS_TS = SS_T + 4;    // padded LDS row stride (16-byte aligned)
+constexpr int SS_NB = SS_T / 4;    // 4-step blocks per tile
 // B/C tile in LDS: per step t a row of 8 slots [B_{g*NPL..}, C_{g*NPL..}] of
 // 2*NPL floats, rows padded by 4 floats so that the staging writes of the 64
 // lanes (2 lanes per step) spread over all banks; a row itself is contiguous,
@@ -111,9 +120,33 @@ __device__ __forceinline__ void load_tile(TileRaw<IN, NPL>& r, const LanePtrs<IN
   }
 }
 
-// Order LDS writes and reads of different lanes of one wavefront: LDS
-// instructions of a wavefront complete in order, so this only keeps the
-// compiler from moving memory operations across the point.
+// Per-task buffer resources of the vector path: the 8 rows of x and delta
+// of the row block, and B and C of its batch.  Every tile, including a
+// sequence tail and the dummy tiles fetched past the end, is loaded with the
+// same vector loads: lanes past the range read zeros (masked when staging).
+// Equal load counts on every path let the compiler wait for exactly the
+// loads of the tile being staged and leave the later tiles in flight.
+struct TaskRsrc {
+  __amdgpu_buffer_rsrc_t x, dl, bm, cm;
+  int32_t row_off;  // byte offset of this lane's staging row and step tq in x / delta
+  int32_t bc_off;   // byte offset of this lane's B/C slice of tile 0
+};
+
+template <typename IN, int NPL>
+__device__ __forceinline__ void load_tile_buf(TileRaw<IN, NPL>& r, const TaskRsrc& rs, int N,
+                                              int64_t t0rel) {
+  constexpr int ES = (int)sizeof(IN);
+  const int32_t ts = (int32_t)t0rel * ES;
+  r.dl.load_buf(rs.dl, rs.row_off + ts);
+  r.xv.load_buf(rs.x, rs.row_off + ts);
+  r.bb.load_buf(rs.bm, rs.bc_off + ts * N);
+  r.cc.load_buf(rs.cm, rs.bc_off + ts * N);
+}
+
+// Compiler-level ordering point for the cross-lane hand-offs through LDS.
+// LDS instructions of a wavefront complete in issue order, so no hardware
+// wait is needed; the wavefront-scope fences only keep the compiler from
+// moving memory operations across this point.
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -122,6 +155,85 @@ __device__ __forceinline__ void wave_sync() {
 
 template <bool B_>
 using Flag = std::integral_constant<bool, B_>;
+template <int I_>
+using Int = std::integral_constant<int, I_>;
+
+// LDS of one wavefront.
+template <int NPL>
+struct Smem {
+  float dl[2][SS_RPW * SS_TS];            // delta, two tile buffers
+  float dx[2][SS_RPW * SS_TS];            // delta * x
+  float bc[2][SS_T * bc_stride<NPL>()];   // per step: [B_g.., C_g..] slot of every group g
+  float p[SS_RPW * SS_G * SS_TS];         // per-lane partials of y, one tile
+};
+
+// Read-ahead depth (4-step blocks) and number of rotating operand sets.
+template <int NPL>
+struct Pipe {
+  static constexpr int LA = NPL <= 2 ? 2 : 1;
+  static constexpr int NS = NPL <= 2 ? 4 : 2;
+  static_assert(SS_NB % NS == 0 && LA < NS, "operand sets must rotate evenly over a tile");
+};
+
+// Operands of one 4-step block for one lane.
+template <int NPL>
+struct Blk {
+  float dl[4], dx[4];
+  float bc[4][2 * NPL];  // B of the lane's states, then C
+};
+
+template <int NPL>
+__device__ __forceinline__ void read_blk(Blk<NPL>& k, const Smem<NPL>& sm, int buf, int r, int g,
+                                         int bi) {
+  const float4 a = *reinterpret_cast<const float4*>(&sm.dl[buf][r * SS_TS + 4 * bi]);
+  const float4 b = *reinterpret_cast<const float4*>(&sm.dx[buf][r * SS_TS + 4 * bi]);
+  k.dl[0] = a.x;
+  k.dl[1] = a.y;
+  k.dl[2] = a.z;
+  k.dl[3] = a.w;
+  k.dx[0] = b.x;
+  k.dx[1] = b.y;
+  k.dx[2] = b.z;
+  k.dx[3] = b.w;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float* src = &sm.bc[buf][(4 * bi + q) * bc_stride<NPL>() + g * (2 * NPL)];
+    if constexpr (NPL == 1) {
+      const float2 v = *reinterpret_cast<const float2*>(src);
+      k.bc[q][0] = v.x;
+      k.bc[q][1] = v.y;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 2 * NPL; j += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(src + j);
+        k.bc[q][j] = v.x;
+        k.bc[q][j + 1] = v.y;
+        k.bc[q][j + 2] = v.z;
+        k.bc[q][j + 3] = v.w;
+      }
+    }
+  }
+}
+
+// Four steps of the recurrence for the lane's NPL states; the partial
+// sum_j C h of each step goes to LDS.
+template <int NPL>
+__device__ __forceinline__ void compute_blk(const Blk<NPL>& k, const float (&Al)[NPL],
+                                            float (&hs)[NPL], float* __restrict__ pdst) {
+  float p4[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float p = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const float a = __builtin_amdgcn_exp2f(k.dl[q] * Al[j]);
+      hs[j] = __builtin_fmaf(a, hs[j], k.dx[q] * k.bc[q][j]);
+      p = j == 0 ? k.bc[q][NPL] * hs[0] : __builtin_fmaf(k.bc[q][NPL + j], hs[j], p);
+    }
+    p4[q] = p;
+  }
+  *reinterpret_cast<float4*>(pdst) = make_float4(p4[0], p4[1], p4[2], p4[3]);
+}
 
 template <typename IN, int NPL, bool VEC, bool NPADDED>
 __global__ __launch_bounds__(64) void selective_fwd_kernel(
@@ -134,10 +246,9 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
   constexpr int T = SS_T;
   constexpr int TS = SS_TS;
   constexpr int PER = 4 * NPL;
-  __shared__ __align__(16) float sDl[SS_RPW * TS];
-  __shared__ __align__(16) float sDx[SS_RPW * TS];
-  __shared__ __align__(16) float sBC[T * bc_stride<NPL>()];
-  __shared__ __align__(16) float sP[SS_RPW * SS_G * TS];
+  constexpr int LA = Pipe<NPL>::LA;
+  constexpr int NS = Pipe<NPL>::NS;
+  __shared__ __align__(16) Smem<NPL> sm;
 
   const int lane = threadIdx.x;
   const int r = lane / SS_G;      // row of this lane within the wavefront
@@ -145,11 +256,8 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
   const int tq = (lane % 8) * 4;  // staging and reduce: steps tq .. tq+3 of a tile
   const int btt = lane / 2;       // staging of B/C: step btt of a tile, slots 4*(lane%2)..+3
   const uint32_t st_inc = carry_status(epoch, CARRY_INC);
-  float* const sDl_w = &sDl[r * TS + tq];
-  float* const sDx_w = &sDx[r * TS + tq];
-  float* const sBC_w = &sBC[btt * bc_stride<NPL>() + 4 * (lane % 2) * (2 * NPL)];
-  float* const sP_w = &sP[(r * SS_G + g) * TS];
-  const float* const sP_r = &sP[(r * SS_G) * TS + tq];
+  float* const p_w = &sm.p[(r * SS_G + g) * TS];
+  const float* const p_r = &sm.p[(r * SS_G) * TS + tq];
 
   for (;;) {
     uint32_t tk = 0;
@@ -194,33 +302,94 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
       }
     }
 
+    TaskRsrc rs;
+    if constexpr (VEC) {
+      const int64_t rows = imin(SS_RPW, D - d0);
+      const int64_t row0 = b * D + d0;
+      rs.x = buffer_rsrc(x + row0 * L, (uint32_t)(rows * L * (int64_t)sizeof(IN)));
+      rs.dl = buffer_rsrc(delta + row0 * L, (uint32_t)(rows * L * (int64_t)sizeof(IN)));
+      rs.bm = buffer_rsrc(Bm + bc_off, (uint32_t)(L * N * (int64_t)sizeof(IN)));
+      rs.cm = buffer_rsrc(Cm + bc_off, (uint32_t)(L * N * (int64_t)sizeof(IN)));
+      rs.row_off = (int32_t)(((dcl - d0) * L + tq) * (int64_t)sizeof(IN));
+      rs.bc_off = (int32_t)(lane * PER * (int)sizeof(IN));
+    }
+
+    // a tile is full when it lies inside both the chunk and the sequence
+    auto is_full = [&](int kt) { return tb + (int64_t)(kt + 1) * T <= te; };
+    // Load tile kt.  The vector path loads every tile, including those past
+    // the end of the chunk, so that each call issues the same loads.
     auto fetch = [&](TileRaw<IN, NPL>& rr, int kt) {
       const int64_t t0 = tb + (int64_t)kt * T;
-      if (VEC && t0 + T <= L)
-        load_tile<true, NPADDED>(rr, lp, x, delta, Bm, Cm, bc_off, N, L, t0, lane);
-      else
+      if constexpr (VEC)
+        load_tile_buf(rr, rs, N, t0);
+      else if (kt < ntile)
         load_tile<false, NPADDED>(rr, lp, x, delta, Bm, Cm, bc_off, N, L, t0, lane);
     };
-    TileRaw<IN, NPL> ra, rbuf;
-    fetch(ra, 0);
-    if (ntile > 1) fetch(rbuf, 1);
-    float ydp[4] = {0.f, 0.f, 0.f, 0.f};  // Dskip*x of the tile awaiting its reduce
 
-    // y = Dskip*x + sum of the 8 partials of tile kt, stored along t
-    auto reduce = [&](int kt, auto full) {
+    // Widen (and, in a tail tile, mask) tile kt from `rr` into LDS buffer
+    // `buf`; yd gets Dskip*x of this lane's four staging steps.
+    auto stage = [&](const TileRaw<IN, NPL>& rr, int kt, int buf, float (&yd)[4], auto full) {
+      constexpr bool FULL = decltype(full)::value;
+      const int64_t t0 = tb + (int64_t)kt * T;
+      float dl4[4], dx4[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float dv = rr.dl.get(q), xv = rr.xv.get(q);
+        if constexpr (!FULL) {
+          if (t0 + tq + q >= te) dv = xv = 0.0f;  // identity step: a = 1, u = 0
+        }
+        dl4[q] = dv;
+        dx4[q] = dv * xv;
+        yd[q] = dsk * xv;
+      }
+      *reinterpret_cast<float4*>(&sm.dl[buf][r * TS + tq]) =
+          make_float4(dl4[0], dl4[1], dl4[2], dl4[3]);
+      *reinterpret_cast<float4*>(&sm.dx[buf][r * TS + tq]) =
+          make_float4(dx4[0], dx4[1], dx4[2], dx4[3]);
+      // this lane holds step btt = lane/2, states (lane%2)*4*NPL .. +4*NPL-1,
+      // i.e. slots 4*(lane%2) .. +3; one slot [B.., C..] is written at a time
+      const bool tmask = !FULL && t0 + btt >= te;
+      float* const bcw = &sm.bc[buf][btt * bc_stride<NPL>() + 4 * (lane % 2) * (2 * NPL)];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        float v[2 * NPL];
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+          float bv = rr.bb.get(k * NPL + j), cv = rr.cc.get(k * NPL + j);
+          if constexpr (NPADDED) {
+            if ((4 * (lane % 2) + k) * NPL + j >= N) bv = cv = 0.0f;
+          }
+          if constexpr (!FULL) {
+            if (tmask) bv = cv = 0.0f;
+          }
+          v[j] = bv;
+          v[NPL + j] = cv;
+        }
+        float* dst = bcw + k * (2 * NPL);
+        if constexpr (NPL == 1) {
+          *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 2 * NPL; j += 4)
+            *reinterpret_cast<float4*>(dst + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+        }
+      }
+    };
+
+    // y of tile kt: Dskip*x plus the 8 partials read into pr, stored along t
+    auto finish_reduce = [&](int kt, const float4 (&pr)[SS_G], const float (&yd)[4]) {
       const int64_t t = tb + (int64_t)kt * T + tq;
-      float4 s = make_float4(ydp[0], ydp[1], ydp[2], ydp[3]);
+      float4 s = make_float4(yd[0], yd[1], yd[2], yd[3]);
 #pragma unroll
       for (int gg = 0; gg < SS_G; ++gg) {
-        const float4 p = *reinterpret_cast<const float4*>(sP_r + gg * TS);
-        s.x += p.x;
-        s.y += p.y;
-        s.z += p.z;
-        s.w += p.w;
+        s.x += pr[gg].x;
+        s.y += pr[gg].y;
+        s.z += pr[gg].z;
+        s.w += pr[gg].w;
       }
       if (dok) {
         float* yr = y_row + (t - tq);
-        if constexpr (decltype(full)::value && VEC) {
+        if (VEC && is_full(kt)) {
           *reinterpret_cast<float4*>(yr) = s;
         } else {
           const float sv[4] = {s.x, s.y, s.z, s.w};
@@ -230,123 +399,76 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
         }
       }
     };
-
-    auto tile = [&](int kt, TileRaw<IN, NPL>& rr, auto full, bool prev_full) {
-      constexpr bool FULL = decltype(full)::value;
-      const int64_t t0 = tb + (int64_t)kt * T;
-      // stage: widen (and, in a tail tile, mask) and write this wavefront's LDS
-      float dl4[4], dx4[4], yd4[4];
+    auto read_partials = [&](float4 (&pr)[SS_G]) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float dv = rr.dl.get(q), xv = rr.xv.get(q);
-        if constexpr (!FULL) {
-          if (t0 + tq + q >= te) dv = xv = 0.0f;  // identity step: a = 1, u = 0
-        }
-        dl4[q] = dv;
-        dx4[q] = dv * xv;
-        yd4[q] = dsk * xv;
-      }
-      *reinterpret_cast<float4*>(sDl_w) = make_float4(dl4[0], dl4[1], dl4[2], dl4[3]);
-      *reinterpret_cast<float4*>(sDx_w) = make_float4(dx4[0], dx4[1], dx4[2], dx4[3]);
-      {
-        // this lane holds step btt = lane/2, states (lane%2)*4*NPL .. +4*NPL-1,
-        // i.e. slots 4*(lane%2) .. +3; one slot [B.., C..] is written at a time
-        const bool tmask = !FULL && t0 + btt >= te;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          float v[2 * NPL];
-#pragma unroll
-          for (int j = 0; j < NPL; ++j) {
-            float bv = rr.bb.get(k * NPL + j), cv = rr.cc.get(k * NPL + j);
-            if constexpr (NPADDED) {
-              if ((4 * (lane % 2) + k) * NPL + j >= N) bv = cv = 0.0f;
-            }
-            if constexpr (!FULL) {
-              if (tmask) bv = cv = 0.0f;
-            }
-            v[j] = bv;
-            v[NPL + j] = cv;
-          }
-          float* dst = sBC_w + k * (2 * NPL);
-          if constexpr (NPL == 1) {
-            *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
-          } else {
-#pragma unroll
-            for (int j = 0; j < 2 * NPL; j += 4)
-              *reinterpret_cast<float4*>(dst + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
-          }
-        }
-      }
-      // the registers are free again: fetch the tile two ahead
-      if (kt + 2 < ntile) fetch(rr, kt + 2);
-      if (kt > 0) {
-        if (prev_full)
-          reduce(kt - 1, Flag<true>());
-        else
-          reduce(kt - 1, Flag<false>());
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) ydp[q] = yd4[q];
-      wave_sync();
-
-      // recurrence over the tile
-#pragma unroll
-      for (int t4 = 0; t4 < T; t4 += 4) {
-        const float4 dlv = *reinterpret_cast<const float4*>(&sDl[r * TS + t4]);
-        const float4 dxv = *reinterpret_cast<const float4*>(&sDx[r * TS + t4]);
-        const float dls[4] = {dlv.x, dlv.y, dlv.z, dlv.w};
-        const float dxs[4] = {dxv.x, dxv.y, dxv.z, dxv.w};
-        float p4[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float bc[2 * NPL];
-          const float* src = &sBC[(t4 + q) * bc_stride<NPL>() + g * (2 * NPL)];
-          if constexpr (NPL == 1) {
-            const float2 v = *reinterpret_cast<const float2*>(src);
-            bc[0] = v.x;
-            bc[1] = v.y;
-          } else {
-#pragma unroll
-            for (int j = 0; j < 2 * NPL; j += 4) {
-              const float4 v = *reinterpret_cast<const float4*>(src + j);
-              bc[j] = v.x;
-              bc[j + 1] = v.y;
-              bc[j + 2] = v.z;
-              bc[j + 3] = v.w;
-            }
-          }
-          float p = 0.0f;
-#pragma unroll
-          for (int j = 0; j < NPL; ++j) {
-            const float a = __builtin_amdgcn_exp2f(dls[q] * Al[j]);
-            hs[j] = __builtin_fmaf(a, hs[j], dxs[q] * bc[j]);
-            p = __builtin_fmaf(bc[NPL + j], hs[j], p);
-          }
-          p4[q] = p;
-        }
-        *reinterpret_cast<float4*>(sP_w + t4) = make_float4(p4[0], p4[1], p4[2], p4[3]);
-      }
-      wave_sync();
+      for (int gg = 0; gg < SS_G; ++gg) pr[gg] = *reinterpret_cast<const float4*>(p_r + gg * TS);
     };
 
-    // a tile is full when it lies inside both the chunk and the sequence
-    auto is_full = [&](int kt) { return tb + (int64_t)(kt + 1) * T <= te; };
-    for (int kt = 0; kt < ntile; kt += 2) {
-      if (is_full(kt))
-        tile(kt, ra, Flag<true>(), kt > 0 && is_full(kt - 1));
-      else
-        tile(kt, ra, Flag<false>(), kt > 0 && is_full(kt - 1));
-      if (kt + 1 < ntile) {
+    TileRaw<IN, NPL> raw0, raw1;  // tile j is held in raw(j % 2)
+    Blk<NPL> ops[NS];             // block i of a tile uses ops[i % NS]
+    float ydc[4] = {0.f, 0.f, 0.f, 0.f};  // Dskip*x of the tile in compute
+    float ydp[4] = {0.f, 0.f, 0.f, 0.f};  // ... and of the tile awaiting its reduce
+
+    // Tile kt (buffer BUF = kt % 2): stage tile kt+1 from `rn` into the other
+    // buffer and refill `rn` with tile kt+3; issue the reads of tile kt-1's
+    // partials; compute the 8 blocks with reads LA blocks ahead, and finish
+    // tile kt-1's reduce after the first block.
+    auto tile = [&](int kt, TileRaw<IN, NPL>& rn, auto bufc) {
+      constexpr int BUF = decltype(bufc)::value;
+      const bool has_next = kt + 1 < ntile;
+      float ydn[4] = {0.f, 0.f, 0.f, 0.f};
+      wave_sync();
+      if (has_next) {
         if (is_full(kt + 1))
-          tile(kt + 1, rbuf, Flag<true>(), is_full(kt));
+          stage(rn, kt + 1, 1 - BUF, ydn, Flag<true>());
         else
-          tile(kt + 1, rbuf, Flag<false>(), is_full(kt));
+          stage(rn, kt + 1, 1 - BUF, ydn, Flag<false>());
       }
-    }
-    if (is_full(ntile - 1))
-      reduce(ntile - 1, Flag<true>());
+      fetch(rn, kt + 3);
+      float4 pr[SS_G];
+      if (kt > 0) read_partials(pr);
+      wave_sync();
+#pragma unroll
+      for (int bi = 0; bi < SS_NB; ++bi) {
+        const int nb = bi + LA;
+        if (nb < SS_NB)
+          read_blk(ops[nb % NS], sm, BUF, r, g, nb);
+        else if (has_next)
+          read_blk(ops[nb % NS], sm, 1 - BUF, r, g, nb - SS_NB);
+        // keep the read-ahead where it is: the scheduler would otherwise sink
+        // the reads next to their use and expose the LDS latency
+        __builtin_amdgcn_sched_barrier(0);
+        compute_blk(ops[bi % NS], Al, hs, p_w + 4 * bi);
+        if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, ydp);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        ydp[q] = ydc[q];
+        ydc[q] = ydn[q];
+      }
+    };
+
+    fetch(raw0, 0);
+    fetch(raw1, 1);
+    if (is_full(0))
+      stage(raw0, 0, 0, ydc, Flag<true>());
     else
-      reduce(ntile - 1, Flag<false>());
+      stage(raw0, 0, 0, ydc, Flag<false>());
+    fetch(raw0, 2);
+    wave_sync();
+#pragma unroll
+    for (int i = 0; i < LA; ++i) read_blk(ops[i], sm, 0, r, g, i);
+    for (int kt = 0; kt < ntile; kt += 2) {
+      tile(kt, raw1, Int<0>());
+      if (kt + 1 < ntile) tile(kt + 1, raw0, Int<1>());
+    }
+    {
+      wave_sync();
+      float4 pr[SS_G];
+      read_partials(pr);
+      finish_reduce(ntile - 1, pr, ydp);
+    }
     wave_sync();  // the next task rewrites this wavefront's LDS
 
     if (c + 1 < nchunks) {
@@ -381,15 +503,17 @@ int make_plan(int64_t B, int64_t D, int64_t L, Plan* p) {
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess || cus <= 0)
     return fail(SW_ERR_HIP, "device query failed: %s", hipGetErrorString(e));
-  // resident wavefronts per CU and tasks per wavefront (tuning knobs)
-  static const int waves_per_cu = env_int("SW_SS_WAVES_PER_CU", 6);
-  static const int tasks_per_wave = env_int("SW_SS_TASKS_PER_WAVE", 4);
+  // Resident wavefronts per CU and tasks per wavefront (tuning knobs, read
+  // per call).  One task per wavefront measured best at Mamba shapes: extra
+  // chunks only add waits on the previous chunk's carry.
+  const int waves_per_cu = env_int("SW_SS_WAVES_PER_CU", 6);
+  const int tasks_per_wave = env_int("SW_SS_TASKS_PER_WAVE", 1);
   p->ndb = (D + SS_RPW - 1) / SS_RPW;
   p->nrb = B * p->ndb;
   int64_t slots = (int64_t)cus * (waves_per_cu > 0 ? waves_per_cu : 6);
   if (slots > p->nrb) slots = p->nrb;  // no more wavefronts than independent chains
   const int64_t tiles = (L + SS_T - 1) / SS_T;
-  int64_t want = (slots * (tasks_per_wave > 0 ? tasks_per_wave : 4) + p->nrb - 1) / p->nrb;
+  int64_t want = (slots * (tasks_per_wave > 0 ? tasks_per_wave : 1) + p->nrb - 1) / p->nrb;
   const int64_t max_chunks = (tiles + 3) / 4;  // a chunk keeps at least 4 tiles
   if (want > max_chunks) want = max_chunks;
   if (want < 1) want = 1;
@@ -442,8 +566,13 @@ int launch_selective(const IN* x, const IN* delta, const float* A, const IN* Bm,
                      int64_t N, int64_t L, bool vec) {
   hipStream_t s = current_stream();
   const int n = (int)N;
-  // vector B/C loads need 16-byte aligned B and C (tile starts are then aligned)
-  const bool v = vec && ((uintptr_t)Bm % 16 == 0) && ((uintptr_t)Cm % 16 == 0);
+  // The vector path loads through buffer resources with 32-bit byte offsets:
+  // it needs 16-byte aligned B and C (tile starts are then aligned) and every
+  // offset of a task, including the tiles fetched past the end, below 2^31.
+  const int64_t es = (int64_t)sizeof(IN), pad = 4 * SS_T;
+  const bool fits = SS_RPW * (L + pad) * es < ((int64_t)1 << 31) &&
+                    (L + pad) * N * es < ((int64_t)1 << 31);
+  const bool v = vec && fits && ((uintptr_t)Bm % 16 == 0) && ((uintptr_t)Cm % 16 == 0);
   if (n <= 8) return launch_npl<IN, 1>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
   if (n <= 16) return launch_npl<IN, 2>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
   if (n <= 32) return launch_npl<IN, 4>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);

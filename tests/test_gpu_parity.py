@@ -240,6 +240,25 @@ def test_selective_reduces_to_bare_scan(sw):
     del rng
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_selective_chained_chunks_bitexact(sw, monkeypatch, dtype):
+    """Several sequence chunks per row, chained through the published exact
+    state, run the same per-step arithmetic as one chunk per row: the results
+    must be bit-identical, and within the oracle gate."""
+    _say("case selective chained chunks", dtype)
+    inp = wl.selective_inputs(2, 21, 16, 3001, 6060, dtype)
+    monkeypatch.setenv("SW_SS_TASKS_PER_WAVE", "1")
+    y1, h1 = _run_selective(sw, inp, dtype)
+    monkeypatch.setenv("SW_SS_TASKS_PER_WAVE", "16")  # 16 chunks of 192 steps per row
+    y2, h2 = _run_selective(sw, inp, dtype)
+    assert torch.equal(y1, y2) and torch.equal(h1, h2)
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                              inp["Dskip"], bounds=True)
+    assert_gate(fp_gate(y2.cpu().numpy(), o["y"], o["y_mag"], o["y_sens"]), "chained y")
+    assert_gate(fp_gate(h2.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]),
+                "chained h_last")
+
+
 # ------------------------------------------------------------ full-size workloads
 
 def _sample_rows(n_rows, k, seed):
