@@ -62,6 +62,8 @@ struct RawVec {
         w[4 * q + 2] = v.z;
         w[4 * q + 3] = v.w;
       }
+    } else if constexpr (W == 1) {
+      w[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
     } else {
       static_assert(W % 2 == 0, "8-byte granularity");
 #pragma unroll

@@ -560,6 +560,16 @@ int launch_npl(const IN* x, const IN* delta, const float* A, const IN* Bm, const
   return launch_cfg<IN, NPL, false, true>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, s);
 }
 
+}  // namespace
+
+bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es);
+template <typename IN>
+int launch_row16(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
+                 const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int64_t L,
+                 hipStream_t s);
+
+namespace {
+
 template <typename IN>
 int launch_selective(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
                      const float* Dskip, float* y, float* h_last, int64_t B, int64_t D,
@@ -573,6 +583,10 @@ int launch_selective(const IN* x, const IN* delta, const float* A, const IN* Bm,
   const bool fits = SS_RPW * (L + pad) * es < ((int64_t)1 << 31) &&
                     (L + pad) * N * es < ((int64_t)1 << 31);
   const bool v = vec && fits && ((uintptr_t)Bm % 16 == 0) && ((uintptr_t)Cm % 16 == 0);
+  // N = 16 on the vector path: one state per lane, 16-lane rows
+  // (selective_scan16.hip); SW_SS_LAYOUT=8 keeps the 8-lane layout.
+  if (v && env_int("SW_SS_LAYOUT", 16) == 16 && row16_fits(D, N, L, sizeof(IN)))
+    return launch_row16<IN>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, L, s);
   if (n <= 8) return launch_npl<IN, 1>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
   if (n <= 16) return launch_npl<IN, 2>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
   if (n <= 32) return launch_npl<IN, 4>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);

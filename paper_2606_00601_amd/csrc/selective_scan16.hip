@@ -1,0 +1,346 @@
+// selective_scan16.hip -- fused selective scan, forward, N = 16, on gfx950.
+//
+// The same operation as selective_scan.hip (the Mamba-style instance of the
+// affine recurrence, Sec. 1 and Sec. 3.1; chunk composition Eq. (7)):
+//   a_{t,n} = exp(delta_t A_n),  u_{t,n} = delta_t B_{t,n} x_t,
+//   h_{t,n} = a_{t,n} h_{t-1,n} + u_{t,n},
+//   y_t     = sum_n C_{t,n} h_{t,n} + Dskip x_t,
+// for the state size of Mamba (N = 16), laid out so that the machine is full
+// at Mamba shapes.  One lane owns ONE state of one (b,d) row and walks the
+// whole sequence; a row is a 16-lane DPP row, a wavefront holds 4 rows and a
+// workgroup 16 rows of one batch.  At B=8, D=1536 that is 3072 wavefronts,
+// three per SIMD, all doing the same work, so every SIMD has other
+// wavefronts to issue from while one waits, and none is left with extra work.
+//
+// Per step a lane issues exactly the method's work: delta*A*log2e, exp2,
+// (delta*x)*B, the state FMA and C*h -- four VALU operations and one
+// transcendental.  The per-row operands cost nothing per step:
+//   * delta and delta*x live in registers in a transposed layout: in a
+//     super-tile of 16*V steps (V = 16/sizeof(IN)), lane m of a row holds
+//     steps V*m .. V*m+V-1 (one 16-byte load per lane), and each step takes
+//     its value from lane m with a row_newbcast DPP operand of the multiply,
+//     i.e. for free;
+//   * B_{t,n} and C_{t,n} are shared by the 16 rows of the workgroup: the
+//     workgroup widens each 32-step tile once into LDS (three rotating
+//     buffers, one barrier per tile), transposed to [n][t] so that a lane
+//     reads its state's four steps with one 16-byte LDS read;
+//   * the 16 partials C_{t,n} h_{t,n} of a row meet in a per-wavefront LDS
+//     transpose and are summed one tile later: lane n adds 8 states over 4
+//     steps, the two halves of the row meet through a row_ror:8 DPP add, and
+//     the first 8 lanes add Dskip*x and store y (16-byte stores along t).
+// All global loads go through buffer resources and run ahead of use: a
+// super-tile of delta/x, two tiles of B/C; lanes past the end read zeros or
+// are masked.  There is no carry between workgroups: each workgroup walks
+// its rows over the whole sequence.
+#include <type_traits>
+
+#include "selective_common.h"
+
+namespace sw {
+
+namespace {
+
+constexpr int R16_N = 16;                   // states per row = lanes per DPP row
+constexpr int R16_WAVES = 4;                // wavefronts per workgroup
+constexpr int R16_RPW = 4;                  // rows per wavefront
+constexpr int R16_ROWS = R16_WAVES * R16_RPW;
+constexpr int R16_T = 32;                   // steps per tile
+constexpr int R16_NB = R16_T / 4;           // 4-step blocks per tile
+constexpr int R16_TS = R16_T + 4;           // LDS stride of one state's B (or C) tile row
+constexpr int R16_NBUF = 3;                 // B/C tile buffers
+constexpr int R16_PRS = R16_N * R16_TS + 32;  // partials: row stride (rows 32 banks apart)
+constexpr int R16_LA = 2;                   // read-ahead, in 4-step blocks
+constexpr int R16_NS = 4;                   // rotating operand sets
+constexpr float R16_LOG2E = 1.4426950408889634f;
+static_assert(R16_NB == 8 && R16_NB % R16_NS == 0 && R16_LA < R16_NS,
+              "operand sets must rotate over a tile");
+
+struct R16Smem {
+  float bc[R16_NBUF][2][R16_N * R16_TS];     // [buf][B, C][n * TS + t]
+  float p[R16_WAVES][R16_RPW * R16_PRS];     // per wavefront: [row][n * TS + t]
+};
+
+// Value of `v` in lane M of this lane's 16-lane row.
+template <int M>
+__device__ __forceinline__ float row_bcast(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x150 + M, 0xf, 0xf,
+                                         false));
+}
+
+// Value of `v` in lane n ^ 8 of this lane's 16-lane row (rotate by 8).
+__device__ __forceinline__ float row_ror8(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xf, 0xf, false));
+}
+
+__device__ __forceinline__ void wg_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+__device__ __forceinline__ void wave_order() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// B and C of one lane's state for one 4-step block.
+struct R16Ops {
+  float4 b, c;
+};
+
+template <typename IN>
+__global__ __launch_bounds__(256) void selective_row16_kernel(
+    const IN* __restrict__ x, const IN* __restrict__ delta, const float* __restrict__ A,
+    const IN* __restrict__ Bm, const IN* __restrict__ Cm, const float* __restrict__ Dskip,
+    float* __restrict__ y, float* __restrict__ h_last, int64_t D, int64_t L, int64_t ndb) {
+  constexpr int ES = (int)sizeof(IN);
+  constexpr int V = 16 / ES;              // steps a lane holds of a super-tile
+  constexpr int ST = R16_N * V;           // steps per super-tile
+  constexpr int TPS = ST / R16_T;         // tiles per super-tile
+  static_assert(TPS * R16_T == ST, "a super-tile is a whole number of tiles");
+  __shared__ __align__(16) R16Smem sm;
+
+  const int tid = threadIdx.x;
+  const int w = tid / 64, lane = tid % 64;
+  const int r = lane / R16_N, n = lane % R16_N;
+  const int64_t b = blockIdx.x / ndb;
+  const int64_t d0 = (blockIdx.x - b * ndb) * R16_ROWS;
+  const int64_t d = d0 + R16_RPW * w + r;
+  const bool dok = d < D;
+  const int64_t dcl = dok ? d : D - 1;  // rows past D compute a copy of row D-1, never stored
+  const int64_t rows = imin(R16_ROWS, D - d0);
+  const int64_t row0 = b * D + d0;
+
+  const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(x + row0 * L, (uint32_t)(rows * L * ES));
+  const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(delta + row0 * L, (uint32_t)(rows * L * ES));
+  const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(Bm + b * L * R16_N, (uint32_t)(L * R16_N * ES));
+  const __amdgpu_buffer_rsrc_t rc = buffer_rsrc(Cm + b * L * R16_N, (uint32_t)(L * R16_N * ES));
+  const int32_t lrow = (int32_t)((dcl - d0) * L * ES);  // byte offset of this lane's row
+
+  const float Al = A[dcl * R16_N + n] * R16_LOG2E;
+  const float dsk = Dskip ? Dskip[dcl] : 0.0f;
+  float h = 0.0f;
+
+  const int64_t nsup = (L + ST - 1) / ST;
+  const int64_t ntile = nsup * TPS;  // tiles past L are identity steps, never stored
+
+  // ---- B/C staging: thread tid widens steps tt = tid/8 of a tile, states
+  // 2*(tid%8) and 2*(tid%8)+1, from one B pair and one C pair.
+  const int stt = tid / 8, sn = 2 * (tid % 8);
+  RawVec<IN, 2> sbr[2], scr[2];  // raw pairs of tiles kt+1 and kt+2 (by tile parity)
+  auto fetch_bc = [&](RawVec<IN, 2>& rbv, RawVec<IN, 2>& rcv, int64_t kt) {
+    const int32_t off = (int32_t)(((kt * R16_T + stt) * R16_N + sn) * ES);
+    rbv.load_buf(rb, off);
+    rcv.load_buf(rc, off);
+  };
+  auto stage_bc = [&](const RawVec<IN, 2>& rbv, const RawVec<IN, 2>& rcv, int buf) {
+    float* bb = &sm.bc[buf][0][sn * R16_TS + stt];
+    float* cc = &sm.bc[buf][1][sn * R16_TS + stt];
+    bb[0] = rbv.get(0);
+    bb[R16_TS] = rbv.get(1);
+    cc[0] = rcv.get(0);
+    cc[R16_TS] = rcv.get(1);
+  };
+
+  // ---- delta / x of a super-tile: this lane's V steps starting at V*n
+  RawVec<IN, V> dlr, xr;  // raw bits of the next super-tile
+  float dl[V], dx[V];     // delta and delta*x of the current one
+  auto fetch_dx = [&](int64_t sup) {
+    const int32_t off = lrow + (int32_t)((sup * ST + V * n) * ES);
+    dlr.load_buf(rd, off);
+    xr.load_buf(rx, off);
+  };
+  auto widen_dx = [&](int64_t sup) {
+    const int64_t t0 = sup * ST + V * n;
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      float dv = dlr.get(k), xv = xr.get(k);
+      if (t0 + k >= L) dv = xv = 0.0f;  // identity step: a = 1, u = 0
+      dl[k] = dv;
+      dx[k] = dv * xv;
+    }
+  };
+
+  // ---- y: the 16 lanes of a row split the reduce of a tile: lane n sums
+  // states 8*(n/8) .. +7 over steps 4*(n%8) .. +3 with 16-byte LDS reads,
+  // the two halves meet through a row_ror:8 DPP add, and lanes n < 8 store.
+  const int rq = n % 8, rh = n / 8;
+  RawVec<IN, 4> yxr;  // raw x of those four steps, for the tile awaiting its reduce
+  auto fetch_yx = [&](int64_t kt) {
+    yxr.load_buf(rx, lrow + (int32_t)((kt * R16_T + 4 * rq) * ES));
+  };
+  float* const p_w = &sm.p[w][r * R16_PRS + n * R16_TS];
+  const float* const p_r = &sm.p[w][r * R16_PRS + 8 * rh * R16_TS + 4 * rq];
+  float* const y_row = y + (b * D + dcl) * L;
+
+  auto read_partials = [&](float4 (&pr)[8]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pr[i] = *reinterpret_cast<const float4*>(p_r + i * R16_TS);
+  };
+  auto finish_reduce = [&](int64_t kt, const float4 (&pr)[8], const float (&yx)[4]) {
+    float s4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      s4[0] += pr[i].x;
+      s4[1] += pr[i].y;
+      s4[2] += pr[i].z;
+      s4[3] += pr[i].w;
+    }
+    // add the other half of the row (lane n ^ 8), then Dskip*x
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      s4[q] = __builtin_fmaf(dsk, yx[q], s4[q] + row_ror8(s4[q]));
+    const int64_t t = kt * R16_T + 4 * rq;
+    if (dok && rh == 0 && t < L)
+      *reinterpret_cast<float4*>(y_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
+  };
+
+  auto read_ops = [&](R16Ops& o, int buf, int bi) {
+    o.b = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n * R16_TS + 4 * bi]);
+    o.c = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n * R16_TS + 4 * bi]);
+  };
+
+  // ---- prologue: delta/x of super-tile 0, B/C of tiles 0..2, y-x of tile 0
+  fetch_dx(0);
+  fetch_bc(sbr[0], scr[0], 0);
+  fetch_bc(sbr[1], scr[1], 1);
+  stage_bc(sbr[0], scr[0], 0);
+  fetch_bc(sbr[0], scr[0], 2);
+  fetch_yx(0);
+  wg_barrier();
+  R16Ops ops[R16_NS];
+#pragma unroll
+  for (int i = 0; i < R16_LA; ++i) read_ops(ops[i], 0, i);
+
+  float yx_prev[4] = {0.f, 0.f, 0.f, 0.f};  // x of the tile awaiting its reduce
+  int buf = 0;                             // B/C buffer of the tile being computed
+
+  // One tile: stage B/C of tile kt+1, issue the reads of tile kt-1's
+  // partials, wait for the workgroup, then compute the 8 blocks with the
+  // operands of block i+LA read ahead (into tile kt+1's buffer at the end).
+  auto tile = [&](int64_t kt, auto ttc) {
+    constexpr int TT = decltype(ttc)::value;  // tile within the super-tile
+    const int nbuf = buf == R16_NBUF - 1 ? 0 : buf + 1;
+    const bool has_next = kt + 1 < ntile;
+    stage_bc(sbr[(TT + 1) & 1], scr[(TT + 1) & 1], nbuf);
+    fetch_bc(sbr[(TT + 1) & 1], scr[(TT + 1) & 1], kt + 3);
+    float yx[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) yx[q] = yxr.get(q);
+    fetch_yx(kt + 1);
+    wg_barrier();
+    // this wavefront's own partials: after the barrier, so that the barrier
+    // only drains the staging writes
+    float4 pr[8];
+    if (kt > 0) read_partials(pr);
+#pragma unroll
+    for (int bi = 0; bi < R16_NB; ++bi) {
+      const int nb = bi + R16_LA;
+      if (nb < R16_NB)
+        read_ops(ops[nb % R16_NS], buf, nb);
+      else if (has_next)
+        read_ops(ops[nb % R16_NS], nbuf, nb - R16_NB);
+      __builtin_amdgcn_sched_barrier(0);
+      const R16Ops& o = ops[bi % R16_NS];
+      const float bq[4] = {o.b.x, o.b.y, o.b.z, o.b.w};
+      const float cq[4] = {o.c.x, o.c.y, o.c.z, o.c.w};
+      float p4[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        constexpr int S0 = TT * R16_T;  // step of the super-tile at block 0
+        const int s = S0 + 4 * bi + q;
+        float dlv, dxv;
+        // the source lane and register are compile-time constants
+        switch (s / V) {
+#define SW_R16_CASE(M)             \
+  case M:                          \
+    dlv = row_bcast<M>(dl[s % V]); \
+    dxv = row_bcast<M>(dx[s % V]); \
+    break;
+          SW_R16_CASE(0) SW_R16_CASE(1) SW_R16_CASE(2) SW_R16_CASE(3)
+          SW_R16_CASE(4) SW_R16_CASE(5) SW_R16_CASE(6) SW_R16_CASE(7)
+          SW_R16_CASE(8) SW_R16_CASE(9) SW_R16_CASE(10) SW_R16_CASE(11)
+          SW_R16_CASE(12) SW_R16_CASE(13) SW_R16_CASE(14) SW_R16_CASE(15)
+#undef SW_R16_CASE
+          default:
+            dlv = dxv = 0.0f;
+        }
+        const float a = __builtin_amdgcn_exp2f(dlv * Al);
+        h = __builtin_fmaf(a, h, dxv * bq[q]);
+        p4[q] = cq[q] * h;
+      }
+      *reinterpret_cast<float4*>(p_w + 4 * bi) = make_float4(p4[0], p4[1], p4[2], p4[3]);
+      if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, yx_prev);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) yx_prev[q] = yx[q];
+    buf = nbuf;
+    wave_order();  // this wavefront's partials are written before its next reads
+  };
+
+  for (int64_t sup = 0; sup < nsup; ++sup) {
+#pragma unroll
+    for (int tt = 0; tt < TPS; ++tt) {
+      // the delta/x registers switch to this super-tile at its first tile,
+      // and the next super-tile is loaded (every super-tile, so that each
+      // path has the same loads in flight)
+      if (tt == 0) {
+        widen_dx(sup);
+        fetch_dx(sup + 1);
+      }
+      switch (tt) {
+        case 0: tile(sup * TPS + 0, std::integral_constant<int, 0>()); break;
+        case 1: tile(sup * TPS + 1, std::integral_constant<int, 1>()); break;
+        case 2: if constexpr (TPS > 2) tile(sup * TPS + 2, std::integral_constant<int, 2>()); break;
+        case 3: if constexpr (TPS > 3) tile(sup * TPS + 3, std::integral_constant<int, 3>()); break;
+        default: break;
+      }
+    }
+  }
+  {
+    float4 pr[8];
+    read_partials(pr);
+    finish_reduce(ntile - 1, pr, yx_prev);
+  }
+  if (h_last && dok) h_last[(b * D + d) * R16_N + n] = h;
+}
+
+}  // namespace
+
+// True when the N = 16 layout can take the call: vector-aligned rows, and
+// every byte offset of a workgroup (including loads run ahead past the end)
+// below 2^31.
+bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
+  if (N != R16_N) return false;
+  const int64_t vstep = 16 / (int64_t)es;
+  if (L % vstep != 0) return false;
+  const int64_t pad = 4 * R16_N * vstep;
+  return R16_ROWS * (L + pad) * (int64_t)es < ((int64_t)1 << 31) &&
+         (L + pad) * R16_N * (int64_t)es < ((int64_t)1 << 31) && D > 0;
+}
+
+template <typename IN>
+int launch_row16(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
+                 const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int64_t L,
+                 hipStream_t s) {
+  const int64_t ndb = (D + R16_ROWS - 1) / R16_ROWS;
+  const int64_t grid = B * ndb;
+  if (grid >= ((int64_t)1 << 31))
+    return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
+  hipLaunchKernelGGL((selective_row16_kernel<IN>), dim3((unsigned)grid), dim3(256), 0, s, x,
+                     delta, A, Bm, Cm, Dskip, y, h_last, D, L, ndb);
+  return check_launch("selective_row16_kernel");
+}
+
+template int launch_row16<float>(const float*, const float*, const float*, const float*,
+                                 const float*, const float*, float*, float*, int64_t, int64_t,
+                                 int64_t, hipStream_t);
+template int launch_row16<uint16_t>(const uint16_t*, const uint16_t*, const float*,
+                                    const uint16_t*, const uint16_t*, const float*, float*,
+                                    float*, int64_t, int64_t, int64_t, hipStream_t);
+
+}  // namespace sw
