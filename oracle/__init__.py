@@ -79,6 +79,8 @@ def _load():
         lib.swo_selective_scan_f64.argtypes = [_vp] * 13 + [_i64, _i64, _i64, ctypes.c_int,
                                                             ctypes.c_int]
         lib.swo_selective_scan_f64.restype = ctypes.c_int
+        lib.swo_selective_scan_f32seq.argtypes = [_vp] * 9 + [_i64, _i64, _i64, ctypes.c_int]
+        lib.swo_selective_scan_f32seq.restype = ctypes.c_int
         _lib = lib
         return lib
 
@@ -191,21 +193,8 @@ def affine_prefix_i32(a, bx, h0=None):
     return A.view(np.int32), U.view(np.int32), h.view(np.int32)
 
 
-def selective_scan(x, delta, A, Bm, Cm, Dskip=None, rows=None, a_mode: int = 0,
-                   bounds: bool = False, threads: int = 0):
-    """Fused selective scan in fp64.
-
-    Shapes: ``x, delta`` (B, D, L); ``A`` (D, N); ``Bm, Cm`` (B, L, N);
-    ``Dskip`` (D,) or None.  All values are taken as given (fp32, or bf16
-    values already widened exactly to fp32).
-
-    ``rows``: optional 1-D array of flat row indices ``b*D + d``; only those
-    rows are evaluated and results have a leading axis of len(rows) instead
-    of (B, D).
-
-    Returns a dict with ``y`` and ``h_last``; with ``bounds=True`` also
-    ``y_mag, y_sens, h_mag, h_sens``.
-    """
+def _selective_rows(x, delta, A, Bm, Cm, Dskip, rows):
+    """Flatten the fused-scan inputs to the per-row layout of the C loops."""
     x = np.asarray(x)
     Bsz, D, L = x.shape
     N = np.asarray(A).shape[1]
@@ -234,21 +223,66 @@ def selective_scan(x, delta, A, Bm, Cm, Dskip=None, rows=None, a_mode: int = 0,
     Cs = _as(Cm, np.float32)
     if Bs.shape != (Bsz, L, N) or Cs.shape != (Bsz, L, N):
         raise ValueError("Bm and Cm must have shape (B, L, N)")
+    return dict(Bsz=Bsz, D=D, L=L, N=N, R=R, ridx=ridx, xs=xs, ds=ds, row_b=row_b, As=As,
+                Ds=Ds, Bs=Bs, Cs=Cs)
+
+
+def _unflatten(out, f):
+    if f["ridx"] is None:
+        for k in list(out):
+            out[k] = out[k].reshape((f["Bsz"], f["D"]) + out[k].shape[1:])
+    return out
+
+
+def selective_scan(x, delta, A, Bm, Cm, Dskip=None, rows=None, a_mode: int = 0,
+                   bounds: bool = False, threads: int = 0):
+    """Fused selective scan in fp64.
+
+    Shapes: ``x, delta`` (B, D, L); ``A`` (D, N); ``Bm, Cm`` (B, L, N);
+    ``Dskip`` (D,) or None.  All values are taken as given (fp32, or bf16
+    values already widened exactly to fp32).
+
+    ``rows``: optional 1-D array of flat row indices ``b*D + d``; only those
+    rows are evaluated and results have a leading axis of len(rows) instead
+    of (B, D).
+
+    ``a_mode=1`` rounds every ``a = exp(delta A)`` to fp32 before use.
+
+    Returns a dict with ``y`` and ``h_last``; with ``bounds=True`` also
+    ``y_mag, y_sens, h_mag, h_sens``.
+    """
+    f = _selective_rows(x, delta, A, Bm, Cm, Dskip, rows)
+    R, N, L = f["R"], f["N"], f["L"]
     y = np.empty((R, L), np.float64)
     h_last = np.empty((R, N), np.float64)
     ym = np.empty((R, L), np.float64) if bounds else None
     ys = np.empty((R, L), np.float64) if bounds else None
     hm = np.empty((R, N), np.float64) if bounds else None
     hs = np.empty((R, N), np.float64) if bounds else None
-    rc = _load().swo_selective_scan_f64(_p(xs), _p(ds), _p(As), _p(Bs), _p(Cs), _p(row_b),
-                                        _p(Ds), _p(y), _p(h_last), _p(ym), _p(ys), _p(hm),
-                                        _p(hs), R, N, L, int(a_mode), int(threads))
+    rc = _load().swo_selective_scan_f64(_p(f["xs"]), _p(f["ds"]), _p(f["As"]), _p(f["Bs"]),
+                                        _p(f["Cs"]), _p(f["row_b"]), _p(f["Ds"]), _p(y),
+                                        _p(h_last), _p(ym), _p(ys), _p(hm), _p(hs), R, N, L,
+                                        int(a_mode), int(threads))
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     out = {"y": y, "h_last": h_last}
     if bounds:
         out.update(y_mag=ym, y_sens=ys, h_mag=hm, h_sens=hs)
-    if ridx is None:
-        for k in list(out):
-            out[k] = out[k].reshape((Bsz, D) + out[k].shape[1:])
-    return out
+    return _unflatten(out, f)
+
+
+def selective_scan_seq32(x, delta, A, Bm, Cm, Dskip=None, rows=None, threads: int = 0):
+    """The fused form as a plain fp32 sequential loop (every operation rounded
+    to fp32 in the written order, libm ``expf``, no FMA).  Same arguments and
+    layout as :func:`selective_scan`; returns fp32 ``y`` and ``h_last``.  It
+    measures what a direct fp32 evaluation incurs against the fp64 loop."""
+    f = _selective_rows(x, delta, A, Bm, Cm, Dskip, rows)
+    R, N, L = f["R"], f["N"], f["L"]
+    y = np.empty((R, L), np.float32)
+    h_last = np.empty((R, N), np.float32)
+    rc = _load().swo_selective_scan_f32seq(_p(f["xs"]), _p(f["ds"]), _p(f["As"]), _p(f["Bs"]),
+                                           _p(f["Cs"]), _p(f["row_b"]), _p(f["Ds"]), _p(y),
+                                           _p(h_last), R, N, L, int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return _unflatten({"y": y, "h_last": h_last}, f)

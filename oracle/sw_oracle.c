@@ -296,3 +296,65 @@ int swo_selective_scan_f64(const float* x, const float* delta, const float* A, c
   run_rows(sel_rows, &c, R, nthreads);
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* The fused form as a plain fp32 sequential loop: the same loop as above with
+ * every quantity held and rounded in fp32, in the order written, with libm's
+ * expf and no FMA contraction (ISO C, -std=c11):
+ *
+ *   a = expf(delta_t * A_n);  u = (delta_t * x_t) * B_{t,n};
+ *   h = a * h + u;            y_t += C_{t,n} * h;   then y_t += Dskip * x_t.
+ *
+ * It is not a reference for the GPU result: it measures what a direct fp32
+ * evaluation of the recurrence incurs against the fp64 loop (the numerical
+ * characterisation of Sec. 6.5). */
+
+typedef struct {
+  const float *x, *delta, *A, *Bm, *Cm, *Dskip;
+  const int64_t* row_b;
+  float *y, *h_last;
+  int64_t N, L;
+} sel32_ctx;
+
+static void sel32_rows(int64_t r0, int64_t r1, const void* vctx) {
+  const sel32_ctx* c = (const sel32_ctx*)vctx;
+  const int64_t N = c->N, L = c->L;
+  for (int64_t r = r0; r < r1; r++) {
+    const float* x = c->x + r * L;
+    const float* dl = c->delta + r * L;
+    const float* Bm = c->Bm + c->row_b[r] * L * N;
+    const float* Cm = c->Cm + c->row_b[r] * L * N;
+    float* y = c->y + r * L;
+    for (int64_t t = 0; t < L; t++) y[t] = 0.0f;
+    for (int64_t n = 0; n < N; n++) {
+      const float An = c->A[r * N + n];
+      float h = 0.0f;
+      for (int64_t t = 0; t < L; t++) {
+        const float a = expf(dl[t] * An);
+        const float u = (dl[t] * x[t]) * Bm[t * N + n];
+        const float ah = a * h;
+        h = ah + u;
+        const float ch = Cm[t * N + n] * h;
+        y[t] = y[t] + ch;
+      }
+      if (c->h_last) c->h_last[r * N + n] = h;
+    }
+    if (c->Dskip) {
+      const float Dr = c->Dskip[r];
+      for (int64_t t = 0; t < L; t++) {
+        const float dx = Dr * x[t];
+        y[t] = y[t] + dx;
+      }
+    }
+  }
+}
+
+int swo_selective_scan_f32seq(const float* x, const float* delta, const float* A,
+                              const float* Bm, const float* Cm, const int64_t* row_b,
+                              const float* Dskip, float* y, float* h_last, int64_t R, int64_t N,
+                              int64_t L, int nthreads) {
+  if (!x || !delta || !A || !Bm || !Cm || !row_b || !y || R < 0 || N < 0 || L < 0) return 1;
+  sel32_ctx c = {x, delta, A, Bm, Cm, Dskip, row_b, y, h_last, N, L};
+  run_rows(sel32_rows, &c, R, nthreads);
+  return 0;
+}

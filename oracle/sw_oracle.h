@@ -40,6 +40,12 @@ int swo_selective_scan_f64(const float* x, const float* delta, const float* A, c
                            double* h_sens, int64_t R, int64_t N, int64_t L, int a_mode,
                            int nthreads);
 
+/* The fused form as a plain fp32 sequential loop (see sw_oracle.c). */
+int swo_selective_scan_f32seq(const float* x, const float* delta, const float* A,
+                              const float* Bm, const float* Cm, const int64_t* row_b,
+                              const float* Dskip, float* y, float* h_last, int64_t R, int64_t N,
+                              int64_t L, int nthreads);
+
 #ifdef __cplusplus
 }
 #endif

@@ -13,7 +13,10 @@ The paper prints no output values, so the oracle is pinned by:
   * for the fused form: exact rational brute force with a rounded to fp32,
     reduction to the bare recurrence, and the closed forms A = 0, a = 0
     (delta*A <= -800), B = 0 and a constant-parameter geometric series that
-    fixes exp(delta*A) (base e, sign as given).
+    fixes exp(delta*A) (base e, sign as given);
+  * for the plain fp32 loop of the fused form: a float32 replica of its
+    operation order (exact when a = 1), exactness on integer data, and the
+    a-priori rounding bound of a sequential fp32 recurrence.
 All of these run on the CPU.
 """
 import json
@@ -418,3 +421,57 @@ def test_threads_do_not_change_results():
     assert np.array_equal(one["y"], many["y"])
     assert oracle.threads_used(3, 100) == 3
     assert oracle.threads_used(8, 2) == 2
+
+
+# ------------------------------------------------------------ plain fp32 loop
+
+def test_seq32_matches_float32_replica_when_a_is_one():
+    """With A = 0 every a = expf(0) = 1 exactly, so the plain fp32 loop is fixed
+    bit for bit by its order of operations: u = (delta*x)*B, h = a*h + u,
+    y += C*h, then y += Dskip*x, each rounded to fp32, no FMA."""
+    rng = _rng(41)
+    B, D, N, L = 2, 3, 4, 40
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L)
+    A[:] = 0.0
+    got = oracle.selective_scan_seq32(x, delta, A, Bm, Cm, Dskip)
+    f = np.float32
+    for b in range(B):
+        for d in range(D):
+            y = [f(0.0)] * L
+            for n in range(N):
+                h = f(0.0)
+                for t in range(L):
+                    u = f(f(delta[b, d, t] * x[b, d, t]) * Bm[b, t, n])
+                    h = f(f(f(1.0) * h) + u)
+                    y[t] = f(y[t] + f(Cm[b, t, n] * h))
+                assert got["h_last"][b, d, n] == h
+            for t in range(L):
+                assert got["y"][b, d, t] == f(y[t] + f(Dskip[d] * x[b, d, t]))
+
+
+def test_seq32_exact_on_integer_data():
+    """Small-integer data keep every fp32 intermediate exact: the fp32 loop then
+    equals the fp64 loop exactly (A = 0)."""
+    rng = _rng(42)
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, 2, 3, 4, 64, dyadic=True)
+    A[:] = 0.0
+    Dskip = rng.integers(-4, 5, size=Dskip.shape).astype(np.float32)
+    s = oracle.selective_scan_seq32(x, delta, A, Bm, Cm, Dskip)
+    o = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip)
+    assert np.array_equal(s["y"].astype(np.float64), o["y"])
+    assert np.array_equal(s["h_last"].astype(np.float64), o["h_last"])
+
+
+def test_seq32_within_fp32_rounding_bound():
+    """A direct fp32 evaluation stays within a few units of 2^-24 (mag + sens)
+    of the fp64 loop: the a-priori bound of a sequential fp32 recurrence.  A
+    dropped term, a wrong index or a transposed operand would exceed it."""
+    rng = _rng(43)
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, 2, 5, 16, 700)
+    s = oracle.selective_scan_seq32(x, delta, A, Bm, Cm, Dskip)
+    o = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, bounds=True)
+    u = 2.0 ** -24
+    ey = np.abs(s["y"] - o["y"]) / (u * (o["y_mag"] + o["y_sens"]))
+    eh = np.abs(s["h_last"] - o["h_last"]) / (u * (o["h_mag"] + o["h_sens"]))
+    assert ey.max() <= 4.0 and eh.max() <= 4.0
+    assert np.any(s["y"] != o["y"])  # it is an fp32 evaluation, not the fp64 one

@@ -88,12 +88,17 @@ def affine_inputs_i32(B: int, D: int, L: int, seed: int, variant: str = "uniform
 
 
 def selective_inputs(B: int, D: int, N: int, L: int, seed: int, dtype: str = "f32",
-                     stress: bool = False) -> dict:
+                     stress: bool = False, growth: bool = False) -> dict:
     """Inputs of the fused selective scan; see the module docstring.
 
     Returns fp32 arrays ``x, delta, A, Bm, Cm, Dskip`` (the values both sides
     use) and, for ``dtype="bf16"``, the bf16 bits ``x_bf16, delta_bf16,
     Bm_bf16, Cm_bf16`` the kernel reads.
+
+    ``growth=True`` (with the stress recipe) draws A positive instead,
+    ``A = +exp(U[ln 1e-5, ln 1e-3])``, so that exp(delta*A) is slightly above
+    one and the states grow: the regime in which the exponential
+    parameterisation amplifies rounding (reported only, not a gated workload).
     """
     if dtype not in ("f32", "bf16"):
         raise ValueError(dtype)
@@ -105,7 +110,10 @@ def selective_inputs(B: int, D: int, N: int, L: int, seed: int, dtype: str = "f3
     z += m
     delta = _softplus(z).astype(np.float32)
     del z
-    A = (-np.exp(rng.uniform(np.log(lo), np.log(hi), size=(D, N)))).astype(np.float32)
+    if growth:
+        lo, hi = 1e-5, 1e-3
+    A = np.exp(rng.uniform(np.log(lo), np.log(hi), size=(D, N)))
+    A = (A if growth else -A).astype(np.float32)
     Bm = rng.standard_normal(size=(B, L, N)).astype(np.float32)
     Cm = rng.standard_normal(size=(B, L, N)).astype(np.float32)
     Dskip = rng.standard_normal(size=(D,)).astype(np.float32)
