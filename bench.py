@@ -33,12 +33,15 @@ DEFAULT_WORKLOAD = "selective_bf16_b8_d1536_n16_l2048"
 
 # MI355X figures used for the roofline
 HBM_PEAK_GBS = 8000.0            # HBM3E, 8 TB/s
-N_CU, SIMD_PER_CU, LANES_PER_SIMD, CLOCK_HZ = 256, 4, 16, 2.4e9
-# fp32 VALU issue peak without packed math: lane-instructions per second
-VALU_PEAK = N_CU * SIMD_PER_CU * LANES_PER_SIMD * CLOCK_HZ  # 3.93e13
-# issue slots the method needs per (b,d,t,n) element: delta*A' mul, exp2
-# (half rate: 2 slots), (delta*x)*B mul, state FMA, C FMA
-SLOTS_PER_ELEM = 6.0
+N_CU, SIMD_PER_CU, CLOCK_HZ = 256, 4, 2.4e9
+# fp32 vector peak 157.3 TFLOP/s = 256 CUs x 4 SIMDs x 32 lanes x 2.4 GHz fp32
+# operations (an FMA counted as one operation of two flops): 78.6e12 lane-slots/s
+FP32_LANES_PER_SIMD = 32
+VALU_PEAK = N_CU * SIMD_PER_CU * FP32_LANES_PER_SIMD * CLOCK_HZ  # 7.86e13
+# slots the method needs per (b,d,t,n) element: delta*A' mul, (delta*x)*B mul,
+# state FMA, C FMA (4 fp32 operations) and one exp2, a transcendental issued
+# at a quarter of the fp32 rate (4 slots)
+SLOTS_PER_ELEM = 8.0
 MALL_BYTES = 256 << 20
 
 
@@ -52,16 +55,26 @@ def algorithmic_bytes(w) -> int:
     return x_dl + bc + a_d + out
 
 
+def kernel_source_sha256() -> str:
+    """Hash of every kernel source and header (sorted by name)."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_00601_amd", "csrc")
+    for p in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        h.update(os.path.basename(p).encode())
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def measured_traffic(w):
     """HBM bytes per launch from the committed counter summary, if it was taken on
-    the current kernel source and this workload; else None."""
+    the current kernel sources and this workload; else None."""
     path = os.path.join(ROOT, "profiles", "selective_fwd_traffic.txt")
-    src = os.path.join(ROOT, "paper_2606_00601_amd", "csrc", "selective_scan.hip")
     if not os.path.exists(path):
         return None
-    import hashlib
-    with open(src, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()
+    sha = kernel_source_sha256()
     rec = {}
     with open(path) as f:
         for line in f:
@@ -191,6 +204,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--sets", type=int, default=0,
                     help="input sets rotated through (default: enough to exceed the MALL)")
+    ap.add_argument("--print-kernel-sha", action="store_true",
+                    help="print the hash of the kernel sources (for the traffic record) and exit")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, 5 times "
                          "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -201,6 +216,10 @@ def main(argv=None):
               "(rows shard across GPUs without communication; see the design notes).",
               file=sys.stderr)
         return 2
+
+    if args.print_kernel_sha:
+        print(kernel_source_sha256())
+        return 0
 
     import torch
 
@@ -291,10 +310,10 @@ def main(argv=None):
             "bound": "alu",
             "achieved": alu_achieved / 1e12,
             "peak": VALU_PEAK / 1e12,
-            "unit": "TVALU-slot/s",
+            "unit": "T fp32-lane-slot/s",
             "frac": alu_achieved / VALU_PEAK,
             "traffic": measured_traffic(w),
-            "kernel": "selective_fwd_kernel",
+            "kernel": ("selective_row16_kernel" if w.N == 16 else "selective_fwd_kernel"),
             "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
                               "median": float(np.median(per)) * 1e6},
             "slots_per_elem": SLOTS_PER_ELEM,
