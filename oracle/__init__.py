@@ -16,7 +16,10 @@ What each routine computes (see ``sw_oracle.c`` for the loops):
   them, ``h_t = A_{1:t} h_0 + U_{1:t}``.
 * ``compose`` / ``compose_u32``: Eq. (7) itself.
 * ``selective_scan``: the Mamba-style fused form (Sec. 1, Sec. 3.1) with
-  ``a = exp(delta A)``, ``u = delta B x``, ``y = sum_n C h + Dskip x``.
+  ``a = exp(delta A)``, ``u = delta B x``, ``y = sum_n C h + Dskip x``, and
+  the optional pieces of a Mamba block (delta bias and softplus, initial
+  state, output gate).
+* ``selective_scan_seq32``: the same as a plain fp32 sequential loop.
 """
 from __future__ import annotations
 
@@ -79,6 +82,9 @@ def _load():
         lib.swo_selective_scan_f64.argtypes = [_vp] * 13 + [_i64, _i64, _i64, ctypes.c_int,
                                                             ctypes.c_int]
         lib.swo_selective_scan_f64.restype = ctypes.c_int
+        lib.swo_selective_scan_ex_f64.argtypes = ([_vp] * 10 + [ctypes.c_int] + [_vp] * 6
+                                                  + [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int])
+        lib.swo_selective_scan_ex_f64.restype = ctypes.c_int
         lib.swo_selective_scan_f32seq.argtypes = [_vp] * 9 + [_i64, _i64, _i64, ctypes.c_int]
         lib.swo_selective_scan_f32seq.restype = ctypes.c_int
         _lib = lib
@@ -193,7 +199,7 @@ def affine_prefix_i32(a, bx, h0=None):
     return A.view(np.int32), U.view(np.int32), h.view(np.int32)
 
 
-def _selective_rows(x, delta, A, Bm, Cm, Dskip, rows):
+def _selective_rows(x, delta, A, Bm, Cm, Dskip, rows, z=None, delta_bias=None, h0=None):
     """Flatten the fused-scan inputs to the per-row layout of the C loops."""
     x = np.asarray(x)
     Bsz, D, L = x.shape
@@ -223,8 +229,16 @@ def _selective_rows(x, delta, A, Bm, Cm, Dskip, rows):
     Cs = _as(Cm, np.float32)
     if Bs.shape != (Bsz, L, N) or Cs.shape != (Bsz, L, N):
         raise ValueError("Bm and Cm must have shape (B, L, N)")
+    sel = slice(None) if ridx is None else ridx
+    zs = None if z is None else _as(np.asarray(z).reshape(Bsz * D, L)[sel], np.float32)
+    h0s = None if h0 is None else _as(np.asarray(h0).reshape(Bsz * D, N)[sel], np.float32)
+    if delta_bias is None:
+        dbs = None
+    else:
+        db = np.asarray(delta_bias, np.float32)
+        dbs = _as(np.tile(db, Bsz) if ridx is None else db[ridx % D], np.float32)
     return dict(Bsz=Bsz, D=D, L=L, N=N, R=R, ridx=ridx, xs=xs, ds=ds, row_b=row_b, As=As,
-                Ds=Ds, Bs=Bs, Cs=Cs)
+                Ds=Ds, Bs=Bs, Cs=Cs, zs=zs, dbs=dbs, h0s=h0s)
 
 
 def _unflatten(out, f):
@@ -235,7 +249,8 @@ def _unflatten(out, f):
 
 
 def selective_scan(x, delta, A, Bm, Cm, Dskip=None, rows=None, a_mode: int = 0,
-                   bounds: bool = False, threads: int = 0):
+                   bounds: bool = False, threads: int = 0, z=None, delta_bias=None, h0=None,
+                   delta_softplus: bool = False):
     """Fused selective scan in fp64.
 
     Shapes: ``x, delta`` (B, D, L); ``A`` (D, N); ``Bm, Cm`` (B, L, N);
@@ -248,10 +263,14 @@ def selective_scan(x, delta, A, Bm, Cm, Dskip=None, rows=None, a_mode: int = 0,
 
     ``a_mode=1`` rounds every ``a = exp(delta A)`` to fp32 before use.
 
+    Optional inputs of a Mamba block: ``delta_bias`` (D,) is added to delta,
+    ``delta_softplus`` then applies log(1 + exp(.)), ``h0`` (B, D, N) is the
+    initial state, and ``z`` (B, D, L) gates the output, y * z / (1 + e^-z).
+
     Returns a dict with ``y`` and ``h_last``; with ``bounds=True`` also
     ``y_mag, y_sens, h_mag, h_sens``.
     """
-    f = _selective_rows(x, delta, A, Bm, Cm, Dskip, rows)
+    f = _selective_rows(x, delta, A, Bm, Cm, Dskip, rows, z, delta_bias, h0)
     R, N, L = f["R"], f["N"], f["L"]
     y = np.empty((R, L), np.float64)
     h_last = np.empty((R, N), np.float64)
@@ -259,10 +278,12 @@ def selective_scan(x, delta, A, Bm, Cm, Dskip=None, rows=None, a_mode: int = 0,
     ys = np.empty((R, L), np.float64) if bounds else None
     hm = np.empty((R, N), np.float64) if bounds else None
     hs = np.empty((R, N), np.float64) if bounds else None
-    rc = _load().swo_selective_scan_f64(_p(f["xs"]), _p(f["ds"]), _p(f["As"]), _p(f["Bs"]),
-                                        _p(f["Cs"]), _p(f["row_b"]), _p(f["Ds"]), _p(y),
-                                        _p(h_last), _p(ym), _p(ys), _p(hm), _p(hs), R, N, L,
-                                        int(a_mode), int(threads))
+    rc = _load().swo_selective_scan_ex_f64(_p(f["xs"]), _p(f["ds"]), _p(f["As"]), _p(f["Bs"]),
+                                           _p(f["Cs"]), _p(f["row_b"]), _p(f["Ds"]),
+                                           _p(f["zs"]), _p(f["dbs"]), _p(f["h0s"]),
+                                           int(bool(delta_softplus)), _p(y), _p(h_last),
+                                           _p(ym), _p(ys), _p(hm), _p(hs), R, N, L,
+                                           int(a_mode), int(threads))
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     out = {"y": y, "h_last": h_last}

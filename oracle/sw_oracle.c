@@ -229,7 +229,15 @@ int swo_affine_prefix_u32(const uint32_t* a, const uint32_t* bx, const uint32_t*
  *
  * a_mode 0: a in fp64.  a_mode 1: a rounded to fp32 before use (isolates the
  * error that any fp32 implementation takes on by storing exp(delta A) in
- * fp32; used for the numerical characterisation of Sec. 6.5). */
+ * fp32; used for the numerical characterisation of Sec. 6.5).
+ *
+ * The optional inputs of a Mamba block (the production kernel the paper
+ * compares against fuses them; Sec. 1, Sec. 6.3), all NULL / 0 by default:
+ *   delta_bias[d]:  delta' = delta + delta_bias[d];
+ *   softplus:       delta' = log(1 + exp(delta'))  (log1p of exp in fp64);
+ *   h0[r, n]:       initial state h[-1] instead of zero (mag_0 = |h0|);
+ *   z[r, t]:        y_t <- y_t * silu(z_t), silu(z) = z / (1 + exp(-z)); the
+ *                   magnitude and sensitivity of y scale by |silu(z_t)|. */
 
 typedef struct {
   const float *x, *delta, *A, *Bm, *Cm, *Dskip;
@@ -237,6 +245,8 @@ typedef struct {
   double *y, *h_last, *y_mag, *y_sens, *h_mag, *h_sens;
   int64_t N, L;
   int a_mode;
+  const float *z, *delta_bias, *h0;
+  int softplus;
 } sel_ctx;
 
 static void sel_rows(int64_t r0, int64_t r1, const void* vctx) {
@@ -257,11 +267,15 @@ static void sel_rows(int64_t r0, int64_t r1, const void* vctx) {
     }
     for (int64_t n = 0; n < N; n++) {
       const double An = (double)c->A[r * N + n];
-      double h = 0.0, m = 0.0, s = 0.0;
+      double h = c->h0 ? (double)c->h0[r * N + n] : 0.0;
+      double m = fabs(h), s = 0.0;
       for (int64_t t = 0; t < L; t++) {
-        double a = exp((double)dl[t] * An);
+        double dv = (double)dl[t];
+        if (c->delta_bias) dv += (double)c->delta_bias[r];
+        if (c->softplus) dv = log1p(exp(dv));
+        double a = exp(dv * An);
         if (c->a_mode == 1) a = (double)(float)a;
-        const double u = (double)dl[t] * (double)x[t] * (double)Bm[t * N + n];
+        const double u = dv * (double)x[t] * (double)Bm[t * N + n];
         const double cc = (double)Cm[t * N + n];
         h = a * h + u;
         s = fabs(a) * (s + m);
@@ -281,7 +295,31 @@ static void sel_rows(int64_t r0, int64_t r1, const void* vctx) {
         if (ym) ym[t] += fabs(Dr * (double)x[t]);
       }
     }
+    if (c->z) {
+      const float* z = c->z + r * L;
+      for (int64_t t = 0; t < L; t++) {
+        const double zv = (double)z[t];
+        const double g = zv / (1.0 + exp(-zv));
+        y[t] *= g;
+        if (ym) ym[t] *= fabs(g);
+        if (ys) ys[t] *= fabs(g);
+      }
+    }
   }
+}
+
+int swo_selective_scan_ex_f64(const float* x, const float* delta, const float* A, const float* Bm,
+                              const float* Cm, const int64_t* row_b, const float* Dskip,
+                              const float* z, const float* delta_bias, const float* h0,
+                              int softplus, double* y, double* h_last, double* y_mag,
+                              double* y_sens, double* h_mag, double* h_sens, int64_t R, int64_t N,
+                              int64_t L, int a_mode, int nthreads) {
+  if (!x || !delta || !A || !Bm || !Cm || !row_b || !y || R < 0 || N < 0 || L < 0) return 1;
+  if (a_mode != 0 && a_mode != 1) return 1;
+  sel_ctx c = {x, delta, A, Bm, Cm, Dskip, row_b, y, h_last, y_mag, y_sens, h_mag, h_sens,
+               N, L, a_mode, z, delta_bias, h0, softplus != 0};
+  run_rows(sel_rows, &c, R, nthreads);
+  return 0;
 }
 
 int swo_selective_scan_f64(const float* x, const float* delta, const float* A, const float* Bm,
@@ -291,10 +329,9 @@ int swo_selective_scan_f64(const float* x, const float* delta, const float* A, c
                            int nthreads) {
   if (!x || !delta || !A || !Bm || !Cm || !row_b || !y || R < 0 || N < 0 || L < 0) return 1;
   if (a_mode != 0 && a_mode != 1) return 1;
-  sel_ctx c = {x, delta, A, Bm, Cm, Dskip, row_b, y, h_last, y_mag, y_sens, h_mag, h_sens,
-               N, L, a_mode};
-  run_rows(sel_rows, &c, R, nthreads);
-  return 0;
+  return swo_selective_scan_ex_f64(x, delta, A, Bm, Cm, row_b, Dskip, NULL, NULL, NULL, 0, y,
+                                   h_last, y_mag, y_sens, h_mag, h_sens, R, N, L, a_mode,
+                                   nthreads);
 }
 
 /* ------------------------------------------------------------------------ */

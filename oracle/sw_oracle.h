@@ -40,6 +40,15 @@ int swo_selective_scan_f64(const float* x, const float* delta, const float* A, c
                            double* h_sens, int64_t R, int64_t N, int64_t L, int a_mode,
                            int nthreads);
 
+/* The fused form with the optional Mamba-block inputs (z, delta_bias, h0,
+ * softplus; any may be NULL / 0), per row; see sw_oracle.c. */
+int swo_selective_scan_ex_f64(const float* x, const float* delta, const float* A, const float* Bm,
+                              const float* Cm, const int64_t* row_b, const float* Dskip,
+                              const float* z, const float* delta_bias, const float* h0,
+                              int softplus, double* y, double* h_last, double* y_mag,
+                              double* y_sens, double* h_mag, double* h_sens, int64_t R, int64_t N,
+                              int64_t L, int a_mode, int nthreads);
+
 /* The fused form as a plain fp32 sequential loop (see sw_oracle.c). */
 int swo_selective_scan_f32seq(const float* x, const float* delta, const float* A,
                               const float* Bm, const float* Cm, const int64_t* row_b,

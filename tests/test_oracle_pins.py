@@ -475,3 +475,116 @@ def test_seq32_within_fp32_rounding_bound():
     eh = np.abs(s["h_last"] - o["h_last"]) / (u * (o["h_mag"] + o["h_sens"]))
     assert ey.max() <= 4.0 and eh.max() <= 4.0
     assert np.any(s["y"] != o["y"])  # it is an fp32 evaluation, not the fp64 one
+
+
+# ------------------------------------------- optional inputs of a Mamba block
+
+def test_fused_h0_split_invariance():
+    """A scan of [0, L) equals a scan of [0, m) followed by a scan of [m, L)
+    started from the first part's final state: the initial state carries the
+    whole history (Sec. 3.2, the chunk-carry property).  Bit for bit on integer
+    data (A = 0: every state is exact in fp32); within the fp32 rounding of the
+    restart state on general data."""
+    rng = _rng(51)
+    B, D, N, L, m = 2, 3, 5, 120, 47
+
+    def split(x, delta, A, Bm, Cm, Dskip):
+        first = oracle.selective_scan(np.ascontiguousarray(x[:, :, :m]),
+                                      np.ascontiguousarray(delta[:, :, :m]), A,
+                                      np.ascontiguousarray(Bm[:, :m]),
+                                      np.ascontiguousarray(Cm[:, :m]), Dskip)
+        second = oracle.selective_scan(np.ascontiguousarray(x[:, :, m:]),
+                                       np.ascontiguousarray(delta[:, :, m:]), A,
+                                       np.ascontiguousarray(Bm[:, m:]),
+                                       np.ascontiguousarray(Cm[:, m:]), Dskip,
+                                       h0=first["h_last"].astype(np.float32))
+        return first, second
+
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L, dyadic=True)
+    A[:] = 0.0
+    Dskip = rng.integers(-3, 4, size=D).astype(np.float32)
+    full = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip)
+    first, second = split(x, delta, A, Bm, Cm, Dskip)
+    assert np.array_equal(first["h_last"].astype(np.float32), first["h_last"])  # exact in fp32
+    assert np.array_equal(np.concatenate([first["y"], second["y"]], axis=2), full["y"])
+    assert np.array_equal(second["h_last"], full["h_last"])
+
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L)
+    o = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, bounds=True)
+    first, second = split(x, delta, A, Bm, Cm, Dskip)
+    err = np.abs(second["y"] - o["y"][:, :, m:])
+    assert np.all(err <= 2.0 ** -23 * o["y_mag"][:, :, m:] + 1e-300)
+    # ignoring h0 would leave the restarted scan off by the decayed history
+    cold = oracle.selective_scan(np.ascontiguousarray(x[:, :, m:]),
+                                 np.ascontiguousarray(delta[:, :, m:]), A,
+                                 np.ascontiguousarray(Bm[:, m:]), np.ascontiguousarray(Cm[:, m:]),
+                                 Dskip)
+    assert np.abs(cold["y"][:, :, 0] - o["y"][:, :, m]).max() > 1e3 * err[:, :, 0].max()
+
+
+def test_fused_h0_closed_form():
+    """A = 0 (a = 1) and B = 0 (u = 0): the state stays h0 and
+    y_t = sum_n C_{t,n} h0_n + Dskip x_t exactly (integer data)."""
+    rng = _rng(52)
+    B, D, N, L = 2, 3, 4, 30
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L, dyadic=True)
+    A[:] = 0.0
+    Dskip = rng.integers(-3, 4, size=D).astype(np.float32)
+    h0 = rng.integers(-5, 6, size=(B, D, N)).astype(np.float32)
+    o = oracle.selective_scan(x, delta, A, np.zeros_like(Bm), Cm, Dskip, h0=h0, bounds=True)
+    ref = np.einsum("bln,bdn->bdl", Cm.astype(np.float64), h0.astype(np.float64)) \
+        + Dskip[None, :, None].astype(np.float64) * x
+    assert np.array_equal(o["y"], ref)
+    assert np.array_equal(o["h_last"], h0.astype(np.float64))
+    assert np.array_equal(o["h_mag"], np.abs(h0).astype(np.float64))
+
+
+def test_fused_delta_bias_is_an_addition():
+    """Without softplus, delta_bias[d] is added to delta: with dyadic data the
+    sum is exact in fp32, so it equals the plain loop on delta + bias."""
+    rng = _rng(53)
+    B, D, N, L = 2, 3, 4, 50
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L, dyadic=True)
+    bias = (2.0 ** rng.integers(-6, -2, size=D)).astype(np.float32)
+    o = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, delta_bias=bias)
+    ref = oracle.selective_scan(x, delta + bias[None, :, None], A, Bm, Cm, Dskip)
+    assert np.array_equal(o["y"], ref["y"]) and np.array_equal(o["h_last"], ref["h_last"])
+
+
+def test_fused_softplus_closed_forms():
+    """softplus(v) = log(1 + e^v): ln 2 at 0, v itself far above 0, e^v far
+    below.  N = 1, A = 0, x = B = C = 1, Dskip = 0 make y_t the running sum of
+    softplus(delta + bias), i.e. (t + 1) softplus(v) for constant v."""
+    L = 64
+    ones = np.ones((1, L, 1), np.float32)
+    x = np.ones((1, 1, L), np.float32)
+    A = np.zeros((1, 1), np.float32)
+    t = np.arange(1, L + 1, dtype=np.float64)
+    for v, sp in ((0.0, math.log(2.0)), (40.0, 40.0), (-40.0, math.exp(-40.0))):
+        # split v into delta + bias to exercise both
+        delta = np.full((1, 1, L), v / 2, np.float32)
+        bias = np.array([v / 2], np.float32)
+        o = oracle.selective_scan(x, delta, A, ones, ones, np.zeros(1, np.float32),
+                                  delta_bias=bias, delta_softplus=True)
+        np.testing.assert_allclose(o["y"][0, 0], t * sp, rtol=1e-14)
+
+
+def test_fused_output_gate():
+    """y <- y * silu(z), silu(z) = z / (1 + e^-z): zero at z = 0, z itself far
+    above 0, and silu(z) + silu(-z) = z tanh(z/2) (which a sign error in the
+    exponent turns into -z tanh(z/2))."""
+    rng = _rng(54)
+    B, D, N, L = 2, 3, 4, 40
+    x, delta, A, Bm, Cm, Dskip = _fused_inputs(rng, B, D, N, L)
+    plain = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, bounds=True)
+    zero = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, z=np.zeros_like(x), bounds=True)
+    assert not np.any(zero["y"]) and not np.any(zero["y_mag"])
+    big = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, z=np.full_like(x, 100.0))
+    assert np.array_equal(big["y"], 100.0 * plain["y"])
+    z = rng.standard_normal(size=x.shape).astype(np.float32) * 3
+    zp = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, z=z, bounds=True)
+    zm = oracle.selective_scan(x, delta, A, Bm, Cm, Dskip, z=-z)
+    z64 = z.astype(np.float64)
+    np.testing.assert_allclose(zp["y"] + zm["y"], plain["y"] * z64 * np.tanh(z64 / 2),
+                               rtol=1e-12, atol=1e-14 * plain["y_mag"].max())
+    assert np.all(zp["y_mag"] <= plain["y_mag"] * np.abs(z64) * (1 + 1e-15))
