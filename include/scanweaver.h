@@ -110,6 +110,45 @@ int sw_selective_scan_fwd_bf16(const uint16_t* x, const uint16_t* delta, const f
                                float* y, float* h_last, int64_t B, int64_t D, int64_t N,
                                int64_t L);
 
+/* Element types of sw_selective_scan_fwd_ex's arrays. */
+typedef enum sw_dtype {
+  SW_DTYPE_F32 = 0,  /* fp32 */
+  SW_DTYPE_BF16 = 1  /* bf16, as raw uint16 bit patterns */
+} sw_dtype;
+
+/* Flags of sw_selective_scan_fwd_ex. */
+enum { SW_DELTA_SOFTPLUS = 1 /* delta' = softplus(delta + delta_bias) */ };
+
+/*
+ * Fused selective scan, forward, with the optional inputs of a Mamba block
+ * (the production kernel the method is measured against fuses the same
+ * pieces; Sec. 1, Sec. 6.3).  With z, delta_bias, h0 NULL and flags 0 it is
+ * sw_selective_scan_fwd (in_dtype F32) or sw_selective_scan_fwd_bf16 (BF16):
+ *
+ *   delta'[b,d,t] = delta[b,d,t] + delta_bias[d]        (bias: 0 if NULL)
+ *                   then softplus(v) = log(1 + e^v)      if flags & SW_DELTA_SOFTPLUS
+ *   a = exp(delta' * A[d,n]),  u = delta' * Bm[b,t,n] * x[b,d,t]
+ *   h[b,d,-1,n] = h0[b,d,n]                              (0 if h0 is NULL)
+ *   h[b,d,t,n] = a * h[b,d,t-1,n] + u                    (Eq. (3))
+ *   y[b,d,t] = sum_n Cm[b,t,n] h[b,d,t,n] + Dskip[d] x[b,d,t]
+ *   y[b,d,t] *= silu(z[b,d,t]) = z / (1 + e^-z)           if z is not NULL
+ *   h_last[b,d,n] = h[b,d,L-1,n]
+ *
+ *   x, delta, z : (B, D, L) of in_dtype        Bm, Cm : (B, L, N) of in_dtype
+ *   A : (D, N) fp32      Dskip, delta_bias : (D) fp32 or NULL
+ *   h0, h_last : (B, D, N) fp32 or NULL        y : (B, D, L) of out_dtype
+ * bf16 y is the fp32 result rounded to nearest even.  Softplus and silu are
+ * evaluated in fp32 (a few ulps).  h0 may be the h_last of the previous
+ * chunk of the same sequences, which continues the scan across calls; with
+ * L == 0, h_last receives h0 (or zeros).  Unknown dtypes or flags:
+ * SW_ERR_INVALID_ARG.  Other conventions as for sw_selective_scan_fwd.
+ */
+int sw_selective_scan_fwd_ex(const void* x, const void* delta, const float* A, const void* Bm,
+                             const void* Cm, const float* Dskip, const void* z,
+                             const float* delta_bias, const float* h0, void* y, float* h_last,
+                             int64_t B, int64_t D, int64_t N, int64_t L, int in_dtype,
+                             int out_dtype, int flags);
+
 /* Stream used by the calling thread's subsequent calls (a hipStream_t;
  * NULL = the null stream).  Always SW_OK. */
 int sw_set_stream(void* hip_stream);

@@ -8,8 +8,10 @@ non-OK status; every step of the computation runs in the HIP kernels.
 * ``affine_scan(a, bx, h0=None)``: h_t = a_t h_{t-1} + bx_t over the last
   axis of (B, D, L) fp32 tensors (ScanWeaver Sec. 3.1, Eq. (3)).
 * ``affine_scan_i32(a, bx, h0=None)``: the same in the int32 wraparound ring.
-* ``selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None)``: the Mamba-style
-  fused form, returning ``(y, h_last)``; x/delta/Bm/Cm may be fp32 or bf16.
+* ``selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, ...)``: the
+  Mamba-style fused form, returning ``(y, h_last)``; x/delta/Bm/Cm may be fp32
+  or bf16, with optional output gate, delta bias and softplus, initial state
+  and bf16 y.
 """
 from __future__ import annotations
 
@@ -75,17 +77,24 @@ def affine_scan_i32(a, bx, h0=None, out=None):
 
 
 def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
-                       want_h_last=True):
+                       want_h_last=True, z=None, delta_bias=None, h0=None,
+                       delta_softplus=False, y_dtype=torch.float32):
     """Fused selective scan forward; returns ``(y, h_last)`` (h_last None if not wanted).
 
     x, delta: (B, D, L); A: (D, N) fp32; Bm, Cm: (B, L, N); Dskip: (D,) fp32 or None.
-    x, delta, Bm, Cm are all fp32 or all bf16; y and h_last are fp32.
+    x, delta, Bm, Cm (and z) are all fp32 or all bf16; h_last is fp32; y is
+    fp32 or bf16 (``y_dtype``).  Optional inputs of a Mamba block: ``z``
+    (B, D, L) gates the output by silu(z); ``delta_bias`` (D,) fp32 is added to
+    delta, then ``delta_softplus`` applies softplus; ``h0`` (B, D, N) fp32 is
+    the initial state (e.g. the h_last of the previous chunk).
     """
     if not isinstance(x, torch.Tensor) or x.dim() != 3:
         raise ValueError("x must be a (B, D, L) tensor")
     dt = x.dtype
     if dt not in (torch.float32, torch.bfloat16):
         raise TypeError("x must be float32 or bfloat16")
+    if y_dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("y_dtype must be float32 or bfloat16")
     B, D, L = x.shape
     _need(x, "x", dt)
     _need(delta, "delta", dt, (B, D, L))
@@ -97,10 +106,16 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
     _need(Cm, "Cm", dt, (B, L, N))
     if Dskip is not None:
         _need(Dskip, "Dskip", torch.float32, (D,))
+    if z is not None:
+        _need(z, "z", dt, (B, D, L))
+    if delta_bias is not None:
+        _need(delta_bias, "delta_bias", torch.float32, (D,))
+    if h0 is not None:
+        _need(h0, "h0", torch.float32, (B, D, N))
     if y is None:
-        y = torch.empty((B, D, L), dtype=torch.float32, device=x.device)
+        y = torch.empty((B, D, L), dtype=y_dtype, device=x.device)
     else:
-        _need(y, "y", torch.float32, (B, D, L))
+        _need(y, "y", y_dtype, (B, D, L))
     if want_h_last:
         if h_last is None:
             h_last = torch.empty((B, D, N), dtype=torch.float32, device=x.device)
@@ -108,10 +123,23 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
             _need(h_last, "h_last", torch.float32, (B, D, N))
     else:
         h_last = None
-    fn = lib().sw_selective_scan_fwd if dt == torch.float32 else lib().sw_selective_scan_fwd_bf16
-    where = "sw_selective_scan_fwd" if dt == torch.float32 else "sw_selective_scan_fwd_bf16"
+    from ._lib import SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32
+    in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
+    out_dt = SW_DTYPE_F32 if y_dtype == torch.float32 else SW_DTYPE_BF16
+    flags = SW_DELTA_SOFTPLUS if delta_softplus else 0
     with torch.cuda.device(x.device):
         _bind_stream(x.device)
-        check(fn(_ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(y),
-                 _ptr(h_last), B, D, N, L), where)
+        if z is None and delta_bias is None and h0 is None and not flags \
+                and out_dt == SW_DTYPE_F32:
+            fn = lib().sw_selective_scan_fwd if dt == torch.float32 \
+                else lib().sw_selective_scan_fwd_bf16
+            where = "sw_selective_scan_fwd" if dt == torch.float32 \
+                else "sw_selective_scan_fwd_bf16"
+            check(fn(_ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(y),
+                     _ptr(h_last), B, D, N, L), where)
+        else:
+            check(lib().sw_selective_scan_fwd_ex(
+                _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
+                _ptr(delta_bias), _ptr(h0), _ptr(y), _ptr(h_last), B, D, N, L, in_dt, out_dt,
+                flags), "sw_selective_scan_fwd_ex")
     return y, h_last

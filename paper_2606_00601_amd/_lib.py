@@ -16,6 +16,9 @@ SW_ERR_INVALID_ARG = 1
 SW_ERR_UNSUPPORTED = 2
 SW_ERR_HIP = 3
 SW_ERR_ALLOC = 4
+SW_DTYPE_F32 = 0
+SW_DTYPE_BF16 = 1
+SW_DELTA_SOFTPLUS = 1
 
 # name -> (restype, argtypes), mirroring include/scanweaver.h
 _vp, _i64, _int = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
@@ -25,6 +28,7 @@ SIGNATURES = {
     "sw_affine_scan_i32": (_int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64]),
     "sw_selective_scan_fwd": (_int, [_vp] * 8 + [_i64] * 4),
     "sw_selective_scan_fwd_bf16": (_int, [_vp] * 8 + [_i64] * 4),
+    "sw_selective_scan_fwd_ex": (_int, [_vp] * 11 + [_i64] * 4 + [_int] * 3),
     "sw_set_stream": (_int, [_vp]),
     "sw_get_stream": (_vp, []),
     "sw_status_string": (ctypes.c_char_p, [_int]),

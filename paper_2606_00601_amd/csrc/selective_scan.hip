@@ -67,7 +67,7 @@ constexpr float LOG2E = 1.4426950408889634f;
 // One lane's share of one tile's global inputs.
 template <typename IN, int NPL>
 struct TileRaw {
-  RawVec<IN, 4> dl, xv;        // its row, steps tq .. tq+3
+  RawVec<IN, 4> dl, xv, zv;    // its row, steps tq .. tq+3 (zv: z, or x when not gated)
   RawVec<IN, 4 * NPL> bb, cc;  // elements lane*4*NPL .. +4*NPL-1 of the (T, 8*NPL) tile
 };
 
@@ -76,6 +76,7 @@ template <typename IN>
 struct LanePtrs {
   const IN* dl;  // delta row of this lane's staging row, at step tq
   const IN* xv;  // x row, at step tq
+  const IN* zsrc;  // z (or x) base, element path
   int64_t bc;    // element offset of this lane's B/C slice in tile 0 (vector path)
   int64_t row;   // element offset of the staging row (element path)
 };
@@ -84,7 +85,7 @@ struct LanePtrs {
 // sequence and vector loads are allowed, so addresses need no clamping.
 // Otherwise elements are gathered one by one with steps clamped to L-1 and
 // padded states to N-1; the caller masks them when staging.
-template <bool FULL, bool NPADDED, typename IN, int NPL>
+template <bool FULL, bool NPADDED, bool OPT, typename IN, int NPL>
 __device__ __forceinline__ void load_tile(TileRaw<IN, NPL>& r, const LanePtrs<IN>& lp,
                                           const IN* __restrict__ x, const IN* __restrict__ delta,
                                           const IN* __restrict__ Bm, const IN* __restrict__ Cm,
@@ -102,6 +103,7 @@ __device__ __forceinline__ void load_tile(TileRaw<IN, NPL>& r, const LanePtrs<IN
       const int64_t t = imin(t0 + tq + k, L - 1);
       r.dl.set(k, Elt<IN>::raw(delta, lp.row + t));
       r.xv.set(k, Elt<IN>::raw(x, lp.row + t));
+      if constexpr (OPT) r.zv.set(k, Elt<IN>::raw(lp.zsrc, lp.row + t));
     }
   }
   if constexpr (FULL && !NPADDED) {
@@ -127,18 +129,20 @@ __device__ __forceinline__ void load_tile(TileRaw<IN, NPL>& r, const LanePtrs<IN
 // Equal load counts on every path let the compiler wait for exactly the
 // loads of the tile being staged and leave the later tiles in flight.
 struct TaskRsrc {
-  __amdgpu_buffer_rsrc_t x, dl, bm, cm;
+  __amdgpu_buffer_rsrc_t x, dl, bm, cm, z;
   int32_t row_off;  // byte offset of this lane's staging row and step tq in x / delta
   int32_t bc_off;   // byte offset of this lane's B/C slice of tile 0
 };
 
-template <typename IN, int NPL>
+// B and C are read as T*N consecutive elements: only for N == 8*NPL.
+template <bool OPT, typename IN, int NPL>
 __device__ __forceinline__ void load_tile_buf(TileRaw<IN, NPL>& r, const TaskRsrc& rs, int N,
                                               int64_t t0rel) {
   constexpr int ES = (int)sizeof(IN);
   const int32_t ts = (int32_t)t0rel * ES;
   r.dl.load_buf(rs.dl, rs.row_off + ts);
   r.xv.load_buf(rs.x, rs.row_off + ts);
+  if constexpr (OPT) r.zv.load_buf(rs.z, rs.row_off + ts);
   r.bb.load_buf(rs.bm, rs.bc_off + ts * N);
   r.cc.load_buf(rs.cm, rs.bc_off + ts * N);
 }
@@ -235,15 +239,19 @@ __device__ __forceinline__ void compute_blk(const Blk<NPL>& k, const float (&Al)
   *reinterpret_cast<float4*>(pdst) = make_float4(p4[0], p4[1], p4[2], p4[3]);
 }
 
-template <typename IN, int NPL, bool VEC, bool NPADDED>
+// OPT: the optional Mamba-block inputs (flags, z, delta bias) are read;
+// without it the kernel is the plain form (an initial state is always taken).
+template <typename IN, int NPL, bool VEC, bool NPADDED, bool OPT>
 __global__ __launch_bounds__(64) void selective_fwd_kernel(
     const IN* __restrict__ x, const IN* __restrict__ delta, const float* __restrict__ A,
     const IN* __restrict__ Bm, const IN* __restrict__ Cm, const float* __restrict__ Dskip,
-    float* __restrict__ y, float* __restrict__ h_last, int64_t D, int N, int64_t L, int64_t ndb,
+    const IN* __restrict__ z, const float* __restrict__ dbias, const float* __restrict__ h0,
+    void* __restrict__ yv, float* __restrict__ h_last, int64_t D, int N, int64_t L, int64_t ndb,
     int64_t nrb, int64_t Lc, int64_t nchunks, uint32_t ntasks,
     unsigned long long* __restrict__ carry, uint32_t* __restrict__ ticket, uint32_t tbase,
-    uint32_t epoch) {
+    uint32_t epoch, uint32_t flags_in) {
   constexpr int T = SS_T;
+  const uint32_t flags = OPT ? flags_in : 0u;
   constexpr int TS = SS_TS;
   constexpr int PER = 4 * NPL;
   constexpr int LA = Pipe<NPL>::LA;
@@ -280,17 +288,21 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
     lp.row = (b * D + dcl) * L;
     lp.dl = delta + lp.row + tq;
     lp.xv = x + lp.row + tq;
+    lp.zsrc = (flags & SEL_GATED) ? z : x;
     lp.bc = bc_off + lane * PER;
-    float* const y_row = y + (b * D + dcl) * L + tq;
+    const bool ybf = (flags & SEL_Y_BF16) != 0;
+    float* const y_row = static_cast<float*>(yv) + (b * D + dcl) * L + tq;
+    uint16_t* const y16_row = static_cast<uint16_t*>(yv) + (b * D + dcl) * L + tq;
     float Al[NPL], hs[NPL];
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
       const int n = g * NPL + j;
       const float av = A[dcl * N + (n < N ? n : N - 1)];
       Al[j] = n < N ? av * LOG2E : 0.0f;  // padded states: a = 1, u = 0 (B masked to 0)
-      hs[j] = 0.0f;
+      hs[j] = (c == 0 && h0 && n < N) ? h0[(b * D + dcl) * N + n] : 0.0f;
     }
     const float dsk = Dskip ? Dskip[dcl] : 0.0f;
+    const float dbv = (OPT && dbias) ? dbias[dcl] : 0.0f;
 
     if (c > 0) {  // state entering the chunk: the previous chunk's final state
       const unsigned long long* cw = carry + ((c - 1) * nrb + rb) * (64 * NPL) + lane * NPL;
@@ -310,6 +322,8 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
       rs.dl = buffer_rsrc(delta + row0 * L, (uint32_t)(rows * L * (int64_t)sizeof(IN)));
       rs.bm = buffer_rsrc(Bm + bc_off, (uint32_t)(L * N * (int64_t)sizeof(IN)));
       rs.cm = buffer_rsrc(Cm + bc_off, (uint32_t)(L * N * (int64_t)sizeof(IN)));
+      rs.z = buffer_rsrc(((flags & SEL_GATED) ? z : x) + row0 * L,
+                         (uint32_t)(rows * L * (int64_t)sizeof(IN)));
       rs.row_off = (int32_t)(((dcl - d0) * L + tq) * (int64_t)sizeof(IN));
       rs.bc_off = (int32_t)(lane * PER * (int)sizeof(IN));
     }
@@ -321,20 +335,27 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
     auto fetch = [&](TileRaw<IN, NPL>& rr, int kt) {
       const int64_t t0 = tb + (int64_t)kt * T;
       if constexpr (VEC)
-        load_tile_buf(rr, rs, N, t0);
+        load_tile_buf<OPT>(rr, rs, N, t0);
       else if (kt < ntile)
-        load_tile<false, NPADDED>(rr, lp, x, delta, Bm, Cm, bc_off, N, L, t0, lane);
+        load_tile<false, NPADDED, OPT>(rr, lp, x, delta, Bm, Cm, bc_off, N, L, t0, lane);
     };
 
     // Widen (and, in a tail tile, mask) tile kt from `rr` into LDS buffer
     // `buf`; yd gets Dskip*x of this lane's four staging steps.
-    auto stage = [&](const TileRaw<IN, NPL>& rr, int kt, int buf, float (&yd)[4], auto full) {
+    auto stage = [&](const TileRaw<IN, NPL>& rr, int kt, int buf, float (&yd)[4],
+                     float (&gt)[4], auto full) {
       constexpr bool FULL = decltype(full)::value;
       const int64_t t0 = tb + (int64_t)kt * T;
       float dl4[4], dx4[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         float dv = rr.dl.get(q), xv = rr.xv.get(q);
+        gt[q] = 1.0f;
+        if constexpr (OPT) {
+          dv += dbv;
+          if (flags & SEL_SOFTPLUS) dv = softplus_f32(dv);
+          if (flags & SEL_GATED) gt[q] = silu_f32(rr.zv.get(q));
+        }
         if constexpr (!FULL) {
           if (t0 + tq + q >= te) dv = xv = 0.0f;  // identity step: a = 1, u = 0
         }
@@ -376,26 +397,39 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
       }
     };
 
-    // y of tile kt: Dskip*x plus the 8 partials read into pr, stored along t
-    auto finish_reduce = [&](int kt, const float4 (&pr)[SS_G], const float (&yd)[4]) {
+    // y of tile kt: Dskip*x plus the 8 partials read into pr, times the gate,
+    // stored along t (fp32, or bf16 rounded to nearest even)
+    auto finish_reduce = [&](int kt, const float4 (&pr)[SS_G], const float (&yd)[4],
+                             const float (&gt)[4]) {
       const int64_t t = tb + (int64_t)kt * T + tq;
-      float4 s = make_float4(yd[0], yd[1], yd[2], yd[3]);
+      float sv[4] = {yd[0], yd[1], yd[2], yd[3]};
 #pragma unroll
       for (int gg = 0; gg < SS_G; ++gg) {
-        s.x += pr[gg].x;
-        s.y += pr[gg].y;
-        s.z += pr[gg].z;
-        s.w += pr[gg].w;
+        sv[0] += pr[gg].x;
+        sv[1] += pr[gg].y;
+        sv[2] += pr[gg].z;
+        sv[3] += pr[gg].w;
       }
-      if (dok) {
-        float* yr = y_row + (t - tq);
-        if (VEC && is_full(kt)) {
-          *reinterpret_cast<float4*>(yr) = s;
-        } else {
-          const float sv[4] = {s.x, s.y, s.z, s.w};
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (t + q < te) yr[q] = sv[q];
+      for (int q = 0; q < 4; ++q) sv[q] *= gt[q];
+      if (dok) {
+        if (VEC && is_full(kt)) {
+          if (ybf)
+            *reinterpret_cast<uint2*>(y16_row + (t - tq)) =
+                make_uint2(bf16_rne(sv[0]) | (bf16_rne(sv[1]) << 16),
+                           bf16_rne(sv[2]) | (bf16_rne(sv[3]) << 16));
+          else
+            *reinterpret_cast<float4*>(y_row + (t - tq)) = make_float4(sv[0], sv[1], sv[2], sv[3]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (t + q < te) {
+              if (ybf)
+                y16_row[t - tq + q] = (uint16_t)bf16_rne(sv[q]);
+              else
+                y_row[t - tq + q] = sv[q];
+            }
+          }
         }
       }
     };
@@ -408,6 +442,8 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
     Blk<NPL> ops[NS];             // block i of a tile uses ops[i % NS]
     float ydc[4] = {0.f, 0.f, 0.f, 0.f};  // Dskip*x of the tile in compute
     float ydp[4] = {0.f, 0.f, 0.f, 0.f};  // ... and of the tile awaiting its reduce
+    float gtc[4] = {1.f, 1.f, 1.f, 1.f};  // output gate of the tile in compute
+    float gtp[4] = {1.f, 1.f, 1.f, 1.f};  // ... and of the tile awaiting its reduce
 
     // Tile kt (buffer BUF = kt % 2): stage tile kt+1 from `rn` into the other
     // buffer and refill `rn` with tile kt+3; issue the reads of tile kt-1's
@@ -416,13 +452,13 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
     auto tile = [&](int kt, TileRaw<IN, NPL>& rn, auto bufc) {
       constexpr int BUF = decltype(bufc)::value;
       const bool has_next = kt + 1 < ntile;
-      float ydn[4] = {0.f, 0.f, 0.f, 0.f};
+      float ydn[4] = {0.f, 0.f, 0.f, 0.f}, gtn[4] = {1.f, 1.f, 1.f, 1.f};
       wave_sync();
       if (has_next) {
         if (is_full(kt + 1))
-          stage(rn, kt + 1, 1 - BUF, ydn, Flag<true>());
+          stage(rn, kt + 1, 1 - BUF, ydn, gtn, Flag<true>());
         else
-          stage(rn, kt + 1, 1 - BUF, ydn, Flag<false>());
+          stage(rn, kt + 1, 1 - BUF, ydn, gtn, Flag<false>());
       }
       fetch(rn, kt + 3);
       float4 pr[SS_G];
@@ -439,22 +475,24 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
         // the reads next to their use and expose the LDS latency
         __builtin_amdgcn_sched_barrier(0);
         compute_blk(ops[bi % NS], Al, hs, p_w + 4 * bi);
-        if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, ydp);
+        if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, ydp, gtp);
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         ydp[q] = ydc[q];
         ydc[q] = ydn[q];
+        gtp[q] = gtc[q];
+        gtc[q] = gtn[q];
       }
     };
 
     fetch(raw0, 0);
     fetch(raw1, 1);
     if (is_full(0))
-      stage(raw0, 0, 0, ydc, Flag<true>());
+      stage(raw0, 0, 0, ydc, gtc, Flag<true>());
     else
-      stage(raw0, 0, 0, ydc, Flag<false>());
+      stage(raw0, 0, 0, ydc, gtc, Flag<false>());
     fetch(raw0, 2);
     wave_sync();
 #pragma unroll
@@ -467,7 +505,7 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
       wave_sync();
       float4 pr[SS_G];
       read_partials(pr);
-      finish_reduce(ntile - 1, pr, ydp);
+      finish_reduce(ntile - 1, pr, ydp, gtp);
     }
     wave_sync();  // the next task rewrites this wavefront's LDS
 
@@ -529,82 +567,72 @@ int make_plan(int64_t B, int64_t D, int64_t L, Plan* p) {
 }
 
 template <typename IN, int NPL, bool VEC, bool NPADDED>
-int launch_cfg(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
-               const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int N,
-               int64_t L, hipStream_t s) {
+int launch_cfg(const SelArgs& a, hipStream_t s) {
+  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16;
   Plan p;
-  int st = make_plan(B, D, L, &p);
+  int st = make_plan(a.B, a.D, a.L, &p);
   if (st != SW_OK) return st;
   ScratchSession ss;
   const size_t words = (size_t)(p.nchunks - 1) * p.nrb * 64 * NPL;
   st = ss.reserve(words, p.ntasks + (uint32_t)p.grid, s);
   if (st != SW_OK) return st;
-  hipLaunchKernelGGL((selective_fwd_kernel<IN, NPL, VEC, NPADDED>), dim3((unsigned)p.grid),
-                     dim3(64), 0, s, x, delta, A, Bm, Cm, Dskip, y, h_last, D, N, L, p.ndb,
-                     p.nrb, p.Lc, p.nchunks, p.ntasks, ss.carry, ss.ticket, ss.ticket_base,
-                     ss.epoch);
+  const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.y_bf16 ? SEL_Y_BF16 : 0u) |
+                         (a.z ? SEL_GATED : 0u);
+  auto kern = opt ? selective_fwd_kernel<IN, NPL, VEC, NPADDED, true>
+                  : selective_fwd_kernel<IN, NPL, VEC, NPADDED, false>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)p.grid), dim3(64), 0, s, static_cast<const IN*>(a.x),
+                     static_cast<const IN*>(a.delta), a.A, static_cast<const IN*>(a.Bm),
+                     static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
+                     a.delta_bias, a.h0, a.y, a.h_last, a.D, (int)a.N, a.L, p.ndb, p.nrb, p.Lc,
+                     p.nchunks, p.ntasks, ss.carry, ss.ticket, ss.ticket_base, ss.epoch, flags);
   st = check_launch("selective_fwd_kernel");
   if (st != SW_OK) ss.invalidate();
   return st;
 }
 
+// The vector path reads a tile's B and C as T*N consecutive elements laid out
+// as T rows of 8*NPL slots, which holds only when N == 8*NPL; a padded N
+// gathers them element by element.
 template <typename IN, int NPL>
-int launch_npl(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
-               const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int N,
-               int64_t L, bool vec, hipStream_t s) {
-  const bool padded = N != SS_G * NPL;
-  if (vec && !padded)
-    return launch_cfg<IN, NPL, true, false>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, s);
-  if (vec)
-    return launch_cfg<IN, NPL, true, true>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, s);
-  return launch_cfg<IN, NPL, false, true>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, s);
+int launch_npl(const SelArgs& a, bool vec, hipStream_t s) {
+  const bool padded = a.N != SS_G * NPL;
+  if (vec && !padded) return launch_cfg<IN, NPL, true, false>(a, s);
+  return launch_cfg<IN, NPL, false, true>(a, s);
 }
 
 }  // namespace
 
 bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es);
 template <typename IN>
-int launch_row16(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
-                 const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int64_t L,
-                 hipStream_t s);
+int launch_row16(const SelArgs& a, hipStream_t s);
 
 namespace {
 
 template <typename IN>
-int launch_selective(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
-                     const float* Dskip, float* y, float* h_last, int64_t B, int64_t D,
-                     int64_t N, int64_t L, bool vec) {
+int launch_selective(const SelArgs& a) {
   hipStream_t s = current_stream();
-  const int n = (int)N;
+  const int64_t N = a.N, L = a.L;
   // The vector path loads through buffer resources with 32-bit byte offsets:
   // it needs 16-byte aligned B and C (tile starts are then aligned) and every
   // offset of a task, including the tiles fetched past the end, below 2^31.
   const int64_t es = (int64_t)sizeof(IN), pad = 4 * SS_T;
   const bool fits = SS_RPW * (L + pad) * es < ((int64_t)1 << 31) &&
                     (L + pad) * N * es < ((int64_t)1 << 31);
-  const bool v = vec && fits && ((uintptr_t)Bm % 16 == 0) && ((uintptr_t)Cm % 16 == 0);
+  const bool v = a.vec && fits && ((uintptr_t)a.Bm % 16 == 0) && ((uintptr_t)a.Cm % 16 == 0);
   // N = 16 on the vector path: one state per lane, 16-lane rows
   // (selective_scan16.hip); SW_SS_LAYOUT=8 keeps the 8-lane layout.
-  if (v && env_int("SW_SS_LAYOUT", 16) == 16 && row16_fits(D, N, L, sizeof(IN)))
-    return launch_row16<IN>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, L, s);
-  if (n <= 8) return launch_npl<IN, 1>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
-  if (n <= 16) return launch_npl<IN, 2>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
-  if (n <= 32) return launch_npl<IN, 4>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
-  return launch_npl<IN, 8>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, n, L, v, s);
+  if (v && env_int("SW_SS_LAYOUT", 16) == 16 && row16_fits(a.D, N, L, sizeof(IN)))
+    return launch_row16<IN>(a, s);
+  if (N <= 8) return launch_npl<IN, 1>(a, v, s);
+  if (N <= 16) return launch_npl<IN, 2>(a, v, s);
+  if (N <= 32) return launch_npl<IN, 4>(a, v, s);
+  return launch_npl<IN, 8>(a, v, s);
 }
 
 }  // namespace
 
-int selective_fwd_f32(const float* x, const float* delta, const float* A, const float* Bm,
-                      const float* Cm, const float* Dskip, float* y, float* h_last, int64_t B,
-                      int64_t D, int64_t N, int64_t L, bool vec) {
-  return launch_selective<float>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, vec);
-}
-
-int selective_fwd_bf16(const uint16_t* x, const uint16_t* delta, const float* A,
-                       const uint16_t* Bm, const uint16_t* Cm, const float* Dskip, float* y,
-                       float* h_last, int64_t B, int64_t D, int64_t N, int64_t L, bool vec) {
-  return launch_selective<uint16_t>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, vec);
+int selective_fwd(const SelArgs& a) {
+  return a.bf16_in ? launch_selective<uint16_t>(a) : launch_selective<float>(a);
 }
 
 }  // namespace sw

@@ -91,12 +91,17 @@ struct R16Ops {
   float4 b, c;
 };
 
-template <typename IN>
+// OPT: the optional Mamba-block inputs (flags, z, delta bias) are read;
+// without it the kernel is the plain form (an initial state is always taken).
+template <typename IN, bool OPT>
 __global__ __launch_bounds__(256) void selective_row16_kernel(
     const IN* __restrict__ x, const IN* __restrict__ delta, const float* __restrict__ A,
     const IN* __restrict__ Bm, const IN* __restrict__ Cm, const float* __restrict__ Dskip,
-    float* __restrict__ y, float* __restrict__ h_last, int64_t D, int64_t L, int64_t ndb) {
+    const IN* __restrict__ z, const float* __restrict__ dbias, const float* __restrict__ h0,
+    void* __restrict__ yv, float* __restrict__ h_last, int64_t D, int64_t L, int64_t ndb,
+    uint32_t flags_in) {
   constexpr int ES = (int)sizeof(IN);
+  const uint32_t flags = OPT ? flags_in : 0u;
   constexpr int V = 16 / ES;              // steps a lane holds of a super-tile
   constexpr int ST = R16_N * V;           // steps per super-tile
   constexpr int TPS = ST / R16_T;         // tiles per super-tile
@@ -118,11 +123,17 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(delta + row0 * L, (uint32_t)(rows * L * ES));
   const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(Bm + b * L * R16_N, (uint32_t)(L * R16_N * ES));
   const __amdgpu_buffer_rsrc_t rc = buffer_rsrc(Cm + b * L * R16_N, (uint32_t)(L * R16_N * ES));
+  // the gate's input; without a gate (OPT set) the same loads read x (cached),
+  // so that every path of one instantiation issues the same loads
+  const __amdgpu_buffer_rsrc_t rz =
+      buffer_rsrc(((flags & SEL_GATED) ? z : x) + row0 * L, (uint32_t)(rows * L * ES));
   const int32_t lrow = (int32_t)((dcl - d0) * L * ES);  // byte offset of this lane's row
 
   const float Al = A[dcl * R16_N + n] * R16_LOG2E;
   const float dsk = Dskip ? Dskip[dcl] : 0.0f;
-  float h = 0.0f;
+  const float dbv = (OPT && dbias) ? dbias[dcl] : 0.0f;
+  const bool ybf = (flags & SEL_Y_BF16) != 0;
+  float h = h0 ? h0[(b * D + dcl) * R16_N + n] : 0.0f;
 
   const int64_t nsup = (L + ST - 1) / ST;
   const int64_t ntile = nsup * TPS;  // tiles past L are identity steps, never stored
@@ -158,6 +169,10 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
 #pragma unroll
     for (int k = 0; k < V; ++k) {
       float dv = dlr.get(k), xv = xr.get(k);
+      if constexpr (OPT) {
+        dv += dbv;
+        if (flags & SEL_SOFTPLUS) dv = softplus_f32(dv);
+      }
       if (t0 + k >= L) dv = xv = 0.0f;  // identity step: a = 1, u = 0
       dl[k] = dv;
       dx[k] = dv * xv;
@@ -168,19 +183,23 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   // states 8*(n/8) .. +7 over steps 4*(n%8) .. +3 with 16-byte LDS reads,
   // the two halves meet through a row_ror:8 DPP add, and lanes n < 8 store.
   const int rq = n % 8, rh = n / 8;
-  RawVec<IN, 4> yxr;  // raw x of those four steps, for the tile awaiting its reduce
+  RawVec<IN, 4> yxr, yzr;  // raw x and z of those four steps, for the tile awaiting its reduce
   auto fetch_yx = [&](int64_t kt) {
-    yxr.load_buf(rx, lrow + (int32_t)((kt * R16_T + 4 * rq) * ES));
+    const int32_t off = lrow + (int32_t)((kt * R16_T + 4 * rq) * ES);
+    yxr.load_buf(rx, off);
+    if constexpr (OPT) yzr.load_buf(rz, off);
   };
   float* const p_w = &sm.p[w][r * R16_PRS + n * R16_TS];
   const float* const p_r = &sm.p[w][r * R16_PRS + 8 * rh * R16_TS + 4 * rq];
-  float* const y_row = y + (b * D + dcl) * L;
+  float* const y_row = static_cast<float*>(yv) + (b * D + dcl) * L;
+  uint16_t* const y16_row = static_cast<uint16_t*>(yv) + (b * D + dcl) * L;
 
   auto read_partials = [&](float4 (&pr)[8]) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) pr[i] = *reinterpret_cast<const float4*>(p_r + i * R16_TS);
   };
-  auto finish_reduce = [&](int64_t kt, const float4 (&pr)[8], const float (&yx)[4]) {
+  auto finish_reduce = [&](int64_t kt, const float4 (&pr)[8], const float (&yx)[4],
+                           const float (&gt)[4]) {
     float s4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -192,10 +211,16 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     // add the other half of the row (lane n ^ 8), then Dskip*x
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      s4[q] = __builtin_fmaf(dsk, yx[q], s4[q] + row_ror8(s4[q]));
+      s4[q] = __builtin_fmaf(dsk, yx[q], s4[q] + row_ror8(s4[q])) * gt[q];
     const int64_t t = kt * R16_T + 4 * rq;
-    if (dok && rh == 0 && t < L)
-      *reinterpret_cast<float4*>(y_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
+    if (dok && rh == 0 && t < L) {
+      if (ybf)
+        *reinterpret_cast<uint2*>(y16_row + t) =
+            make_uint2(bf16_rne(s4[0]) | (bf16_rne(s4[1]) << 16),
+                       bf16_rne(s4[2]) | (bf16_rne(s4[3]) << 16));
+      else
+        *reinterpret_cast<float4*>(y_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
+    }
   };
 
   auto read_ops = [&](R16Ops& o, int buf, int bi) {
@@ -216,6 +241,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   for (int i = 0; i < R16_LA; ++i) read_ops(ops[i], 0, i);
 
   float yx_prev[4] = {0.f, 0.f, 0.f, 0.f};  // x of the tile awaiting its reduce
+  float gt_prev[4] = {1.f, 1.f, 1.f, 1.f};  // ... and its output gate
   int buf = 0;                             // B/C buffer of the tile being computed
 
   // One tile: stage B/C of tile kt+1, issue the reads of tile kt-1's
@@ -227,9 +253,12 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     const bool has_next = kt + 1 < ntile;
     stage_bc(sbr[(TT + 1) & 1], scr[(TT + 1) & 1], nbuf);
     fetch_bc(sbr[(TT + 1) & 1], scr[(TT + 1) & 1], kt + 3);
-    float yx[4];
+    float yx[4], gt[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) yx[q] = yxr.get(q);
+    for (int q = 0; q < 4; ++q) {
+      yx[q] = yxr.get(q);
+      gt[q] = (OPT && (flags & SEL_GATED)) ? silu_f32(yzr.get(q)) : 1.0f;
+    }
     fetch_yx(kt + 1);
     wg_barrier();
     // this wavefront's own partials: after the barrier, so that the barrier
@@ -273,11 +302,14 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
         p4[q] = cq[q] * h;
       }
       *reinterpret_cast<float4*>(p_w + 4 * bi) = make_float4(p4[0], p4[1], p4[2], p4[3]);
-      if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, yx_prev);
+      if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, yx_prev, gt_prev);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) yx_prev[q] = yx[q];
+    for (int q = 0; q < 4; ++q) {
+      yx_prev[q] = yx[q];
+      gt_prev[q] = gt[q];
+    }
     buf = nbuf;
     wave_order();  // this wavefront's partials are written before its next reads
   };
@@ -304,7 +336,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   {
     float4 pr[8];
     read_partials(pr);
-    finish_reduce(ntile - 1, pr, yx_prev);
+    finish_reduce(ntile - 1, pr, yx_prev, gt_prev);
   }
   if (h_last && dok) h_last[(b * D + d) * R16_N + n] = h;
 }
@@ -324,23 +356,23 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
 }
 
 template <typename IN>
-int launch_row16(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
-                 const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int64_t L,
-                 hipStream_t s) {
-  const int64_t ndb = (D + R16_ROWS - 1) / R16_ROWS;
-  const int64_t grid = B * ndb;
+int launch_row16(const SelArgs& a, hipStream_t s) {
+  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16;
+  const int64_t ndb = (a.D + R16_ROWS - 1) / R16_ROWS;
+  const int64_t grid = a.B * ndb;
   if (grid >= ((int64_t)1 << 31))
     return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
-  hipLaunchKernelGGL((selective_row16_kernel<IN>), dim3((unsigned)grid), dim3(256), 0, s, x,
-                     delta, A, Bm, Cm, Dskip, y, h_last, D, L, ndb);
+  const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.y_bf16 ? SEL_Y_BF16 : 0u) |
+                         (a.z ? SEL_GATED : 0u);
+  auto kern = opt ? selective_row16_kernel<IN, true> : selective_row16_kernel<IN, false>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, static_cast<const IN*>(a.x),
+                     static_cast<const IN*>(a.delta), a.A, static_cast<const IN*>(a.Bm),
+                     static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
+                     a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L, ndb, flags);
   return check_launch("selective_row16_kernel");
 }
 
-template int launch_row16<float>(const float*, const float*, const float*, const float*,
-                                 const float*, const float*, float*, float*, int64_t, int64_t,
-                                 int64_t, hipStream_t);
-template int launch_row16<uint16_t>(const uint16_t*, const uint16_t*, const float*,
-                                    const uint16_t*, const uint16_t*, const float*, float*,
-                                    float*, int64_t, int64_t, int64_t, hipStream_t);
+template int launch_row16<float>(const SelArgs&, hipStream_t);
+template int launch_row16<uint16_t>(const SelArgs&, hipStream_t);
 
 }  // namespace sw

@@ -17,12 +17,6 @@ int affine_scan_f32(const float* a, const float* bx, const float* h0, float* h, 
                     int64_t L, bool vec);
 int affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
                     int64_t R, int64_t L, bool vec);
-int selective_fwd_f32(const float* x, const float* delta, const float* A, const float* Bm,
-                      const float* Cm, const float* Dskip, float* y, float* h_last, int64_t B,
-                      int64_t D, int64_t N, int64_t L, bool vec);
-int selective_fwd_bf16(const uint16_t* x, const uint16_t* delta, const float* A,
-                       const uint16_t* Bm, const uint16_t* Cm, const float* Dskip, float* y,
-                       float* h_last, int64_t B, int64_t D, int64_t N, int64_t L, bool vec);
 
 namespace {
 thread_local hipStream_t tls_stream = nullptr;
@@ -126,13 +120,9 @@ int affine_common(const T* a, const T* bx, const T* h0, T* h_out, int64_t B, int
   return run(a, bx, h0, h_out, R, L, vec);
 }
 
-template <typename IN>
-int selective_common(const IN* x, const IN* delta, const float* A, const IN* Bm, const IN* Cm,
-                     const float* Dskip, float* y, float* h_last, int64_t B, int64_t D, int64_t N,
-                     int64_t L,
-                     int (*run)(const IN*, const IN*, const float*, const IN*, const IN*,
-                                const float*, float*, float*, int64_t, int64_t, int64_t, int64_t,
-                                bool)) {
+// Validation shared by the fused entry points; see include/scanweaver.h.
+int selective_common(SelArgs a) {
+  const int64_t B = a.B, D = a.D, N = a.N, L = a.L;
   if (B < 0 || D < 0 || L < 0 || N < 0)
     return fail(SW_ERR_INVALID_ARG, "negative size (B=%lld D=%lld N=%lld L=%lld)",
                 (long long)B, (long long)D, (long long)N, (long long)L);
@@ -149,26 +139,62 @@ int selective_common(const IN* x, const IN* delta, const float* A, const IN* Bm,
   int dev, st;
   if ((st = current_device(&dev)) != SW_OK) return st;
   if (L == 0) {
-    if (!h_last) return SW_OK;
-    if ((st = check_ptr(h_last, 4, "h_last", true, dev)) != SW_OK) return st;
-    return zero_words(reinterpret_cast<uint32_t*>(h_last), (size_t)nh, current_stream());
+    if (!a.h_last) return SW_OK;
+    if ((st = check_ptr(a.h_last, 4, "h_last", true, dev)) != SW_OK) return st;
+    if ((st = check_ptr(a.h0, 4, "h0", false, dev)) != SW_OK) return st;
+    if (a.h0) {
+      // the final state of an empty sequence is the initial one
+      Span o[] = {{a.h_last, (size_t)nh * 4, "h_last"}};
+      Span i[] = {{a.h0, (size_t)nh * 4, "h0"}};
+      if ((st = check_spans(o, 1, i, 1)) != SW_OK) return st;
+      hipError_t e = hipMemcpyAsync(a.h_last, a.h0, (size_t)nh * 4, hipMemcpyDeviceToDevice,
+                                    current_stream());
+      if (e != hipSuccess) return fail(SW_ERR_HIP, "h_last copy: %s", hipGetErrorString(e));
+      return SW_OK;
+    }
+    return zero_words(reinterpret_cast<uint32_t*>(a.h_last), (size_t)nh, current_stream());
   }
-  const size_t es = sizeof(IN);
-  if ((st = check_ptr(x, es, "x", true, dev)) != SW_OK) return st;
-  if ((st = check_ptr(delta, es, "delta", true, dev)) != SW_OK) return st;
-  if ((st = check_ptr(A, 4, "A", true, dev)) != SW_OK) return st;
-  if ((st = check_ptr(Bm, es, "Bm", true, dev)) != SW_OK) return st;
-  if ((st = check_ptr(Cm, es, "Cm", true, dev)) != SW_OK) return st;
-  if ((st = check_ptr(Dskip, 4, "Dskip", false, dev)) != SW_OK) return st;
-  if ((st = check_ptr(y, 4, "y", true, dev)) != SW_OK) return st;
-  if ((st = check_ptr(h_last, 4, "h_last", false, dev)) != SW_OK) return st;
-  Span outs[] = {{y, (size_t)nx * 4, "y"}, {h_last, (size_t)nh * 4, "h_last"}};
-  Span ins[] = {{x, (size_t)nx * es, "x"},          {delta, (size_t)nx * es, "delta"},
-                {A, (size_t)(D * N) * 4, "A"},      {Bm, (size_t)nbc * es, "Bm"},
-                {Cm, (size_t)nbc * es, "Cm"},       {Dskip, (size_t)D * 4, "Dskip"}};
-  if ((st = check_spans(outs, 2, ins, 6)) != SW_OK) return st;
-  const bool vec = L % 4 == 0 && all_aligned16({x, delta, y});
-  return run(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, vec);
+  const size_t es = a.bf16_in ? 2 : 4, ys = a.y_bf16 ? 2 : 4;
+  if ((st = check_ptr(a.x, es, "x", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.delta, es, "delta", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.A, 4, "A", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.Bm, es, "Bm", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.Cm, es, "Cm", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.Dskip, 4, "Dskip", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.z, es, "z", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.delta_bias, 4, "delta_bias", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.h0, 4, "h0", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.y, ys, "y", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.h_last, 4, "h_last", false, dev)) != SW_OK) return st;
+  Span outs[] = {{a.y, (size_t)nx * ys, "y"}, {a.h_last, (size_t)nh * 4, "h_last"}};
+  Span ins[] = {{a.x, (size_t)nx * es, "x"},          {a.delta, (size_t)nx * es, "delta"},
+                {a.A, (size_t)(D * N) * 4, "A"},      {a.Bm, (size_t)nbc * es, "Bm"},
+                {a.Cm, (size_t)nbc * es, "Cm"},       {a.Dskip, (size_t)D * 4, "Dskip"},
+                {a.z, (size_t)nx * es, "z"},          {a.delta_bias, (size_t)D * 4, "delta_bias"},
+                {a.h0, (size_t)nh * 4, "h0"}};
+  if ((st = check_spans(outs, 2, ins, 9)) != SW_OK) return st;
+  a.vec = L % 4 == 0 && all_aligned16({a.x, a.delta, a.y, a.z});
+  return selective_fwd(a);
+}
+
+SelArgs sel_args(const void* x, const void* delta, const float* A, const void* Bm, const void* Cm,
+                 const float* Dskip, void* y, float* h_last, int64_t B, int64_t D, int64_t N,
+                 int64_t L, bool bf16_in) {
+  SelArgs a{};
+  a.x = x;
+  a.delta = delta;
+  a.A = A;
+  a.Bm = Bm;
+  a.Cm = Cm;
+  a.Dskip = Dskip;
+  a.y = y;
+  a.h_last = h_last;
+  a.B = B;
+  a.D = D;
+  a.N = N;
+  a.L = L;
+  a.bf16_in = bf16_in;
+  return a;
 }
 
 }  // namespace
@@ -296,16 +322,36 @@ SW_API int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t
 SW_API int sw_selective_scan_fwd(const float* x, const float* delta, const float* A,
                                  const float* Bm, const float* Cm, const float* Dskip, float* y,
                                  float* h_last, int64_t B, int64_t D, int64_t N, int64_t L) {
-  return sw::selective_common<float>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L,
-                                     sw::selective_fwd_f32);
+  return sw::selective_common(
+      sw::sel_args(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, false));
 }
 
 SW_API int sw_selective_scan_fwd_bf16(const uint16_t* x, const uint16_t* delta, const float* A,
                                       const uint16_t* Bm, const uint16_t* Cm, const float* Dskip,
                                       float* y, float* h_last, int64_t B, int64_t D, int64_t N,
                                       int64_t L) {
-  return sw::selective_common<uint16_t>(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L,
-                                        sw::selective_fwd_bf16);
+  return sw::selective_common(
+      sw::sel_args(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L, true));
+}
+
+SW_API int sw_selective_scan_fwd_ex(const void* x, const void* delta, const float* A,
+                                    const void* Bm, const void* Cm, const float* Dskip,
+                                    const void* z, const float* delta_bias, const float* h0,
+                                    void* y, float* h_last, int64_t B, int64_t D, int64_t N,
+                                    int64_t L, int in_dtype, int out_dtype, int flags) {
+  if ((in_dtype != SW_DTYPE_F32 && in_dtype != SW_DTYPE_BF16) ||
+      (out_dtype != SW_DTYPE_F32 && out_dtype != SW_DTYPE_BF16))
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown dtype (in=%d out=%d)", in_dtype, out_dtype);
+  if (flags & ~SW_DELTA_SOFTPLUS)
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown flags 0x%x", (unsigned)flags);
+  sw::SelArgs a = sw::sel_args(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L,
+                               in_dtype == SW_DTYPE_BF16);
+  a.z = z;
+  a.delta_bias = delta_bias;
+  a.h0 = h0;
+  a.y_bf16 = out_dtype == SW_DTYPE_BF16;
+  a.softplus = (flags & SW_DELTA_SOFTPLUS) != 0;
+  return sw::selective_common(a);
 }
 
 SW_API int sw_set_stream(void* hip_stream) {

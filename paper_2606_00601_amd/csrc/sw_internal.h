@@ -53,12 +53,53 @@ struct ScratchSession {
   hipStream_t stream_ = nullptr;
 };
 
+// Arguments of one fused selective scan call, already validated.  x, delta,
+// Bm, Cm and z are fp32 or bf16 (raw bits) as `bf16_in` says; y is fp32 or
+// bf16 bits as `y_bf16` says.  z, delta_bias, h0, Dskip and h_last may be NULL.
+struct SelArgs {
+  const void *x, *delta, *Bm, *Cm, *z;
+  const float *A, *Dskip, *delta_bias, *h0;
+  void* y;
+  float* h_last;
+  int64_t B, D, N, L;
+  bool bf16_in, y_bf16, softplus, vec;
+};
+int selective_fwd(const SelArgs& a);
+
+// Flags of the fused kernels (runtime, wave-uniform).
+enum : uint32_t { SEL_SOFTPLUS = 1u, SEL_Y_BF16 = 2u, SEL_GATED = 4u };
+
 // ---------------------------------------------------------------- device side
 
 // bf16 bits -> fp32, exact.
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ float bf16_one(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// fp32 -> bf16 bits, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint32_t bf16_rne(float v) {
+  const uint32_t u = __float_as_uint(v);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// softplus(v) = log(1 + e^v) in fp32 from the hardware exp2/log2/rcp, a few
+// ulps: e^-v is negligible past v = 16; log1p(u) = log(w) * u / (w - 1) with
+// w = 1 + u keeps the small-u end accurate (w == 1 means log1p(u) = u).
+__device__ __forceinline__ float softplus_f32(float v) {
+  constexpr float LOG2E_ = 1.4426950408889634f, LN2_ = 0.6931471805599453f;
+  if (v > 16.0f) return v + __builtin_amdgcn_exp2f(-v * LOG2E_);
+  const float u = __builtin_amdgcn_exp2f(v * LOG2E_);
+  const float w = 1.0f + u;
+  if (w == 1.0f) return u;
+  return __builtin_amdgcn_logf(w) * LN2_ * (u * __builtin_amdgcn_rcpf(w - 1.0f));
+}
+
+// silu(z) = z / (1 + e^-z) in fp32 (exp2 and rcp; 0 for z -> -inf).
+__device__ __forceinline__ float silu_f32(float z) {
+  constexpr float LOG2E_ = 1.4426950408889634f;
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-z * LOG2E_));
+}
 
 // Affine-pair arithmetic.  combine(later, earlier) is Eq. (7):
 //   (A2,U2) (+) (A1,U1) = (A2*A1, A2*U1 + U2).

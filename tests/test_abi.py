@@ -65,6 +65,16 @@ def test_validation_without_gpu(lib):
     # overflowing sizes are refused
     big = 1 << 40
     assert lib.sw_affine_scan(None, None, None, None, big, big, 4) == 2
+    # the extended fused entry point: unknown dtypes and flags are refused
+    # before anything else; otherwise it validates like the plain one
+    ex = lib.sw_selective_scan_fwd_ex
+    assert ex(*([None] * 11), 1, 1, 16, 4, 2, 0, 0) == 1
+    assert "dtype" in lib.sw_last_error().decode()
+    assert ex(*([None] * 11), 1, 1, 16, 4, 0, 5, 0) == 1
+    assert ex(*([None] * 11), 1, 1, 16, 4, 0, 0, 2) == 1
+    assert "flags" in lib.sw_last_error().decode()
+    assert ex(*([None] * 11), 1, 1, 65, 4, 1, 1, 1) == 2
+    assert ex(*([None] * 11), 2, 0, 16, 9, 1, 1, 1) == 0
 
 
 def test_status_strings(lib):

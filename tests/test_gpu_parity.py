@@ -191,7 +191,8 @@ def _selective_check(sw, inp, dtype, rows=None, with_dskip=True):
 
 @pytest.mark.parametrize("B,D,N,L", [(1, 1, 1, 1), (2, 70, 16, 200), (1, 33, 3, 37),
                                      (3, 31, 8, 64), (1, 40, 17, 33), (2, 9, 32, 129),
-                                     (1, 5, 64, 100), (2, 64, 16, 31), (1, 3, 16, 5000)])
+                                     (1, 5, 64, 100), (2, 64, 16, 31), (1, 3, 16, 5000),
+                                     (2, 9, 5, 96), (1, 7, 12, 64), (1, 6, 40, 128)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_selective_small_full_compare(sw, B, D, N, L, dtype):
     _say("case selective", dtype, B, D, N, L)
@@ -309,3 +310,138 @@ def test_abi_rejects_bad_pointers(sw):
     rc = lib.sw_selective_scan_fwd(x.data_ptr(), x.data_ptr(), A.data_ptr(), x.data_ptr(),
                                    x.data_ptr(), None, h.data_ptr(), None, 1, 2, 65, 8)
     assert rc == 2
+
+
+# ------------------------------------------------------------ Mamba-block options
+
+def _ex_inputs(B, D, N, L, seed, dtype, opts):
+    inp = wl.selective_inputs(B, D, N, L, seed, dtype)
+    rng = np.random.Generator(np.random.PCG64(seed + 77))
+    ex = {}
+    if "z" in opts:
+        z = (rng.standard_normal(size=(B, D, L)) * 2).astype(np.float32)
+        if dtype == "bf16":
+            ex["z_bits"] = wl.bf16_round(z)
+            z = wl.bf16_widen(ex["z_bits"])
+        ex["z"] = z
+    if "bias" in opts:
+        # raw delta before softplus: the generator's softplus output is reused
+        # as a raw value, shifted by a per-channel bias around -1
+        ex["delta_bias"] = rng.uniform(-2.0, 0.0, size=D).astype(np.float32)
+    if "h0" in opts:
+        ex["h0"] = rng.standard_normal(size=(B, D, N)).astype(np.float32)
+    return inp, ex
+
+
+def _run_ex(sw, inp, ex, dtype, softplus, y_bf16):
+    if dtype == "bf16":
+        x, dl = bf16_dev(inp["x_bf16"]), bf16_dev(inp["delta_bf16"])
+        Bm, Cm = bf16_dev(inp["Bm_bf16"]), bf16_dev(inp["Cm_bf16"])
+        z = bf16_dev(ex["z_bits"]) if "z" in ex else None
+    else:
+        x, dl, Bm, Cm = dev(inp["x"]), dev(inp["delta"]), dev(inp["Bm"]), dev(inp["Cm"])
+        z = dev(ex["z"]) if "z" in ex else None
+    y, hl = sw.selective_scan_fwd(
+        x, dl, dev(inp["A"]), Bm, Cm, dev(inp["Dskip"]), z=z,
+        delta_bias=dev(ex["delta_bias"]) if "delta_bias" in ex else None,
+        h0=dev(ex["h0"]) if "h0" in ex else None, delta_softplus=softplus,
+        y_dtype=torch.bfloat16 if y_bf16 else torch.float32)
+    torch.cuda.synchronize()
+    return y, hl
+
+
+def _ex_oracle(inp, ex, softplus, rows=None):
+    return oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                                 inp["Dskip"], rows=rows, bounds=True, z=ex.get("z"),
+                                 delta_bias=ex.get("delta_bias"), h0=ex.get("h0"),
+                                 delta_softplus=softplus)
+
+
+def _y_gate(yt, o, y_bf16, what, rows=None):
+    yg = yt.float().cpu().numpy()
+    if rows is not None:
+        yg = yg.reshape(-1, yg.shape[-1])[rows]
+    if y_bf16:
+        # bf16 y: the fp32 result rounded once more, half an ulp of 8 bits
+        err = np.abs(yg - o["y"])
+        ok = err <= 2.0 ** -8 * np.abs(o["y"]) + 1.01e-4 * o["y_mag"] \
+            + 4 * 2.0 ** -24 * o["y_sens"]
+        assert ok.all(), f"{what}: bf16 y off at {np.argwhere(~ok)[:3]}"
+    else:
+        assert_gate(fp_gate(yg, o["y"], o["y_mag"], o["y_sens"]), what)
+
+
+# (B, D, N, L): N = 16 with L % 8 == 0 takes the 16-lane kernel; the others the 8-lane one
+_EX_SHAPES = [(2, 37, 16, 520), (1, 20, 16, 133), (2, 9, 5, 96)]
+_EX_OPTS = [("h0",), ("bias", "softplus"), ("softplus",), ("z",), ("ybf16",),
+            ("h0", "bias", "softplus", "z", "ybf16")]
+
+
+@pytest.mark.parametrize("shape", _EX_SHAPES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("opts", _EX_OPTS)
+def test_selective_mamba_options(sw, shape, dtype, opts):
+    B, D, N, L = shape
+    _say("case selective options", dtype, shape, opts)
+    inp, ex = _ex_inputs(B, D, N, L, 7000 + B + D + N + L, dtype, opts)
+    softplus, y_bf16 = "softplus" in opts, "ybf16" in opts
+    y, hl = _run_ex(sw, inp, ex, dtype, softplus, y_bf16)
+    assert y.dtype == (torch.bfloat16 if y_bf16 else torch.float32)
+    o = _ex_oracle(inp, ex, softplus)
+    _y_gate(y, o, y_bf16, f"y {dtype} {shape} {opts}")
+    assert_gate(fp_gate(hl.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]),
+                f"h_last {dtype} {shape} {opts}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["16", "8"])
+def test_selective_continued_across_calls_bitexact(sw, monkeypatch, dtype, layout):
+    """A sequence scanned in three calls, each starting from the previous
+    call's h_last, runs the same per-step arithmetic as one call: y and the
+    final state are bit-identical."""
+    monkeypatch.setenv("SW_SS_LAYOUT", layout)
+    _say("case selective continued", dtype, layout)
+    B, D, N, L = 2, 24, 16, 4096
+    inp = wl.selective_inputs(B, D, N, L, 7777, dtype)
+    k = "_bf16" if dtype == "bf16" else ""
+    cv = (lambda a: bf16_dev(a)) if dtype == "bf16" else (lambda a: dev(a))
+    x, dl, Bm, Cm = (inp[n + k] for n in ("x", "delta", "Bm", "Cm"))
+    A, Dk = dev(inp["A"]), dev(inp["Dskip"])
+    y_one, h_one = sw.selective_scan_fwd(cv(x), cv(dl), A, cv(Bm), cv(Cm), Dk)
+    parts, h = [], None
+    for t0, t1 in ((0, 1024), (1024, 1536), (1536, L)):
+        yp, h = sw.selective_scan_fwd(cv(np.ascontiguousarray(x[:, :, t0:t1])),
+                                      cv(np.ascontiguousarray(dl[:, :, t0:t1])), A,
+                                      cv(np.ascontiguousarray(Bm[:, t0:t1])),
+                                      cv(np.ascontiguousarray(Cm[:, t0:t1])), Dk, h0=h)
+        parts.append(yp)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat(parts, dim=2), y_one)
+    assert torch.equal(h, h_one)
+
+
+def test_selective_L0_returns_h0(sw):
+    x = torch.empty((2, 3, 0), device="cuda")
+    A = torch.randn((3, 16), device="cuda")
+    Bm = torch.empty((2, 0, 16), device="cuda")
+    h0 = torch.randn((2, 3, 16), device="cuda")
+    y, hl = sw.selective_scan_fwd(x, x, A, Bm, Bm, None, h0=h0)
+    torch.cuda.synchronize()
+    assert y.shape == (2, 3, 0) and torch.equal(hl, h0)
+
+
+def test_selective_mamba_options_full_size(sw):
+    """Every option at the Mamba-130M-like shape (bf16, B=8, D=1536, N=16,
+    L=2048), in the bench's launch configuration, on sampled rows."""
+    w = wl.workload("selective_bf16_b8_d1536_n16_l2048")
+    _say("case options full size", w.name)
+    opts = ("h0", "bias", "softplus", "z")
+    inp, ex = _ex_inputs(w.B, w.D, w.N, w.L, 8080, "bf16", opts)
+    for y_bf16 in (False, True):
+        y, hl = _run_ex(sw, inp, ex, "bf16", True, y_bf16)
+        rows = _sample_rows(w.B * w.D, 256, 81)
+        o = _ex_oracle(inp, ex, True, rows=rows)
+        _y_gate(y, o, y_bf16, f"full-size options y_bf16={y_bf16}", rows=rows)
+        hg = hl.reshape(w.B * w.D, w.N).index_select(
+            0, torch.as_tensor(rows, device="cuda")).cpu().numpy()
+        assert_gate(fp_gate(hg, o["h_last"], o["h_mag"], o["h_sens"]), "full-size h_last")
