@@ -81,6 +81,37 @@ int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t* h0, i
                        int64_t B, int64_t D, int64_t L);
 
 /*
+ * Recurrence with input and output projections, elementwise (Eq. (3)-(4)):
+ *   h[b,d,t] = a[b,d,t] * h[b,d,t-1] + b[b,d,t] * x[b,d,t]      (h[b,d,-1] = h0)
+ *   y[b,d,t] = c[b,d,t] * h[b,d,t]
+ * The weighted prefix of Eq. (10) is the case x = 1, c = 1 (alpha -> a,
+ * beta -> b).
+ *   a, b, y      : (B, D, L) fp32, L fastest, required.
+ *   x, c         : (B, D, L) fp32, or NULL for all ones.
+ *   h0           : (B, D) fp32 initial state, or NULL for zero.
+ *   h_last       : (B, D) fp32, receives h[b,d,L-1] (h0, or zero, when
+ *                  L == 0), or NULL.
+ * b*x and c*h are each rounded to fp32 once; the scan itself is that of
+ * sw_affine_scan on the pairs (a, b*x), so with x and c NULL, y equals the
+ * h_out of sw_affine_scan bit for bit.  Same conventions as sw_affine_scan
+ * otherwise: caller-owned device pointers, outputs may not overlap inputs,
+ * SW_ERR_INVALID_ARG for a NULL required pointer, misalignment, foreign or
+ * host memory, negative sizes or overlap; SW_ERR_UNSUPPORTED when B*D*L
+ * overflows.
+ */
+int sw_affine_scan_proj(const float* a, const float* b, const float* x, const float* c,
+                        const float* h0, float* y, float* h_last, int64_t B, int64_t D,
+                        int64_t L);
+
+/*
+ * The same in the int32 wraparound ring: b*x, the recurrence and c*h modulo
+ * 2^32 on two's-complement bit patterns; bit-identical to the sequential loop.
+ */
+int sw_affine_scan_proj_i32(const int32_t* a, const int32_t* b, const int32_t* x,
+                            const int32_t* c, const int32_t* h0, int32_t* y, int32_t* h_last,
+                            int64_t B, int64_t D, int64_t L);
+
+/*
  * Fused selective scan, forward, fp32 inputs (the Mamba-style instance of
  * Eq. (3) that motivates the method, Sec. 1 and Sec. 3.1), zero initial state:
  *

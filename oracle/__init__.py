@@ -75,6 +75,10 @@ def _load():
         lib.swo_affine_scan_f64.restype = ctypes.c_int
         lib.swo_affine_scan_u32.argtypes = [_vp] * 4 + [_i64, _i64, ctypes.c_int]
         lib.swo_affine_scan_u32.restype = ctypes.c_int
+        lib.swo_affine_proj_f64.argtypes = [_vp] * 9 + [_i64, _i64, ctypes.c_int]
+        lib.swo_affine_proj_f64.restype = ctypes.c_int
+        lib.swo_affine_proj_u32.argtypes = [_vp] * 7 + [_i64, _i64, ctypes.c_int]
+        lib.swo_affine_proj_u32.restype = ctypes.c_int
         lib.swo_affine_prefix_f64.argtypes = [_vp] * 6 + [_i64, _i64]
         lib.swo_affine_prefix_f64.restype = ctypes.c_int
         lib.swo_affine_prefix_u32.argtypes = [_vp] * 6 + [_i64, _i64]
@@ -169,6 +173,53 @@ def affine_scan_i32(a, bx, h0=None, threads: int = 0):
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     return h.view(np.int32)
+
+
+def _proj_args(a, b, x, c, h0, dtype):
+    a, b = _as(a, dtype), _as(b, dtype)
+    x, c = _as(x, dtype), _as(c, dtype)
+    for v, name in ((b, "b"), (x, "x"), (c, "c")):
+        if v is not None and v.shape != a.shape:
+            raise ValueError(f"{name} must have the shape of a")
+    rows, L = _rows_L(a)
+    h0 = _as(h0, dtype)
+    if h0 is not None and h0.size != rows:
+        raise ValueError("h0 must hold one value per row")
+    return a, b, x, c, h0, rows, L
+
+
+def affine_proj(a, b, x=None, c=None, h0=None, bounds: bool = False, threads: int = 0):
+    """Eq. (3)-(4) with input and output projections, fp64: per row
+    h_t = a_t h_{t-1} + b_t x_t and y_t = c_t h_t (x, c None: ones).
+
+    fp32 arrays of shape (..., L); ``h0`` has shape (...) or is None.  Returns
+    ``(y, h_last)`` and with ``bounds=True`` also ``(y_mag, y_sens)``.
+    """
+    a, b, x, c, h0, rows, L = _proj_args(a, b, x, c, h0, np.float32)
+    y = np.empty(a.shape, np.float64)
+    h_last = np.empty(a.shape[:-1], np.float64)
+    ym = np.empty(a.shape, np.float64) if bounds else None
+    ys = np.empty(a.shape, np.float64) if bounds else None
+    rc = _load().swo_affine_proj_f64(_p(a), _p(b), _p(x), _p(c), _p(h0), _p(y), _p(h_last),
+                                     _p(ym), _p(ys), rows, L, int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return (y, h_last, ym, ys) if bounds else (y, h_last)
+
+
+def affine_proj_i32(a, b, x=None, c=None, h0=None, threads: int = 0):
+    """Eq. (3)-(4) with projections in the int32 wraparound ring; returns
+    ``(y, h_last)`` as int32."""
+    cv = (lambda v: None if v is None else _as(v, np.int32).view(np.uint32))
+    a, b, x, c, h0 = (cv(v) for v in (a, b, x, c, h0))
+    a, b, x, c, h0, rows, L = _proj_args(a, b, x, c, h0, np.uint32)
+    y = np.empty(a.shape, np.uint32)
+    h_last = np.empty(a.shape[:-1], np.uint32)
+    rc = _load().swo_affine_proj_u32(_p(a), _p(b), _p(x), _p(c), _p(h0), _p(y), _p(h_last),
+                                     rows, L, int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return y.view(np.int32), h_last.view(np.int32)
 
 
 def affine_prefix(a, bx, h0=None):

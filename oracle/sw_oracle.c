@@ -171,6 +171,80 @@ int swo_affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h
 }
 
 /* ------------------------------------------------------------------------ */
+/* Eq. (3)-(4) with the input and output projections written out: per row,
+ * h_t = a_t h_{t-1} + b_t x_t and y_t = c_t h_t, with x or c absent meaning
+ * all ones (the weighted prefix of Eq. (10) is x = 1, c = 1).  fp64: the
+ * products of two fp32 values are exact.  y_mag = |c_t| M_t and
+ * y_sens = |c_t| M1_t, with M and M1 as for the bare recurrence. */
+
+typedef struct {
+  const float *a, *b, *x, *c, *h0;
+  double *y, *h_last, *y_mag, *y_sens;
+  int64_t L;
+} proj_f64_ctx;
+
+static void proj_f64_rows(int64_t r0, int64_t r1, const void* vctx) {
+  const proj_f64_ctx* c = (const proj_f64_ctx*)vctx;
+  const int64_t L = c->L;
+  for (int64_t r = r0; r < r1; r++) {
+    double h = c->h0 ? (double)c->h0[r] : 0.0;
+    double m = fabs(h), s = 0.0;
+    for (int64_t t = 0; t < L; t++) {
+      const int64_t i = r * L + t;
+      const double at = (double)c->a[i];
+      const double ut = (double)c->b[i] * (c->x ? (double)c->x[i] : 1.0);
+      const double ct = c->c ? (double)c->c[i] : 1.0;
+      h = at * h + ut;
+      s = fabs(at) * (s + m);
+      m = fabs(at) * m + fabs(ut);
+      c->y[i] = ct * h;
+      if (c->y_mag) c->y_mag[i] = fabs(ct) * m;
+      if (c->y_sens) c->y_sens[i] = fabs(ct) * s;
+    }
+    if (c->h_last) c->h_last[r] = h;
+  }
+}
+
+int swo_affine_proj_f64(const float* a, const float* b, const float* x, const float* cc,
+                        const float* h0, double* y, double* h_last, double* y_mag, double* y_sens,
+                        int64_t rows, int64_t L, int nthreads) {
+  if (!a || !b || !y || rows < 0 || L < 0) return 1;
+  proj_f64_ctx c = {a, b, x, cc, h0, y, h_last, y_mag, y_sens, L};
+  run_rows(proj_f64_rows, &c, rows, nthreads);
+  return 0;
+}
+
+typedef struct {
+  const uint32_t *a, *b, *x, *c, *h0;
+  uint32_t *y, *h_last;
+  int64_t L;
+} proj_u32_ctx;
+
+static void proj_u32_rows(int64_t r0, int64_t r1, const void* vctx) {
+  const proj_u32_ctx* c = (const proj_u32_ctx*)vctx;
+  const int64_t L = c->L;
+  for (int64_t r = r0; r < r1; r++) {
+    uint32_t h = c->h0 ? c->h0[r] : 0u;
+    for (int64_t t = 0; t < L; t++) {
+      const int64_t i = r * L + t;
+      const uint32_t ut = c->b[i] * (c->x ? c->x[i] : 1u);
+      h = c->a[i] * h + ut;
+      c->y[i] = (c->c ? c->c[i] : 1u) * h;
+    }
+    if (c->h_last) c->h_last[r] = h;
+  }
+}
+
+int swo_affine_proj_u32(const uint32_t* a, const uint32_t* b, const uint32_t* x,
+                        const uint32_t* cc, const uint32_t* h0, uint32_t* y, uint32_t* h_last,
+                        int64_t rows, int64_t L, int nthreads) {
+  if (!a || !b || !y || rows < 0 || L < 0) return 1;
+  proj_u32_ctx c = {a, b, x, cc, h0, y, h_last, L};
+  run_rows(proj_u32_rows, &c, rows, nthreads);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Sec. 3.2: inclusive prefix compositions P_t = p_t (+) P_{t-1}, P_0 = the
  * identity pair (1, 0), p_t = (a_t, bx_t) of Eq. (6).  The state is rebuilt
  * from the prefix pair as h_t = A_{1:t} h_0 + U_{1:t}.  This is a second,

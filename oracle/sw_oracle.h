@@ -26,6 +26,16 @@ int swo_affine_scan_f64(const float* a, const float* bx, const float* h0, double
 int swo_affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
                         int64_t rows, int64_t L, int nthreads);
 
+/* Eq. (3)-(4) with input and output projections: h_t = a_t h_{t-1} + b_t x_t,
+ * y_t = c_t h_t per row (x, c NULL: ones); h_last[r] = h_{L-1} (h0 when L = 0).
+ * Any of h0 / h_last / y_mag / y_sens may be NULL. */
+int swo_affine_proj_f64(const float* a, const float* b, const float* x, const float* c,
+                        const float* h0, double* y, double* h_last, double* y_mag, double* y_sens,
+                        int64_t rows, int64_t L, int nthreads);
+int swo_affine_proj_u32(const uint32_t* a, const uint32_t* b, const uint32_t* x,
+                        const uint32_t* c, const uint32_t* h0, uint32_t* y, uint32_t* h_last,
+                        int64_t rows, int64_t L, int nthreads);
+
 /* Sec. 3.2 prefix compositions and the state rebuilt from them.  Any of
  * Apre / Upre / h may be NULL. */
 int swo_affine_prefix_f64(const float* a, const float* bx, const float* h0, double* Apre,

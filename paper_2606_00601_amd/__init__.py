@@ -19,7 +19,8 @@ import torch
 
 from ._lib import ScanWeaverError, check, last_error, lib, status_string  # noqa: F401
 
-__all__ = ["affine_scan", "affine_scan_i32", "selective_scan_fwd", "ScanWeaverError",
+__all__ = ["affine_scan", "affine_scan_i32", "affine_scan_proj", "affine_scan_proj_i32",
+           "selective_scan_fwd", "ScanWeaverError",
            "version"]
 
 
@@ -74,6 +75,42 @@ def affine_scan(a, bx, h0=None, out=None):
 def affine_scan_i32(a, bx, h0=None, out=None):
     """The recurrence in Z/2^32 on int32 tensors (bit-exact for any schedule)."""
     return _affine(lib().sw_affine_scan_i32, "sw_affine_scan_i32", torch.int32, a, bx, h0, out)
+
+
+def _affine_proj(fn, where, dtype, a, b, x, c, h0, y, want_h_last):
+    _need(a, "a", dtype)
+    if a.dim() != 3:
+        raise ValueError("a must have shape (B, D, L)")
+    B, D, L = a.shape
+    _need(b, "b", dtype, a.shape)
+    for t, name in ((x, "x"), (c, "c")):
+        if t is not None:
+            _need(t, name, dtype, a.shape)
+    if h0 is not None:
+        _need(h0, "h0", dtype, (B, D))
+    if y is None:
+        y = torch.empty_like(a)
+    else:
+        _need(y, "y", dtype, a.shape)
+    h_last = torch.empty((B, D), dtype=dtype, device=a.device) if want_h_last else None
+    with torch.cuda.device(a.device):
+        _bind_stream(a.device)
+        check(fn(_ptr(a), _ptr(b), _ptr(x), _ptr(c), _ptr(h0), _ptr(y), _ptr(h_last), B, D, L),
+              where)
+    return y, h_last
+
+
+def affine_scan_proj(a, b, x=None, c=None, h0=None, *, y=None, want_h_last=True):
+    """Eq. (3)-(4) elementwise: h_t = a_t h_{t-1} + b_t x_t, y_t = c_t h_t (fp32,
+    shape (B, D, L); x, c None mean ones).  Returns ``(y, h_last)``."""
+    return _affine_proj(lib().sw_affine_scan_proj, "sw_affine_scan_proj", torch.float32, a, b,
+                        x, c, h0, y, want_h_last)
+
+
+def affine_scan_proj_i32(a, b, x=None, c=None, h0=None, *, y=None, want_h_last=True):
+    """The projection form in Z/2^32 on int32 tensors (bit-exact)."""
+    return _affine_proj(lib().sw_affine_scan_proj_i32, "sw_affine_scan_proj_i32", torch.int32,
+                        a, b, x, c, h0, y, want_h_last)
 
 
 def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,

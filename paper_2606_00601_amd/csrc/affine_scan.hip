@@ -17,6 +17,8 @@
 //      inclusive state, and then publishes its own inclusive state;
 //   5. every lane rebuilds its states as h = A_pre * h_in + U_pre (Sec. 3.2)
 //      and stores them with 16-byte vector stores.
+// The elementwise form of Eq. (3)-(4) (IO variant) forms bx = b * x at the
+// load, stores y = c * h instead of h and can write the final state h_last.
 // Chunks are handed out through an atomic ticket in chunk-major order (all
 // rows' chunk 0 first), so a chunk only ever waits on chunks that already
 // hold a ticket, which guarantees forward progress.  When the rows alone fill
@@ -30,10 +32,29 @@ namespace {
 constexpr int AS_THREADS = 256;
 constexpr int AS_WAVES = AS_THREADS / 64;
 
-template <typename T, int K, bool VEC>
+// Operands of one call.  The plain scan has b = bx, y = h and no x, c or
+// h_last; the IO variant reads x (NULL: 1) and c (NULL: 1) and writes h_last
+// (NULL: not written).
+template <typename T>
+struct AffIO {
+  const T *a, *b, *x, *c, *h0;
+  T *y, *h_last;
+};
+
+// y element of state hv at step t (IO: times c_t; the final state goes to h_last)
+template <bool IO, typename T>
+__device__ __forceinline__ T out_elem(const AffIO<T>& io, const T* __restrict__ cr, T hv,
+                                      int64_t t, int64_t L, int64_t row) {
+  if constexpr (IO) {
+    if (io.h_last && t == L - 1) io.h_last[row] = hv;
+    if (cr) return Ring<T>::mul(cr[t], hv);
+  }
+  return hv;
+}
+
+template <typename T, int K, bool VEC, bool IO>
 __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
-    const T* __restrict__ a, const T* __restrict__ bx, const T* __restrict__ h0,
-    T* __restrict__ h, int64_t R, int64_t L, int64_t nchunks, int64_t total,
+    const AffIO<T> io, int64_t R, int64_t L, int64_t nchunks, int64_t total,
     unsigned long long* __restrict__ carry, uint32_t* __restrict__ ticket, uint32_t tbase,
     uint32_t epoch) {
   static_assert(K % 4 == 0, "K must be a multiple of 4");
@@ -60,9 +81,11 @@ __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
     const int64_t c = id / R;
     const int64_t row = id - c * R;
     const int64_t t0 = c * CH + (int64_t)tid * K;
-    const T* __restrict__ ar = a + row * L;
-    const T* __restrict__ br = bx + row * L;
-    T* __restrict__ hr = h + row * L;
+    const T* __restrict__ ar = io.a + row * L;
+    const T* __restrict__ br = io.b + row * L;
+    const T* __restrict__ xr = (IO && io.x) ? io.x + row * L : nullptr;
+    const T* __restrict__ cr = (IO && io.c) ? io.c + row * L : nullptr;
+    T* __restrict__ hr = io.y + row * L;
 
     // 1. load and local inclusive prefixes
     T pa[K], pu[K];
@@ -79,13 +102,20 @@ __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
         pu[4 * q + 1] = Rg::from_bits(vb.y);
         pu[4 * q + 2] = Rg::from_bits(vb.z);
         pu[4 * q + 3] = Rg::from_bits(vb.w);
+        if (xr) {
+          const uint4 vx = *reinterpret_cast<const uint4*>(xr + t0 + 4 * q);
+          pu[4 * q + 0] = Rg::mul(pu[4 * q + 0], Rg::from_bits(vx.x));
+          pu[4 * q + 1] = Rg::mul(pu[4 * q + 1], Rg::from_bits(vx.y));
+          pu[4 * q + 2] = Rg::mul(pu[4 * q + 2], Rg::from_bits(vx.z));
+          pu[4 * q + 3] = Rg::mul(pu[4 * q + 3], Rg::from_bits(vx.w));
+        }
       }
     } else {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         const bool ok = t0 + k < L;
         pa[k] = ok ? ar[t0 + k] : Rg::one();
-        pu[k] = ok ? br[t0 + k] : Rg::zero();
+        pu[k] = ok ? (xr ? Rg::mul(br[t0 + k], xr[t0 + k]) : br[t0 + k]) : Rg::zero();
       }
     }
 #pragma unroll
@@ -120,7 +150,7 @@ __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
     // 4. carry into the chunk
     T hin;
     if (c == 0) {
-      hin = h0 ? h0[row] : Rg::zero();
+      hin = io.h0 ? io.h0[row] : Rg::zero();
       if (nchunks > 1 && tid == 0)
         carry_put(carry + (row * nchunks) * 3, st_inc, Rg::bits(Rg::mad(cA, hin, cU)));
     } else {
@@ -156,7 +186,7 @@ __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
 
     // 5. rebuild the states and store
     const T hs = Rg::mad(wA, hin, wU);
-    if (VEC && t0 + K <= L) {
+    if (VEC && !IO && t0 + K <= L) {
 #pragma unroll
       for (int q = 0; q < K / 4; ++q) {
         uint4 o;
@@ -166,10 +196,27 @@ __global__ __launch_bounds__(AS_THREADS) void affine_scan_kernel(
         o.w = Rg::bits(Rg::mad(pa[4 * q + 3], hs, pu[4 * q + 3]));
         *reinterpret_cast<uint4*>(hr + t0 + 4 * q) = o;
       }
+    } else if (VEC && t0 + K <= L) {
+#pragma unroll
+      for (int q = 0; q < K / 4; ++q) {
+        uint4 vc = make_uint4(0u, 0u, 0u, 0u);
+        if (cr) vc = *reinterpret_cast<const uint4*>(cr + t0 + 4 * q);
+        const uint32_t cb[4] = {vc.x, vc.y, vc.z, vc.w};
+        T v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int k = 4 * q + e;
+          v[e] = Rg::mad(pa[k], hs, pu[k]);
+          if (io.h_last && t0 + k == L - 1) io.h_last[row] = v[e];
+          if (cr) v[e] = Rg::mul(Rg::from_bits(cb[e]), v[e]);
+        }
+        *reinterpret_cast<uint4*>(hr + t0 + 4 * q) =
+            make_uint4(Rg::bits(v[0]), Rg::bits(v[1]), Rg::bits(v[2]), Rg::bits(v[3]));
+      }
     } else {
 #pragma unroll
       for (int k = 0; k < K; ++k)
-        if (t0 + k < L) hr[t0 + k] = Rg::mad(pa[k], hs, pu[k]);
+        if (t0 + k < L) hr[t0 + k] = out_elem<IO>(io, cr, Rg::mad(pa[k], hs, pu[k]), t0 + k, L, row);
     }
     if (nchunks <= 1) {
       id += gridDim.x;
@@ -190,13 +237,22 @@ struct ChunkRegs {
   T a[K], u[K];
 };
 
+// In the IO variant the c of the chunk is prefetched with it.
+template <typename T, int K>
+struct ChunkC {
+  T c[K];
+};
+
 // Branch-free loads (clamped addresses, identity pairs past the end): the
 // prefetch then never forces a wait, and the register buffer is never written
 // from two control-flow paths.  Requires L >= 4; with VEC, L is a multiple of
 // 4, so every 4-element piece is wholly inside or wholly outside the row.
-template <typename T, int K, bool VEC>
-__device__ __forceinline__ void load_chunk(ChunkRegs<T, K, VEC>& r, const T* __restrict__ ar,
-                                           const T* __restrict__ br, int64_t t0, int64_t L) {
+// IO: u = b * x (x row `xr`, or 1 when NULL), and c (row `cr`, or 1) into `rc`.
+template <bool IO, typename T, int K, bool VEC>
+__device__ __forceinline__ void load_chunk(ChunkRegs<T, K, VEC>& r, ChunkC<T, K>& rc,
+                                           const T* __restrict__ ar, const T* __restrict__ br,
+                                           const T* __restrict__ xr, const T* __restrict__ cr,
+                                           int64_t t0, int64_t L) {
   using Rg = Ring<T>;
   if (VEC) {
 #pragma unroll
@@ -205,7 +261,21 @@ __device__ __forceinline__ void load_chunk(ChunkRegs<T, K, VEC>& r, const T* __r
       const bool ok = tq < L;
       const int64_t at = ok ? tq : L - 4;
       const uint4 va = *reinterpret_cast<const uint4*>(ar + at);
-      const uint4 vb = *reinterpret_cast<const uint4*>(br + at);
+      uint4 vb = *reinterpret_cast<const uint4*>(br + at);
+      if (IO && xr) {
+        const uint4 vx = *reinterpret_cast<const uint4*>(xr + at);
+        vb = make_uint4(Rg::bits(Rg::mul(Rg::from_bits(vb.x), Rg::from_bits(vx.x))),
+                        Rg::bits(Rg::mul(Rg::from_bits(vb.y), Rg::from_bits(vx.y))),
+                        Rg::bits(Rg::mul(Rg::from_bits(vb.z), Rg::from_bits(vx.z))),
+                        Rg::bits(Rg::mul(Rg::from_bits(vb.w), Rg::from_bits(vx.w))));
+      }
+      if (IO && cr) {
+        const uint4 vc = *reinterpret_cast<const uint4*>(cr + at);
+        rc.c[4 * q + 0] = Rg::from_bits(vc.x);
+        rc.c[4 * q + 1] = Rg::from_bits(vc.y);
+        rc.c[4 * q + 2] = Rg::from_bits(vc.z);
+        rc.c[4 * q + 3] = Rg::from_bits(vc.w);
+      }
       r.a[4 * q + 0] = ok ? Rg::from_bits(va.x) : Rg::one();
       r.a[4 * q + 1] = ok ? Rg::from_bits(va.y) : Rg::one();
       r.a[4 * q + 2] = ok ? Rg::from_bits(va.z) : Rg::one();
@@ -220,17 +290,19 @@ __device__ __forceinline__ void load_chunk(ChunkRegs<T, K, VEC>& r, const T* __r
     for (int k = 0; k < K; ++k) {
       const bool ok = t0 + k < L;
       const int64_t at = ok ? t0 + k : L - 1;
-      const T va = ar[at], vb = br[at];
+      const T va = ar[at];
+      T vb = br[at];
+      if (IO && xr) vb = Rg::mul(vb, xr[at]);
+      if (IO && cr) rc.c[k] = cr[at];
       r.a[k] = ok ? va : Rg::one();
       r.u[k] = ok ? vb : Rg::zero();
     }
   }
 }
 
-template <typename T, int K, bool VEC>
-__global__ __launch_bounds__(AS_THREADS) void affine_rows_kernel(
-    const T* __restrict__ a, const T* __restrict__ bx, const T* __restrict__ h0,
-    T* __restrict__ h, int64_t R, int64_t L) {
+template <typename T, int K, bool VEC, bool IO>
+__global__ __launch_bounds__(AS_THREADS) void affine_rows_kernel(const AffIO<T> io, int64_t R,
+                                                                 int64_t L) {
   constexpr int64_t CH = (int64_t)AS_THREADS * K;
   using Rg = Ring<T>;
   __shared__ T sA[2][AS_WAVES], sU[2][AS_WAVES];
@@ -240,15 +312,19 @@ __global__ __launch_bounds__(AS_THREADS) void affine_rows_kernel(
   const int64_t nch = (L + CH - 1) / CH;
 
   for (int64_t row = blockIdx.x; row < R; row += gridDim.x) {
-    const T* __restrict__ ar = a + row * L;
-    const T* __restrict__ br = bx + row * L;
-    T* __restrict__ hr = h + row * L;
-    T carry = h0 ? h0[row] : Rg::zero();
+    const T* __restrict__ ar = io.a + row * L;
+    const T* __restrict__ br = io.b + row * L;
+    const T* __restrict__ xr = (IO && io.x) ? io.x + row * L : nullptr;
+    const T* __restrict__ cr = (IO && io.c) ? io.c + row * L : nullptr;
+    T* __restrict__ hr = io.y + row * L;
+    T carry = io.h0 ? io.h0[row] : Rg::zero();
     ChunkRegs<T, K, VEC> cur, nxt;
-    load_chunk(cur, ar, br, (int64_t)tid * K, L);
+    ChunkC<T, K> ccur, cnxt;
+    load_chunk<IO>(cur, ccur, ar, br, xr, cr, (int64_t)tid * K, L);
     for (int64_t c = 0; c < nch; ++c) {
       const int64_t t0 = c * CH + (int64_t)tid * K;
-      if (c + 1 < nch) load_chunk(nxt, ar, br, t0 + CH, L);  // in flight during the scan
+      if (c + 1 < nch)  // in flight during the scan
+        load_chunk<IO>(nxt, cnxt, ar, br, xr, cr, t0 + CH, L);
       T pa[K], pu[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) {
@@ -280,30 +356,40 @@ __global__ __launch_bounds__(AS_THREADS) void affine_rows_kernel(
       }
       absorb_earlier(wA, wU, pA, pU);
       const T hs = Rg::mad(wA, carry, wU);
+      // y = c * h (IO with c), else h; the state of step L-1 also goes to h_last
+      auto outv = [&](int k) {
+        const T hv = Rg::mad(pa[k], hs, pu[k]);
+        if constexpr (IO) {
+          if (io.h_last && t0 + k == L - 1) io.h_last[row] = hv;
+          if (cr) return Rg::mul(ccur.c[k], hv);
+        }
+        return hv;
+      };
       if (VEC) {
 #pragma unroll
         for (int q = 0; q < K / 4; ++q) {
           uint4 o;
-          o.x = Rg::bits(Rg::mad(pa[4 * q + 0], hs, pu[4 * q + 0]));
-          o.y = Rg::bits(Rg::mad(pa[4 * q + 1], hs, pu[4 * q + 1]));
-          o.z = Rg::bits(Rg::mad(pa[4 * q + 2], hs, pu[4 * q + 2]));
-          o.w = Rg::bits(Rg::mad(pa[4 * q + 3], hs, pu[4 * q + 3]));
+          o.x = Rg::bits(outv(4 * q + 0));
+          o.y = Rg::bits(outv(4 * q + 1));
+          o.z = Rg::bits(outv(4 * q + 2));
+          o.w = Rg::bits(outv(4 * q + 3));
           if (t0 + 4 * q < L) *reinterpret_cast<uint4*>(hr + t0 + 4 * q) = o;
         }
       } else {
 #pragma unroll
         for (int k = 0; k < K; ++k)
-          if (t0 + k < L) hr[t0 + k] = Rg::mad(pa[k], hs, pu[k]);
+          if (t0 + k < L) hr[t0 + k] = outv(k);
       }
       carry = Rg::mad(cA, carry, cU);
       cur = nxt;
+      if constexpr (IO) ccur = cnxt;
     }
     __syncthreads();  // the totals buffers are reused by the next row
   }
 }
 
-template <typename T>
-int launch_affine(const T* a, const T* bx, const T* h0, T* h, int64_t R, int64_t L, bool vec) {
+template <typename T, bool IO>
+int launch_affine(const AffIO<T>& io, int64_t R, int64_t L, bool vec) {
   hipStream_t s = current_stream();
   constexpr int64_t CH = (int64_t)AS_THREADS * AS_K;
   int dev = 0, cus = 0;
@@ -315,12 +401,8 @@ int launch_affine(const T* a, const T* bx, const T* h0, T* h, int64_t R, int64_t
   if (L > CH && R >= 8 * (int64_t)cus) {
     // enough rows to fill the machine: one workgroup per row, carries stay on chip
     const int64_t grid = R < ((int64_t)1 << 30) ? R : ((int64_t)1 << 30);
-    if (vec)
-      hipLaunchKernelGGL((affine_rows_kernel<T, AS_K, true>), dim3((unsigned)grid),
-                         dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L);
-    else
-      hipLaunchKernelGGL((affine_rows_kernel<T, AS_K, false>), dim3((unsigned)grid),
-                         dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L);
+    auto kern = vec ? affine_rows_kernel<T, AS_K, true, IO> : affine_rows_kernel<T, AS_K, false, IO>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(AS_THREADS), 0, s, io, R, L);
     return check_launch("affine_rows_kernel");
   }
   const int64_t nchunks = (L + CH - 1) / CH;
@@ -334,14 +416,9 @@ int launch_affine(const T* a, const T* bx, const T* h0, T* h, int64_t R, int64_t
     int st = ss.reserve((size_t)total * 3, (uint32_t)(total + grid), s);
     if (st != SW_OK) return st;
   }
-  if (vec)
-    hipLaunchKernelGGL((affine_scan_kernel<T, AS_K, true>), dim3((unsigned)grid),
-                       dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L, nchunks, total, ss.carry,
-                       ss.ticket, ss.ticket_base, ss.epoch);
-  else
-    hipLaunchKernelGGL((affine_scan_kernel<T, AS_K, false>), dim3((unsigned)grid),
-                       dim3(AS_THREADS), 0, s, a, bx, h0, h, R, L, nchunks, total, ss.carry,
-                       ss.ticket, ss.ticket_base, ss.epoch);
+  auto kern = vec ? affine_scan_kernel<T, AS_K, true, IO> : affine_scan_kernel<T, AS_K, false, IO>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(AS_THREADS), 0, s, io, R, L, nchunks, total,
+                     ss.carry, ss.ticket, ss.ticket_base, ss.epoch);
   int st = check_launch("affine_scan_kernel");
   if (st != SW_OK) ss.invalidate();
   return st;
@@ -351,12 +428,25 @@ int launch_affine(const T* a, const T* bx, const T* h0, T* h, int64_t R, int64_t
 
 int affine_scan_f32(const float* a, const float* bx, const float* h0, float* h, int64_t R,
                     int64_t L, bool vec) {
-  return launch_affine<float>(a, bx, h0, h, R, L, vec);
+  return launch_affine<float, false>(AffIO<float>{a, bx, nullptr, nullptr, h0, h, nullptr}, R, L,
+                                     vec);
 }
 
 int affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
                     int64_t R, int64_t L, bool vec) {
-  return launch_affine<uint32_t>(a, bx, h0, h, R, L, vec);
+  return launch_affine<uint32_t, false>(
+      AffIO<uint32_t>{a, bx, nullptr, nullptr, h0, h, nullptr}, R, L, vec);
+}
+
+int affine_scan_io_f32(const float* a, const float* b, const float* x, const float* c,
+                       const float* h0, float* y, float* h_last, int64_t R, int64_t L, bool vec) {
+  return launch_affine<float, true>(AffIO<float>{a, b, x, c, h0, y, h_last}, R, L, vec);
+}
+
+int affine_scan_io_u32(const uint32_t* a, const uint32_t* b, const uint32_t* x, const uint32_t* c,
+                       const uint32_t* h0, uint32_t* y, uint32_t* h_last, int64_t R, int64_t L,
+                       bool vec) {
+  return launch_affine<uint32_t, true>(AffIO<uint32_t>{a, b, x, c, h0, y, h_last}, R, L, vec);
 }
 
 }  // namespace sw

@@ -17,6 +17,11 @@ int affine_scan_f32(const float* a, const float* bx, const float* h0, float* h, 
                     int64_t L, bool vec);
 int affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
                     int64_t R, int64_t L, bool vec);
+int affine_scan_io_f32(const float* a, const float* b, const float* x, const float* c,
+                       const float* h0, float* y, float* h_last, int64_t R, int64_t L, bool vec);
+int affine_scan_io_u32(const uint32_t* a, const uint32_t* b, const uint32_t* x, const uint32_t* c,
+                       const uint32_t* h0, uint32_t* y, uint32_t* h_last, int64_t R, int64_t L,
+                       bool vec);
 
 namespace {
 thread_local hipStream_t tls_stream = nullptr;
@@ -118,6 +123,47 @@ int affine_common(const T* a, const T* bx, const T* h0, T* h_out, int64_t B, int
   if ((st = check_spans(outs, 1, ins, 3)) != SW_OK) return st;
   const bool vec = L % 4 == 0 && all_aligned16({a, bx, h_out});
   return run(a, bx, h0, h_out, R, L, vec);
+}
+
+// Validation of the output-projection form (Eq. (3)-(4)); see include/scanweaver.h.
+template <typename T>
+int affine_proj_common(const T* a, const T* b, const T* x, const T* c, const T* h0, T* y,
+                       T* h_last, int64_t B, int64_t D, int64_t L,
+                       int (*run)(const T*, const T*, const T*, const T*, const T*, T*, T*,
+                                  int64_t, int64_t, bool)) {
+  if (B < 0 || D < 0 || L < 0)
+    return fail(SW_ERR_INVALID_ARG, "negative size (B=%lld D=%lld L=%lld)", (long long)B,
+                (long long)D, (long long)L);
+  int64_t R, n;
+  if (!mul_ok(B, D, &R) || !mul_ok(R, L, &n) || !mul_ok(n, (int64_t)sizeof(T), &n))
+    return fail(SW_ERR_UNSUPPORTED, "B*D*L overflows");
+  if (R == 0) return SW_OK;
+  int dev, st;
+  if ((st = current_device(&dev)) != SW_OK) return st;
+  const size_t big = (size_t)n, small = (size_t)R * sizeof(T);
+  if ((st = check_ptr(h0, sizeof(T), "h0", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(h_last, sizeof(T), "h_last", false, dev)) != SW_OK) return st;
+  if (L == 0) {
+    if (!h_last) return SW_OK;
+    Span o[] = {{h_last, small, "h_last"}};
+    Span i[] = {{h0, small, "h0"}};
+    if ((st = check_spans(o, 1, i, 1)) != SW_OK) return st;
+    if (!h0) return zero_words(reinterpret_cast<uint32_t*>(h_last), (size_t)R, current_stream());
+    // the final state of an empty sequence is the initial one
+    hipError_t e = hipMemcpyAsync(h_last, h0, small, hipMemcpyDeviceToDevice, current_stream());
+    if (e != hipSuccess) return fail(SW_ERR_HIP, "h_last copy: %s", hipGetErrorString(e));
+    return SW_OK;
+  }
+  if ((st = check_ptr(a, sizeof(T), "a", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(b, sizeof(T), "b", true, dev)) != SW_OK) return st;
+  if ((st = check_ptr(x, sizeof(T), "x", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(c, sizeof(T), "c", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(y, sizeof(T), "y", true, dev)) != SW_OK) return st;
+  Span outs[] = {{y, big, "y"}, {h_last, small, "h_last"}};
+  Span ins[] = {{a, big, "a"}, {b, big, "b"}, {x, big, "x"}, {c, big, "c"}, {h0, small, "h0"}};
+  if ((st = check_spans(outs, 2, ins, 5)) != SW_OK) return st;
+  const bool vec = L % 4 == 0 && all_aligned16({a, b, x, c, y});
+  return run(a, b, x, c, h0, y, h_last, R, L, vec);
 }
 
 // Validation shared by the fused entry points; see include/scanweaver.h.
@@ -317,6 +363,22 @@ SW_API int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t
                                      reinterpret_cast<const uint32_t*>(h0),
                                      reinterpret_cast<uint32_t*>(h_out), B, D, L,
                                      sw::affine_scan_u32);
+}
+
+SW_API int sw_affine_scan_proj(const float* a, const float* b, const float* x, const float* c,
+                               const float* h0, float* y, float* h_last, int64_t B, int64_t D,
+                               int64_t L) {
+  return sw::affine_proj_common<float>(a, b, x, c, h0, y, h_last, B, D, L, sw::affine_scan_io_f32);
+}
+
+SW_API int sw_affine_scan_proj_i32(const int32_t* a, const int32_t* b, const int32_t* x,
+                                   const int32_t* c, const int32_t* h0, int32_t* y,
+                                   int32_t* h_last, int64_t B, int64_t D, int64_t L) {
+  using U = const uint32_t*;
+  return sw::affine_proj_common<uint32_t>(U(a), U(b), U(x), U(c), U(h0),
+                                          reinterpret_cast<uint32_t*>(y),
+                                          reinterpret_cast<uint32_t*>(h_last), B, D, L,
+                                          sw::affine_scan_io_u32);
 }
 
 SW_API int sw_selective_scan_fwd(const float* x, const float* delta, const float* A,

@@ -65,6 +65,11 @@ def test_validation_without_gpu(lib):
     # overflowing sizes are refused
     big = 1 << 40
     assert lib.sw_affine_scan(None, None, None, None, big, big, 4) == 2
+    # the projection form: negative sizes, then empty shapes are a no-op
+    assert lib.sw_affine_scan_proj(*([None] * 7), -1, 1, 1) == 1
+    assert lib.sw_affine_scan_proj_i32(*([None] * 7), 1, 1, -1) == 1
+    assert lib.sw_affine_scan_proj(*([None] * 7), 0, 4, 9) == 0
+    assert lib.sw_affine_scan_proj_i32(*([None] * 7), big, big, 4) == 2
     # the extended fused entry point: unknown dtypes and flags are refused
     # before anything else; otherwise it validates like the plain one
     ex = lib.sw_selective_scan_fwd_ex

@@ -445,3 +445,91 @@ def test_selective_mamba_options_full_size(sw):
         hg = hl.reshape(w.B * w.D, w.N).index_select(
             0, torch.as_tensor(rows, device="cuda")).cpu().numpy()
         assert_gate(fp_gate(hg, o["h_last"], o["h_mag"], o["h_sens"]), "full-size h_last")
+
+
+# --------------------------------- Eq. (3)-(4): input and output projections
+
+def _proj_inputs(B, D, L, seed, dtype="f32"):
+    """a in [-1.05, 1.05] (growth and sign changes included), b, x, c ~ N(0,1),
+    h0 ~ N(0,1); int32: full-range words with odd a."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    if dtype == "i32":
+        a, b, x, c = (rng.integers(-2**31, 2**31, size=(B, D, L), dtype=np.int64)
+                      .astype(np.int32) for _ in range(4))
+        a |= 1
+        h0 = rng.integers(-2**31, 2**31, size=(B, D), dtype=np.int64).astype(np.int32)
+        return a, b, x, c, h0
+    a = rng.uniform(-1.05, 1.05, size=(B, D, L)).astype(np.float32)
+    b, x, c = (rng.standard_normal(size=(B, D, L)).astype(np.float32) for _ in range(3))
+    h0 = rng.standard_normal(size=(B, D)).astype(np.float32)
+    return a, b, x, c, h0
+
+
+# (B, D, L): element path (ragged L), one chunk, look-back chunks, and >= 2048
+# rows longer than a chunk (the row-per-workgroup kernel), vector and ragged
+_PROJ_SHAPES = [(2, 5, 37), (3, 7, 1024), (1, 3, 5003), (1, 2, 20480), (2, 1100, 4100),
+                (1, 2100, 2049)]
+_PROJ_OPTS = [("x", "c", "h0"), ("c",), ("x",), ()]
+
+
+@pytest.mark.parametrize("shape", _PROJ_SHAPES)
+@pytest.mark.parametrize("opts", _PROJ_OPTS)
+def test_proj_f32(sw, shape, opts):
+    B, D, L = shape
+    _say("case proj f32", shape, opts)
+    a, b, x, c, h0 = _proj_inputs(B, D, L, 9000 + L)
+    x = x if "x" in opts else None
+    c = c if "c" in opts else None
+    h0 = h0 if "h0" in opts else None
+    y, hl = sw.affine_scan_proj(dev(a), dev(b), None if x is None else dev(x),
+                                None if c is None else dev(c), None if h0 is None else dev(h0))
+    ref, href, ym, ys = oracle.affine_proj(a, b, x, c, h0, bounds=True)
+    assert_gate(fp_gate(y.cpu().numpy(), ref, ym, ys), f"proj y {shape} {opts}")
+    # h_last: the state before the output projection, gated by the state bounds
+    _, hm, hs = oracle.affine_scan(a, b * (x if x is not None else 1.0),
+                                   h0, bounds=True)
+    assert_gate(fp_gate(hl.cpu().numpy(), href, hm[..., -1], hs[..., -1]),
+                f"proj h_last {shape} {opts}")
+
+
+@pytest.mark.parametrize("shape", _PROJ_SHAPES)
+def test_proj_i32_bitexact(sw, shape):
+    B, D, L = shape
+    _say("case proj i32", shape)
+    a, b, x, c, h0 = _proj_inputs(B, D, L, 9100 + L, "i32")
+    for xx, cc, hh in ((x, c, h0), (None, c, None), (x, None, h0)):
+        y, hl = sw.affine_scan_proj_i32(*(None if v is None else dev(v)
+                                          for v in (a, b, xx, cc, hh)))
+        ry, rh = oracle.affine_proj_i32(a, b, xx, cc, hh)
+        assert np.array_equal(y.cpu().numpy(), ry)
+        assert np.array_equal(hl.cpu().numpy(), rh)
+
+
+def test_proj_weighted_prefix_is_the_bare_scan(sw):
+    """Eq. (10) through the projection form (x = c = 1) runs the bare scan's
+    arithmetic on the pairs (alpha, beta): bit-identical to sw_affine_scan,
+    in both kernels, and within the gate of the oracle."""
+    rng = np.random.Generator(np.random.PCG64(67))
+    for B, D, L in ((2, 7, 3000), (2, 1100, 4100)):
+        alpha = rng.uniform(0.0, 1.0, size=(B, D, L)).astype(np.float32)
+        beta = rng.uniform(0.0, 1.0, size=(B, D, L)).astype(np.float32)
+        y, hl = sw.affine_scan_proj(dev(alpha), dev(beta))
+        h = sw.affine_scan(dev(alpha), dev(beta))
+        assert torch.equal(y, h)
+        assert torch.equal(hl, h[..., -1])
+        ref, _, ym, ys = oracle.affine_proj(alpha, beta, bounds=True)
+        assert_gate(fp_gate(y.cpu().numpy(), ref, ym, ys), f"weighted prefix {B}x{D}x{L}")
+
+
+def test_proj_empty_and_L0(sw):
+    e = torch.empty((2, 3, 0), device="cuda")
+    h0 = torch.randn((2, 3), device="cuda")
+    y, hl = sw.affine_scan_proj(e, e, h0=h0)
+    torch.cuda.synchronize()
+    assert y.shape == (2, 3, 0) and torch.equal(hl, h0)
+    y, hl = sw.affine_scan_proj(e, e)
+    torch.cuda.synchronize()
+    assert torch.equal(hl, torch.zeros_like(h0))
+    e = torch.empty((0, 3, 5), device="cuda")
+    y, hl = sw.affine_scan_proj(e, e)
+    assert y.shape == (0, 3, 5) and hl.shape == (0, 3)

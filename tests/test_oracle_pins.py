@@ -588,3 +588,84 @@ def test_fused_output_gate():
     np.testing.assert_allclose(zp["y"] + zm["y"], plain["y"] * z64 * np.tanh(z64 / 2),
                                rtol=1e-12, atol=1e-14 * plain["y_mag"].max())
     assert np.all(zp["y_mag"] <= plain["y_mag"] * np.abs(z64) * (1 + 1e-15))
+
+
+# ------------------------------------ Eq. (3)-(4) with input/output projections
+
+@pytest.mark.parametrize("seed,L", [(601, 1), (602, 9), (603, 20)])
+def test_proj_matches_eq4_bruteforce(seed, L):
+    """y_t = c_t h_t with h from Eq. (5) on u_k = b_k x_k, in exact rationals."""
+    rng = _rng(seed)
+    rows = 3
+    a = rng.uniform(-1.2, 1.2, size=(rows, L)).astype(np.float32)
+    b, x, c = (rng.standard_normal(size=(rows, L)).astype(np.float32) for _ in range(3))
+    h0 = rng.standard_normal(size=(rows,)).astype(np.float32)
+    y, h_last, ym, ys = oracle.affine_proj(a, b, x, c, h0, bounds=True)
+    for r in range(rows):
+        u = b[r].astype(np.float64) * x[r].astype(np.float64)  # exact: 24 + 24 bits
+        exact = _brute_eq5(a[r], u, h0[r])
+        for t in range(L):
+            yt = _frac(c[r, t]) * exact[t]
+            assert abs(y[r, t] - float(yt)) <= 1e-14 * (ym[r, t] + ys[r, t]) + 1e-300
+        assert abs(h_last[r] - float(exact[-1])) <= 1e-14 * (abs(float(exact[-1])) + 1) * L
+
+
+@pytest.mark.parametrize("seed,L", [(611, 1), (612, 40)])
+def test_proj_int_matches_eq4_bruteforce(seed, L):
+    rng = _rng(seed)
+    rows = 2
+    a, b, x, c = (rng.integers(-2**31, 2**31, size=(rows, L), dtype=np.int64).astype(np.int32)
+                  for _ in range(4))
+    a |= 1  # units: every prefix product keeps all bits, so no carry can hide
+    h0 = rng.integers(-2**31, 2**31, size=(rows,), dtype=np.int64).astype(np.int32)
+    y, h_last = oracle.affine_proj_i32(a, b, x, c, h0)
+    for r in range(rows):
+        u = ((b[r].astype(np.int64) & MASK) * (x[r].astype(np.int64) & MASK)) & MASK
+        h = _brute_eq5_int(a[r], u, h0[r]).view(np.uint32).astype(np.uint64)
+        yr = ((c[r].view(np.uint32).astype(np.uint64) * h) & MASK).astype(np.uint32)
+        assert np.array_equal(y[r].view(np.uint32), yr)
+        assert h_last[r] == h[-1].astype(np.uint32).view(np.int32)
+
+
+def test_proj_closed_forms():
+    """a = 1, b = 1: h is h0 plus the prefix sum of x (exact on integers), so
+    y = c (h0 + cumsum x).  Weighted prefix of Eq. (10) with constant
+    alpha = 1/2, beta = 1 (x = c = ones): h_t = 2 - (2 - h0) 2^-(t+1)."""
+    rng = _rng(621)
+    L = 300
+    x = rng.integers(-50, 50, size=(2, L)).astype(np.float32)
+    c = rng.integers(-4, 5, size=(2, L)).astype(np.float32)
+    h0 = np.array([3.0, -7.0], np.float32)
+    ones = np.ones((2, L), np.float32)
+    y, hl = oracle.affine_proj(ones, ones, x, c, h0)
+    expect = c.astype(np.float64) * (h0[:, None] + np.cumsum(x.astype(np.float64), axis=1))
+    assert np.array_equal(y, expect)
+    assert np.array_equal(hl, h0 + x.astype(np.float64).sum(axis=1))
+    half = np.full((2, 40), 0.5, np.float32)
+    y, hl = oracle.affine_proj(half, np.ones((2, 40), np.float32), None, None, h0)
+    t = np.arange(40)
+    expect = 2.0 - (2.0 - h0[:, None].astype(np.float64)) * 2.0 ** -(t + 1)
+    assert np.array_equal(y, expect)  # dyadic with < 53 significant bits: exact in fp64
+    assert np.array_equal(hl, expect[:, -1])
+
+
+def test_proj_int_weighted_prefix_closed_form():
+    """int32 ring, alpha = -1, beta = 1 (Eq. (10)): h_t alternates between
+    1 - h0 and h0 modulo 2^32."""
+    L = 7
+    a = np.full((1, L), -1, np.int32)
+    b = np.ones((1, L), np.int32)
+    h0 = np.array([2**31 - 5], np.int32)
+    y, hl = oracle.affine_proj_i32(a, b, None, None, h0)
+    alt = [(1 - int(h0[0])) & MASK, int(h0[0]) & MASK]
+    assert [int(v) & MASK for v in y[0]] == [alt[t % 2] for t in range(L)]
+    assert (int(hl[0]) & MASK) == alt[(L - 1) % 2]
+
+
+def test_proj_empty_sequence_keeps_h0():
+    h0 = np.array([1.5, -2.0], np.float32)
+    e = np.zeros((2, 0), np.float32)
+    y, hl = oracle.affine_proj(e, e, None, None, h0)
+    assert y.shape == (2, 0) and np.array_equal(hl, h0.astype(np.float64))
+    y, hl = oracle.affine_proj(e, e)
+    assert np.array_equal(hl, np.zeros(2))
