@@ -89,6 +89,9 @@ def _load():
         lib.swo_selective_scan_ex_f64.argtypes = ([_vp] * 10 + [ctypes.c_int] + [_vp] * 6
                                                   + [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int])
         lib.swo_selective_scan_ex_f64.restype = ctypes.c_int
+        lib.swo_selective_scan_bwd_f64.argtypes = ([_vp] * 10 + [ctypes.c_int] + [_vp] * 12
+                                                   + [_i64] * 4 + [ctypes.c_int])
+        lib.swo_selective_scan_bwd_f64.restype = ctypes.c_int
         lib.swo_selective_scan_f32seq.argtypes = [_vp] * 9 + [_i64, _i64, _i64, ctypes.c_int]
         lib.swo_selective_scan_f32seq.restype = ctypes.c_int
         _lib = lib
@@ -358,3 +361,62 @@ def selective_scan_seq32(x, delta, A, Bm, Cm, Dskip=None, rows=None, threads: in
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     return _unflatten({"y": y, "h_last": h_last}, f)
+
+
+def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip=None, dy=None, dh_last=None, *, z=None,
+                       delta_bias=None, h0=None, delta_softplus: bool = False, rows=None,
+                       bounds: bool = False, threads: int = 0):
+    """Backward of the fused selective scan in fp64 (chain rule through the
+    forward loop; see sw_oracle.c): gradients of sum(dy * y) + sum(dh_last *
+    h_last) with respect to every input.
+
+    Inputs as for :func:`selective_scan`; ``dy`` (B, D, L), ``dh_last``
+    (B, D, N) or None.  Returns a dict with ``dx, ddelta`` (and ``dz`` when z
+    is given) of shape (B, D, L), ``dh0`` (B, D, N), ``dA`` (D, N), ``dDskip``
+    and ``ddelta_bias`` (D,), ``dB, dC`` (B, L, N).  With ``rows`` (flat row
+    indices b*D + d) only those rows are evaluated: per-row outputs get a
+    leading axis of len(rows), ``dA_rows`` (R, N), ``dDskip_rows`` and
+    ``ddelta_bias_rows`` (R,) hold each row's share, and ``dB, dC`` are summed
+    over the given rows only.  With ``bounds=True`` every output ``k`` also
+    has ``m_k``, the magnitude (sum of absolute values of its terms).
+    """
+    f = _selective_rows(x, delta, A, Bm, Cm, Dskip, rows, z=z, delta_bias=delta_bias, h0=h0)
+    Bsz, D, L, N, R = f["Bsz"], f["D"], f["L"], f["N"], f["R"]
+    sel = slice(None) if f["ridx"] is None else f["ridx"]
+    dys = _as(np.asarray(dy, np.float32).reshape(Bsz * D, L)[sel], np.float32)
+    dhl = None if dh_last is None else _as(
+        np.asarray(dh_last, np.float32).reshape(Bsz * D, N)[sel], np.float32)
+    out = {k: np.zeros((R, L)) for k in ("dx", "ddelta")}
+    out["dz"] = np.zeros((R, L)) if z is not None else None
+    out["dh0"] = np.zeros((R, N))
+    out["dA_rows"] = np.zeros((R, N))
+    out["dDskip_rows"] = np.zeros(R)
+    out["ddelta_bias_rows"] = np.zeros(R)
+    out["dB"] = np.zeros((Bsz, L, N))
+    out["dC"] = np.zeros((Bsz, L, N))
+    names = ["dx", "ddelta", "dz", "dA_rows", "dDskip_rows", "ddelta_bias_rows", "dh0", "dB", "dC"]
+    mags = None
+    if bounds:
+        for k in names:
+            out["m_" + k] = None if out[k] is None else np.zeros_like(out[k])
+        mags = (ctypes.c_void_p * 9)(*[_p(out["m_" + k]) for k in names])
+    rc = _load().swo_selective_scan_bwd_f64(
+        _p(f["xs"]), _p(f["ds"]), _p(f["As"]), _p(f["Bs"]), _p(f["Cs"]), _p(f["row_b"]),
+        _p(f["Ds"]), _p(f["zs"]), _p(f["dbs"]), _p(f["h0s"]), int(bool(delta_softplus)),
+        _p(dys), _p(dhl), _p(out["dx"]), _p(out["ddelta"]), _p(out["dz"]), _p(out["dA_rows"]),
+        _p(out["dDskip_rows"]), _p(out["ddelta_bias_rows"]), _p(out["dh0"]), _p(out["dB"]),
+        _p(out["dC"]), mags, Bsz, R, N, L, int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    if f["ridx"] is None:
+        for k in ("dx", "ddelta", "dz", "dh0"):
+            for kk in (k, "m_" + k):
+                if out.get(kk) is not None:
+                    out[kk] = out[kk].reshape((Bsz, D) + out[kk].shape[1:])
+        for src, dst in (("dA_rows", "dA"), ("dDskip_rows", "dDskip"),
+                         ("ddelta_bias_rows", "ddelta_bias")):
+            for pre in ("", "m_"):
+                if (pre + src) in out:
+                    v = out.pop(pre + src)
+                    out[pre + dst] = v.reshape((Bsz, D) + v.shape[1:]).sum(axis=0)
+    return out

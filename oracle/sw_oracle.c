@@ -409,6 +409,262 @@ int swo_selective_scan_f64(const float* x, const float* delta, const float* A, c
 }
 
 /* ------------------------------------------------------------------------ */
+/* Backward of the fused form (the gradient of a scalar loss
+ * sum_t dy_t y_t + sum_n dh_last_n h_last_n with respect to every input),
+ * by the chain rule through the forward loop above.  The paper gives the
+ * forward only; the adjoint of Eq. (3) is the same kind of recurrence run
+ * backwards in time:
+ *   ds_t      = dy_t g_t                       (g_t = silu(z_t), or 1)
+ *   lam_t     = ds_t C_{t,n} + a_{t+1,n} lam_{t+1},   lam_{L} term = dh_last_n
+ *   dh0_n     = a_{0,n} lam_0
+ *   dC_{t,n} += ds_t h_{t,n}                   (summed over the rows of a batch)
+ *   dB_{t,n} += lam_t delta_t x_t              (summed over the rows of a batch)
+ *   ddelta'_t = sum_n lam_t (a_t h_{t-1} A_n + B_{t,n} x_t)
+ *   dx_t      = sum_n lam_t delta_t B_{t,n} + ds_t Dskip
+ *   dA_n     += sum_t lam_t a_t h_{t-1} delta_t
+ *   dDskip   += sum_t ds_t x_t
+ *   dz_t      = dy_t s_t silu'(z_t),  s_t = sum_n C h + Dskip x (pre-gate y)
+ *   ddelta_t  = ddelta'_t sigmoid(delta_t + bias) with softplus, else ddelta'_t
+ *   dbias    += sum_t ddelta_t
+ * where delta is the delta after bias and softplus.  Each row also gets the
+ * magnitude of every output: the same expressions evaluated on absolute
+ * values with |h| replaced by the forward magnitude M_t and lam by
+ *   Mlam_t = |ds_t C_{t,n}| + |a_{t+1}| Mlam_{t+1},   Mlam_L = |dh_last|,
+ * which bounds the sum of the absolute values of the terms of each output.
+ * Per-row outputs: dx, ddelta, dz (R, L); dh0 (R, N); the row's share of dA
+ * (R, N), dDskip and dbias (R).  dB and dC (nb, L, N) are summed over the
+ * rows of each batch (each thread accumulates its own copy; the copies are
+ * added in thread order). */
+
+typedef struct {
+  const float *x, *delta, *A, *Bm, *Cm, *Dskip, *z, *delta_bias, *h0, *dy, *dh_last;
+  const int64_t* row_b;
+  int softplus;
+  double *dx, *ddelta, *dz, *dA, *dD, *dbias, *dh0;
+  double *mdx, *mddelta, *mdz, *mdA, *mdD, *mdbias, *mdh0;
+  double *accB, *accC, *accMB, *accMC; /* per thread: nthreads x (nb, L, N) */
+  int64_t nb, N, L;
+} bwd_ctx;
+
+static void bwd_rows(int64_t r0, int64_t r1, int ti, const void* vctx) {
+  const bwd_ctx* c = (const bwd_ctx*)vctx;
+  const int64_t N = c->N, L = c->L;
+  const int64_t per = c->nb * L * N;
+  double* aB = c->accB + (int64_t)ti * per;
+  double* aC = c->accC + (int64_t)ti * per;
+  double* aMB = c->accMB ? c->accMB + (int64_t)ti * per : NULL;
+  double* aMC = c->accMC ? c->accMC + (int64_t)ti * per : NULL;
+  /* per-row work arrays */
+  double* dl = (double*)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1) * 7);
+  double* hs = (double*)malloc(sizeof(double) * (size_t)(L + 1) * 2);
+  if (!dl || !hs) {
+    free(dl);
+    free(hs);
+    return;
+  }
+  double* sg = dl + L;     /* d delta / d raw delta */
+  double* g = dl + 2 * L;  /* gate */
+  double* gp = dl + 3 * L; /* gate derivative */
+  double* ds = dl + 4 * L;
+  double* s = dl + 5 * L;  /* pre-gate y */
+  double* ms = dl + 6 * L; /* its magnitude */
+  double* mh = hs + (L + 1);
+  for (int64_t r = r0; r < r1; r++) {
+    const float* x = c->x + r * L;
+    const float* dyr = c->dy + r * L;
+    const int64_t b = c->row_b[r];
+    const float* Bm = c->Bm + b * L * N;
+    const float* Cm = c->Cm + b * L * N;
+    const double Dr = c->Dskip ? (double)c->Dskip[r] : 0.0;
+    for (int64_t t = 0; t < L; t++) {
+      const double raw = (double)c->delta[r * L + t] + (c->delta_bias ? (double)c->delta_bias[r] : 0.0);
+      if (c->softplus) {
+        dl[t] = log1p(exp(raw));
+        sg[t] = 1.0 / (1.0 + exp(-raw));
+      } else {
+        dl[t] = raw;
+        sg[t] = 1.0;
+      }
+      if (c->z) {
+        const double zv = (double)c->z[r * L + t];
+        const double sig = 1.0 / (1.0 + exp(-zv));
+        g[t] = zv * sig;
+        gp[t] = sig * (1.0 + zv * (1.0 - sig));
+      } else {
+        g[t] = 1.0;
+        gp[t] = 0.0;
+      }
+      ds[t] = (double)dyr[t] * g[t];
+      s[t] = Dr * (double)x[t];
+      ms[t] = fabs(Dr * (double)x[t]);
+      c->dx[r * L + t] = ds[t] * Dr;
+      c->ddelta[r * L + t] = 0.0;
+      if (c->mdx) c->mdx[r * L + t] = fabs(ds[t] * Dr);
+      if (c->mddelta) c->mddelta[r * L + t] = 0.0;
+    }
+    double dD_sum = 0.0, mD_sum = 0.0;
+    for (int64_t n = 0; n < N; n++) {
+      const double An = (double)c->A[r * N + n];
+      /* forward: hs[t+1] = h_t, hs[0] = h_{-1} */
+      hs[0] = c->h0 ? (double)c->h0[r * N + n] : 0.0;
+      mh[0] = fabs(hs[0]);
+      for (int64_t t = 0; t < L; t++) {
+        const double a = exp(dl[t] * An);
+        const double u = dl[t] * (double)x[t] * (double)Bm[t * N + n];
+        hs[t + 1] = a * hs[t] + u;
+        mh[t + 1] = fabs(a) * mh[t] + fabs(u);
+        s[t] += (double)Cm[t * N + n] * hs[t + 1];
+        ms[t] += fabs((double)Cm[t * N + n]) * mh[t + 1];
+      }
+      /* backward */
+      double lam_next = c->dh_last ? (double)c->dh_last[r * N + n] : 0.0;
+      double mlam_next = fabs(lam_next);
+      double dA_n = 0.0, mA_n = 0.0;
+      for (int64_t t = L - 1; t >= 0; t--) {
+        const double a = exp(dl[t] * An);
+        const double Bt = (double)Bm[t * N + n], Ct = (double)Cm[t * N + n];
+        const double lam = ds[t] * Ct + lam_next;
+        const double mlam = fabs(ds[t] * Ct) + mlam_next;
+        const double xb = (double)x[t] * Bt;
+        c->ddelta[r * L + t] += lam * (a * hs[t] * An + xb);
+        c->dx[r * L + t] += lam * dl[t] * Bt;
+        if (c->mddelta) c->mddelta[r * L + t] += mlam * (fabs(a * An) * mh[t] + fabs(xb));
+        if (c->mdx) c->mdx[r * L + t] += mlam * fabs(dl[t] * Bt);
+        dA_n += lam * a * hs[t] * dl[t];
+        mA_n += mlam * fabs(a * dl[t]) * mh[t];
+        aB[(b * L + t) * N + n] += lam * dl[t] * (double)x[t];
+        aC[(b * L + t) * N + n] += ds[t] * hs[t + 1];
+        if (aMB) aMB[(b * L + t) * N + n] += mlam * fabs(dl[t] * (double)x[t]);
+        if (aMC) aMC[(b * L + t) * N + n] += fabs(ds[t]) * mh[t + 1];
+        lam_next = a * lam;
+        mlam_next = fabs(a) * mlam;
+      }
+      c->dA[r * N + n] = dA_n;
+      if (c->mdA) c->mdA[r * N + n] = mA_n;
+      if (c->dh0) c->dh0[r * N + n] = lam_next;
+      if (c->mdh0) c->mdh0[r * N + n] = mlam_next;
+    }
+    double dbias = 0.0, mbias = 0.0;
+    for (int64_t t = 0; t < L; t++) {
+      dD_sum += ds[t] * (double)x[t];
+      mD_sum += fabs(ds[t] * (double)x[t]);
+      c->ddelta[r * L + t] *= sg[t];
+      if (c->mddelta) c->mddelta[r * L + t] *= fabs(sg[t]);
+      dbias += c->ddelta[r * L + t];
+      if (c->mddelta) mbias += c->mddelta[r * L + t];
+      if (c->dz) {
+        c->dz[r * L + t] = (double)dyr[t] * s[t] * gp[t];
+        if (c->mdz) c->mdz[r * L + t] = fabs((double)dyr[t] * gp[t]) * ms[t];
+      }
+    }
+    c->dD[r] = dD_sum;
+    if (c->mdD) c->mdD[r] = mD_sum;
+    c->dbias[r] = dbias;
+    if (c->mdbias) c->mdbias[r] = mbias;
+  }
+  free(dl);
+  free(hs);
+}
+
+typedef void (*row_fn_i)(int64_t r0, int64_t r1, int ti, const void* ctx);
+
+typedef struct {
+  row_fn_i fn;
+  const void* ctx;
+  int64_t r0, r1;
+  int ti;
+} worker_arg_i;
+
+static void* worker_main_i(void* p) {
+  worker_arg_i* w = (worker_arg_i*)p;
+  w->fn(w->r0, w->r1, w->ti, w->ctx);
+  return NULL;
+}
+
+/* run_rows with the worker's index passed along (for per-thread buffers) */
+static void run_rows_i(row_fn_i fn, const void* ctx, int64_t rows, int t) {
+  if (t <= 1) {
+    fn(0, rows, 0, ctx);
+    return;
+  }
+  pthread_t tid[256];
+  worker_arg_i args[256];
+  int64_t per = rows / t, extra = rows % t, r = 0;
+  for (int i = 0; i < t; i++) {
+    int64_t n = per + (i < extra ? 1 : 0);
+    args[i].fn = fn;
+    args[i].ctx = ctx;
+    args[i].r0 = r;
+    args[i].r1 = r + n;
+    args[i].ti = i;
+    r += n;
+    if (pthread_create(&tid[i], NULL, worker_main_i, &args[i]) != 0) {
+      fn(args[i].r0, args[i].r1, i, ctx);
+      args[i].fn = NULL;
+    }
+  }
+  for (int i = 0; i < t; i++)
+    if (args[i].fn) pthread_join(tid[i], NULL);
+}
+
+int swo_selective_scan_bwd_f64(const float* x, const float* delta, const float* A, const float* Bm,
+                               const float* Cm, const int64_t* row_b, const float* Dskip,
+                               const float* z, const float* delta_bias, const float* h0,
+                               int softplus, const float* dy, const float* dh_last, double* dx,
+                               double* ddelta, double* dz, double* dA, double* dD, double* dbias,
+                               double* dh0, double* dB, double* dC, double* const* mags,
+                               int64_t nb, int64_t R, int64_t N, int64_t L, int nthreads) {
+  if (!x || !delta || !A || !Bm || !Cm || !row_b || !dy || !dx || !ddelta || !dA || !dD ||
+      !dbias || !dB || !dC || nb < 0 || R < 0 || N < 0 || L < 0)
+    return 1;
+  if (z && !dz) return 1;
+  for (int64_t r = 0; r < R; r++)
+    if (row_b[r] < 0 || row_b[r] >= nb) return 1;
+  const int t = swo_threads_used(nthreads, R);
+  const int64_t per = nb * L * N;
+  const int want_m = mags != NULL;
+  double* acc = (double*)calloc((size_t)t * (size_t)per * (want_m ? 4 : 2) + 1, sizeof(double));
+  if (!acc) return 1;
+  bwd_ctx c;
+  memset(&c, 0, sizeof(c));
+  c.x = x; c.delta = delta; c.A = A; c.Bm = Bm; c.Cm = Cm; c.Dskip = Dskip; c.z = z;
+  c.delta_bias = delta_bias; c.h0 = h0; c.dy = dy; c.dh_last = dh_last; c.row_b = row_b;
+  c.softplus = softplus != 0;
+  c.dx = dx; c.ddelta = ddelta; c.dz = dz; c.dA = dA; c.dD = dD; c.dbias = dbias; c.dh0 = dh0;
+  if (want_m) {
+    c.mdx = mags[0]; c.mddelta = mags[1]; c.mdz = mags[2]; c.mdA = mags[3]; c.mdD = mags[4];
+    c.mdbias = mags[5]; c.mdh0 = mags[6];
+  }
+  c.accB = acc;
+  c.accC = acc + (size_t)t * per;
+  if (want_m) {
+    c.accMB = acc + 2 * (size_t)t * per;
+    c.accMC = acc + 3 * (size_t)t * per;
+  }
+  c.nb = nb; c.N = N; c.L = L;
+  run_rows_i(bwd_rows, &c, R, t);
+  for (int64_t i = 0; i < per; i++) {
+    double sb = 0.0, sc = 0.0, mb = 0.0, mc = 0.0;
+    for (int k = 0; k < t; k++) {
+      sb += c.accB[(size_t)k * per + i];
+      sc += c.accC[(size_t)k * per + i];
+      if (want_m) {
+        mb += c.accMB[(size_t)k * per + i];
+        mc += c.accMC[(size_t)k * per + i];
+      }
+    }
+    dB[i] = sb;
+    dC[i] = sc;
+    if (want_m) {
+      if (mags[7]) mags[7][i] = mb;
+      if (mags[8]) mags[8][i] = mc;
+    }
+  }
+  free(acc);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* The fused form as a plain fp32 sequential loop: the same loop as above with
  * every quantity held and rounded in fp32, in the order written, with libm's
  * expf and no FMA contraction (ISO C, -std=c11):

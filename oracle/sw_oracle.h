@@ -59,6 +59,19 @@ int swo_selective_scan_ex_f64(const float* x, const float* delta, const float* A
                               double* y_sens, double* h_mag, double* h_sens, int64_t R, int64_t N,
                               int64_t L, int a_mode, int nthreads);
 
+/* Backward of the fused form (see sw_oracle.c).  Per-row outputs dx, ddelta,
+ * dz (R, L), dh0 (R, N), the row's share of dA (R, N), dDskip and dbias (R);
+ * dB, dC (nb, L, N) summed over the rows of each batch.  `mags`, if not NULL,
+ * points to 9 arrays (any may be NULL) receiving the magnitudes of dx, ddelta,
+ * dz, dA, dDskip, dbias, dh0, dB, dC in the same layouts. */
+int swo_selective_scan_bwd_f64(const float* x, const float* delta, const float* A, const float* Bm,
+                               const float* Cm, const int64_t* row_b, const float* Dskip,
+                               const float* z, const float* delta_bias, const float* h0,
+                               int softplus, const float* dy, const float* dh_last, double* dx,
+                               double* ddelta, double* dz, double* dA, double* dD, double* dbias,
+                               double* dh0, double* dB, double* dC, double* const* mags,
+                               int64_t nb, int64_t R, int64_t N, int64_t L, int nthreads);
+
 /* The fused form as a plain fp32 sequential loop (see sw_oracle.c). */
 int swo_selective_scan_f32seq(const float* x, const float* delta, const float* A,
                               const float* Bm, const float* Cm, const int64_t* row_b,
