@@ -180,6 +180,43 @@ int sw_selective_scan_fwd_ex(const void* x, const void* delta, const float* A, c
                              int64_t B, int64_t D, int64_t N, int64_t L, int in_dtype,
                              int out_dtype, int flags);
 
+/*
+ * Backward of sw_selective_scan_fwd_ex: the gradients of
+ *   sum_{b,d,t} dy[b,d,t] y[b,d,t] + sum_{b,d,n} dh_last[b,d,n] h_last[b,d,n]
+ * with respect to every input, by the chain rule through Eq. (3).  The
+ * paper gives the forward only; the adjoint lam = dL/dh is the same affine
+ * recurrence run backwards in time (Eq. (6)-(7) with the order reversed):
+ *   ds_t = dy_t silu(z_t) (dy_t without z),  lam_t = ds_t Cm_t + a_{t+1} lam_{t+1}
+ * and every gradient follows from lam, h and the inputs (see the oracle's
+ * documentation for the full list of formulas).
+ *
+ * Inputs: as for sw_selective_scan_fwd_ex (same dtypes, same flags), plus
+ *   dy      : (B, D, L) of dy_dtype (fp32 or bf16), required
+ *   dh_last : (B, D, N) fp32 or NULL (zero)
+ * Outputs (fp32, overwritten, never accumulated into):
+ *   dx, ddelta : (B, D, L), required; ddelta is with respect to the delta
+ *                passed in (before bias and softplus)
+ *   dA : (D, N), dB, dC : (B, L, N), required (sums over b, resp. over d)
+ *   dDskip, ddelta_bias : (D) or NULL (not written); each is the gradient at
+ *                the given value (at zero when the input is NULL)
+ *   dz : (B, D, L), or NULL; requires z
+ *   dh0 : (B, D, N) or NULL; the gradient with respect to the initial state
+ *                (h0, or the zero state when h0 is NULL)
+ * With L == 0 (or B*D == 0) the sums are zero and dh0 = dh_last.
+ * Results are deterministic: cross-row sums are added in a fixed order.
+ * Supports N <= 16 (SW_ERR_UNSUPPORTED above).  A workspace of about
+ * (B*D*L*8 + B*ceil(D/16)*L*128 + B*D*L*4 if z) bytes is taken from the
+ * device's stream-ordered pool for the call.  Other conventions (and
+ * errors) as for sw_selective_scan_fwd_ex.
+ */
+int sw_selective_scan_bwd(const void* x, const void* delta, const float* A, const void* Bm,
+                          const void* Cm, const float* Dskip, const void* z,
+                          const float* delta_bias, const float* h0, const void* dy,
+                          const float* dh_last, float* dx, float* ddelta, float* dA, float* dB,
+                          float* dC, float* dDskip, float* dz, float* ddelta_bias, float* dh0,
+                          int64_t B, int64_t D, int64_t N, int64_t L, int in_dtype, int dy_dtype,
+                          int flags);
+
 /* Stream used by the calling thread's subsequent calls (a hipStream_t;
  * NULL = the null stream).  Always SW_OK. */
 int sw_set_stream(void* hip_stream);

@@ -430,7 +430,8 @@ int swo_selective_scan_f64(const float* x, const float* delta, const float* A, c
  * magnitude of every output: the same expressions evaluated on absolute
  * values with |h| replaced by the forward magnitude M_t and lam by
  *   Mlam_t = |ds_t C_{t,n}| + |a_{t+1}| Mlam_{t+1},   Mlam_L = |dh_last|,
- * which bounds the sum of the absolute values of the terms of each output.
+ * which bounds the sum of the absolute values of the terms of each output
+ * (silu'(z) = sig + z sig (1 - sig) enters with |sig| + |z sig (1 - sig)|).
  * Per-row outputs: dx, ddelta, dz (R, L); dh0 (R, N); the row's share of dA
  * (R, N), dDskip and dbias (R).  dB and dC (nb, L, N) are summed over the
  * rows of each batch (each thread accumulates its own copy; the copies are
@@ -455,7 +456,7 @@ static void bwd_rows(int64_t r0, int64_t r1, int ti, const void* vctx) {
   double* aMB = c->accMB ? c->accMB + (int64_t)ti * per : NULL;
   double* aMC = c->accMC ? c->accMC + (int64_t)ti * per : NULL;
   /* per-row work arrays */
-  double* dl = (double*)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1) * 7);
+  double* dl = (double*)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1) * 8);
   double* hs = (double*)malloc(sizeof(double) * (size_t)(L + 1) * 2);
   if (!dl || !hs) {
     free(dl);
@@ -468,6 +469,7 @@ static void bwd_rows(int64_t r0, int64_t r1, int ti, const void* vctx) {
   double* ds = dl + 4 * L;
   double* s = dl + 5 * L;  /* pre-gate y */
   double* ms = dl + 6 * L; /* its magnitude */
+  double* mgp = dl + 7 * L; /* |sig| + |z sig (1 - sig)|: the terms of the gate derivative */
   double* mh = hs + (L + 1);
   for (int64_t r = r0; r < r1; r++) {
     const float* x = c->x + r * L;
@@ -490,9 +492,11 @@ static void bwd_rows(int64_t r0, int64_t r1, int ti, const void* vctx) {
         const double sig = 1.0 / (1.0 + exp(-zv));
         g[t] = zv * sig;
         gp[t] = sig * (1.0 + zv * (1.0 - sig));
+        mgp[t] = sig + fabs(zv * sig * (1.0 - sig));
       } else {
         g[t] = 1.0;
         gp[t] = 0.0;
+        mgp[t] = 0.0;
       }
       ds[t] = (double)dyr[t] * g[t];
       s[t] = Dr * (double)x[t];
@@ -554,7 +558,7 @@ static void bwd_rows(int64_t r0, int64_t r1, int ti, const void* vctx) {
       if (c->mddelta) mbias += c->mddelta[r * L + t];
       if (c->dz) {
         c->dz[r * L + t] = (double)dyr[t] * s[t] * gp[t];
-        if (c->mdz) c->mdz[r * L + t] = fabs((double)dyr[t] * gp[t]) * ms[t];
+        if (c->mdz) c->mdz[r * L + t] = fabs((double)dyr[t]) * mgp[t] * ms[t];
       }
     }
     c->dD[r] = dD_sum;

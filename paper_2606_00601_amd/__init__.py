@@ -20,7 +20,7 @@ import torch
 from ._lib import ScanWeaverError, check, last_error, lib, status_string  # noqa: F401
 
 __all__ = ["affine_scan", "affine_scan_i32", "affine_scan_proj", "affine_scan_proj_i32",
-           "selective_scan_fwd", "ScanWeaverError",
+           "selective_scan_fwd", "selective_scan_bwd", "ScanWeaverError",
            "version"]
 
 
@@ -180,3 +180,65 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
                 _ptr(delta_bias), _ptr(h0), _ptr(y), _ptr(h_last), B, D, N, L, in_dt, out_dt,
                 flags), "sw_selective_scan_fwd_ex")
     return y, h_last
+
+
+def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, delta_bias=None,
+                       h0=None, delta_softplus=False, want_dh0=True):
+    """Backward of :func:`selective_scan_fwd`: gradients of sum(dy * y) +
+    sum(dh_last * h_last) with respect to every input.
+
+    Inputs as for the forward; ``dy`` (B, D, L) fp32 or bf16, ``dh_last``
+    (B, D, N) fp32 or None.  Returns a dict of fp32 tensors ``dx, ddelta``
+    (B, D, L), ``dA`` (D, N), ``dB, dC`` (B, L, N), ``dDskip`` and
+    ``ddelta_bias`` (D,) when Dskip / delta_bias are given, ``dz`` (B, D, L)
+    when z is given, and ``dh0`` (B, D, N) when ``want_dh0``.
+    """
+    if not isinstance(x, torch.Tensor) or x.dim() != 3:
+        raise ValueError("x must be a (B, D, L) tensor")
+    dt = x.dtype
+    if dt not in (torch.float32, torch.bfloat16):
+        raise TypeError("x must be float32 or bfloat16")
+    B, D, L = x.shape
+    _need(x, "x", dt)
+    _need(delta, "delta", dt, (B, D, L))
+    _need(A, "A", torch.float32)
+    if A.dim() != 2 or A.shape[0] != D:
+        raise ValueError("A must have shape (D, N)")
+    N = A.shape[1]
+    _need(Bm, "Bm", dt, (B, L, N))
+    _need(Cm, "Cm", dt, (B, L, N))
+    if Dskip is not None:
+        _need(Dskip, "Dskip", torch.float32, (D,))
+    if z is not None:
+        _need(z, "z", dt, (B, D, L))
+    if delta_bias is not None:
+        _need(delta_bias, "delta_bias", torch.float32, (D,))
+    if h0 is not None:
+        _need(h0, "h0", torch.float32, (B, D, N))
+    if not isinstance(dy, torch.Tensor) or dy.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("dy must be a float32 or bfloat16 tensor")
+    _need(dy, "dy", dy.dtype, (B, D, L))
+    if dh_last is not None:
+        _need(dh_last, "dh_last", torch.float32, (B, D, N))
+    dev = x.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = {"dx": torch.empty((B, D, L), **f32), "ddelta": torch.empty((B, D, L), **f32),
+           "dA": torch.empty((D, N), **f32), "dB": torch.empty((B, L, N), **f32),
+           "dC": torch.empty((B, L, N), **f32)}
+    out["dDskip"] = torch.empty((D,), **f32) if Dskip is not None else None
+    out["ddelta_bias"] = torch.empty((D,), **f32) if delta_bias is not None else None
+    out["dz"] = torch.empty((B, D, L), **f32) if z is not None else None
+    out["dh0"] = torch.empty((B, D, N), **f32) if want_dh0 else None
+    from ._lib import SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32
+    in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
+    dy_dt = SW_DTYPE_F32 if dy.dtype == torch.float32 else SW_DTYPE_BF16
+    with torch.cuda.device(dev):
+        _bind_stream(dev)
+        check(lib().sw_selective_scan_bwd(
+            _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
+            _ptr(delta_bias), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(out["dx"]),
+            _ptr(out["ddelta"]), _ptr(out["dA"]), _ptr(out["dB"]), _ptr(out["dC"]),
+            _ptr(out["dDskip"]), _ptr(out["dz"]), _ptr(out["ddelta_bias"]), _ptr(out["dh0"]),
+            B, D, N, L, in_dt, dy_dt, SW_DELTA_SOFTPLUS if delta_softplus else 0),
+            "sw_selective_scan_bwd")
+    return {k: v for k, v in out.items() if v is not None}

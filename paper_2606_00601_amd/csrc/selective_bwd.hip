@@ -1,0 +1,463 @@
+// selective_bwd.hip -- backward of the fused selective scan on gfx950.
+//
+// The gradient of sum_t dy_t y_t (+ sum_n dh_last_n h_last_n) by the chain
+// rule through the forward recurrence h_t = a_t h_{t-1} + u_t (Eq. (3)),
+// a_{t,n} = exp(delta_t A_n), u_{t,n} = delta_t B_{t,n} x_t,
+// y_t = (sum_n C_{t,n} h_{t,n} + Dskip x_t) g_t, g_t = silu(z_t) or 1.
+// The adjoint lam_t = dL/dh_t obeys the same kind of recurrence run
+// backwards in time, lam_t = ds_t C_t + a_{t+1} lam_{t+1} (ds_t = dy_t g_t),
+// the affine pair of Eq. (6) with the order of Eq. (7) reversed.  With
+// q_t = a_t h_{t-1}:
+//   ddelta_t = sum_n lam (q A_n + B x_t)        dx_t = delta_t sum_n lam B + ds_t Dskip
+//   dA_n    += lam q delta_t                    dB_{t,n} += lam delta_t x_t   (over d)
+//   dC_{t,n} += ds_t h_t                        (over d)
+//   dh0 = a_0 lam_0,  dDskip += ds x,  dz = dy s silu'(z) with s the pre-gate y.
+//
+// One workgroup (4 wavefronts) owns 16 (b,d) rows of one batch; lane n of a
+// 16-lane row owns state n (N <= 16; states past N are identity steps).
+//   1. A forward sweep over the sequence stores the state at the start of
+//      every 8-step tile (a checkpoint per lane per tile, in a workspace).
+//   2. A reverse sweep over the tiles: the tile's delta, delta*x, ds and
+//      B, C are staged in LDS; every lane reloads its checkpoint, recomputes
+//      the tile's a_t and q_t forward into registers, then walks the tile
+//      backwards carrying lam.  Per step it writes four partial products to
+//      LDS: lam q A and lam B (summed over n, per row and step, into ddelta
+//      and dx) and lam delta x and ds h (summed over the 16 rows, per step and
+//      state, into this workgroup's share of dB and dC).
+//   3. Half of the workgroup sums the first pair per (row, step), the other
+//      half the second pair per (step, state); the shares of dB / dC, dA,
+//      dDskip and ddelta_bias go to a workspace, and a second kernel adds the
+//      shares in a fixed order (no atomics: the result is reproducible).
+// The pre-gate output s needed by dz comes from the forward kernel run
+// without the gate.
+#include "selective_common.h"
+
+namespace sw {
+namespace {
+
+constexpr int BW_N = 16;                 // state lanes per row
+constexpr int BW_T = 8;                  // steps per tile
+constexpr int BW_TS = 12;                // LDS stride of one [t] run (16-byte aligned)
+constexpr int BW_ROWS = 16;              // (b,d) rows per workgroup
+constexpr int BW_RS = BW_N * BW_TS + 8;  // stride of one row's [n][t] block (8 mod 64 banks)
+constexpr float BW_LOG2E = 1.4426950408889634f;
+
+struct BwSmem {
+  float rv[3][BW_ROWS][BW_TS];   // per row and step: delta, delta*x, ds
+  float bc[2][BW_N][BW_TS];      // B, C of the tile as [n][t]
+  float sp[2][BW_ROWS * BW_RS];  // per row [n][t]: lam q A, lam B      (sum over n)
+  float pb[2][BW_ROWS * BW_RS];  // per row [n][t]: lam delta x, ds h   (sum over rows)
+};
+
+template <typename T>
+__device__ __forceinline__ float ldf(const T* __restrict__ p, int64_t i);
+template <>
+__device__ __forceinline__ float ldf<float>(const float* __restrict__ p, int64_t i) {
+  return p[i];
+}
+template <>
+__device__ __forceinline__ float ldf<uint16_t>(const uint16_t* __restrict__ p, int64_t i) {
+  return bf16_one(p[i]);
+}
+
+__device__ __forceinline__ float sigmoid_f32(float v) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-v * BW_LOG2E));
+}
+
+__device__ __forceinline__ void bw_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+struct BwWork {
+  float* ck;       // (B*D, ntile, 16) states at tile starts
+  const float* s;  // (B*D, L) pre-gate output (gated calls)
+  float* dA_p;     // (B*D, 16)
+  float* dD_p;     // (B*D)
+  float* db_p;     // (B*D)
+  float* dB_p;     // (B, G, L, 16)
+  float* dC_p;     // (B, G, L, 16)
+};
+
+// Raw per-(row, step) inputs of one tile, held by the staging thread.
+struct RowStep {
+  float x, dl, dy, z, s;
+  bool live;  // a step of a real row inside the sequence
+};
+
+template <typename IN, bool GATED>
+__global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, const BwWork w,
+                                                            int64_t G, int64_t ntile) {
+  __shared__ __align__(16) BwSmem sm;
+  const IN* __restrict__ X = static_cast<const IN*>(a.x);
+  const IN* __restrict__ DL = static_cast<const IN*>(a.delta);
+  const IN* __restrict__ BM = static_cast<const IN*>(a.Bm);
+  const IN* __restrict__ CM = static_cast<const IN*>(a.Cm);
+  const IN* __restrict__ Z = static_cast<const IN*>(a.z);
+  const int64_t D = a.D, L = a.L, N = a.N;
+
+  const int tid = threadIdx.x;
+  const int wv = tid / 64, lane = tid % 64;
+  const int rr = 4 * wv + lane / 16;  // compute role: row within the workgroup
+  const int n = lane % 16;            // ... and state
+  const int64_t b = blockIdx.x / G;
+  const int64_t g = blockIdx.x - b * G;
+  const int64_t d0 = g * BW_ROWS;
+  const int64_t d = d0 + rr;
+  const bool dok = d < D;
+  const bool nok = n < N;
+  const int64_t row = b * D + (dok ? d : D - 1);
+
+  // staging / reduce roles: threads 0..127 own (row sr, step st); threads
+  // 128..255 own (step bt, state bn)
+  const bool role_a = tid < 128;
+  const int sr = tid / BW_T, st = tid % BW_T;
+  const int bt = (tid - 128) / BW_N, bn = (tid - 128) % BW_N;
+  const int64_t sd = d0 + sr;
+  const bool sdok = role_a && sd < D;
+  const int64_t srow = b * D + (sd < D ? sd : D - 1);
+
+  const float Ar = nok ? a.A[(dok ? d : D - 1) * N + n] : 0.0f;
+  const float Al = Ar * BW_LOG2E;
+  const float dbias = (a.delta_bias && role_a) ? a.delta_bias[sd < D ? sd : D - 1] : 0.0f;
+  const float Dsk = (a.Dskip && role_a) ? a.Dskip[sd < D ? sd : D - 1] : 0.0f;
+
+  // --- staging helpers -----------------------------------------------------
+  auto load_rowstep = [&](int64_t k, RowStep& v) {
+    const int64_t t = k * BW_T + st;
+    const bool ok = sdok && t < L;
+    v.live = ok;
+    const int64_t i = srow * L + (ok ? t : 0);
+    v.x = ok ? ldf<IN>(X, i) : 0.0f;
+    v.dl = ok ? ldf<IN>(DL, i) : 0.0f;
+    if (a.dy_bf16)
+      v.dy = ok ? bf16_one(static_cast<const uint16_t*>(a.dy)[i]) : 0.0f;
+    else
+      v.dy = ok ? static_cast<const float*>(a.dy)[i] : 0.0f;
+    if constexpr (GATED) {
+      v.z = ok ? ldf<IN>(Z, i) : 0.0f;
+      v.s = ok ? w.s[i] : 0.0f;
+    }
+  };
+  // delta after bias and softplus, and d delta / d raw (1 without softplus)
+  auto widen_delta = [&](float raw, bool live, float& dlv, float& sg) {
+    float v = raw + dbias;
+    sg = 1.0f;
+    if (a.softplus) {
+      sg = sigmoid_f32(v);
+      v = softplus_f32(v);
+    }
+    dlv = live ? v : 0.0f;
+  };
+  auto load_bc = [&](int64_t k, float& bv, float& cv) {
+    const int64_t t = k * BW_T + bt;
+    const bool ok = !role_a && t < L && bn < N;
+    const int64_t i = (b * L + (ok ? t : 0)) * N + (ok ? bn : 0);
+    bv = ok ? ldf<IN>(BM, i) : 0.0f;
+    cv = ok ? ldf<IN>(CM, i) : 0.0f;
+  };
+
+  // --- 1. forward sweep: checkpoints ---------------------------------------
+  float h = (a.h0 && dok && nok) ? a.h0[row * N + n] : 0.0f;
+  {
+    RowStep nx;
+    float nb_ = 0.f, nc_ = 0.f;
+    if (role_a) load_rowstep(0, nx);
+    else load_bc(0, nb_, nc_);
+    for (int64_t k = 0; k < ntile; ++k) {
+      if (role_a) {
+        float dlv, sg;
+        widen_delta(nx.dl, nx.live, dlv, sg);
+        sm.rv[0][sr][st] = dlv;
+        sm.rv[1][sr][st] = dlv * nx.x;
+        if (k + 1 < ntile) load_rowstep(k + 1, nx);
+      } else {
+        sm.bc[0][bn][bt] = nb_;
+        if (k + 1 < ntile) load_bc(k + 1, nb_, nc_);
+      }
+      bw_barrier();
+      if (dok) w.ck[(row * ntile + k) * BW_N + n] = h;
+#pragma unroll
+      for (int q = 0; q < BW_T; q += 4) {
+        const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[0][rr][q]);
+        const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[1][rr][q]);
+        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[0][n][q]);
+        const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
+        const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
+        const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          h = __builtin_fmaf(__builtin_amdgcn_exp2f(dlq[j] * Al), h, dxq[j] * bq[j]);
+      }
+      bw_barrier();
+    }
+  }
+
+  // --- 2./3. reverse sweep ---------------------------------------------------
+  float lam = (a.dh_last && dok && nok) ? a.dh_last[row * N + n] : 0.0f;
+  float dA_acc = 0.0f;
+  float dD_acc = 0.0f, db_acc = 0.0f;  // role a: this thread's (row, step slot)
+  RowStep cur;
+  float cb = 0.f, cc = 0.f;
+  if (role_a) load_rowstep(ntile - 1, cur);
+  else load_bc(ntile - 1, cb, cc);
+  for (int64_t k = ntile - 1; k >= 0; --k) {
+    // stage tile k
+    float dlv = 0.f, sg = 1.f, ds = 0.f, gp = 0.f;
+    const bool live = role_a && cur.live;
+    if (role_a) {
+      widen_delta(cur.dl, live, dlv, sg);
+      float gt = 1.0f;
+      if constexpr (GATED) {
+        const float sz = sigmoid_f32(cur.z);
+        gt = cur.z * sz;
+        gp = sz * (1.0f + cur.z * (1.0f - sz));
+      }
+      ds = cur.dy * gt;
+      sm.rv[0][sr][st] = dlv;
+      sm.rv[1][sr][st] = dlv * cur.x;
+      sm.rv[2][sr][st] = ds;
+    } else {
+      sm.bc[0][bn][bt] = cb;
+      sm.bc[1][bn][bt] = cc;
+    }
+    const RowStep mine = cur;
+    if (k > 0) {
+      if (role_a) load_rowstep(k - 1, cur);
+      else load_bc(k - 1, cb, cc);
+    }
+    const float hck = dok ? w.ck[(row * ntile + k) * BW_N + n] : 0.0f;
+    bw_barrier();
+
+    // recompute a_t and q_t = a_t h_{t-1} of the tile
+    float av[BW_T], qv[BW_T];
+    {
+      float hh = hck;
+#pragma unroll
+      for (int q = 0; q < BW_T; q += 4) {
+        const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[0][rr][q]);
+        const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[1][rr][q]);
+        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[0][n][q]);
+        const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
+        const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
+        const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          av[q + j] = __builtin_amdgcn_exp2f(dlq[j] * Al);
+          qv[q + j] = av[q + j] * hh;
+          hh = __builtin_fmaf(dxq[j], bq[j], qv[q + j]);
+        }
+      }
+    }
+    // walk the tile backwards
+    float* const sp0 = &sm.sp[0][rr * BW_RS + n * BW_TS];
+    float* const sp1 = &sm.sp[1][rr * BW_RS + n * BW_TS];
+    float* const pb0 = &sm.pb[0][rr * BW_RS + n * BW_TS];
+    float* const pb1 = &sm.pb[1][rr * BW_RS + n * BW_TS];
+#pragma unroll
+    for (int q = BW_T - 4; q >= 0; q -= 4) {
+      const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[0][rr][q]);
+      const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[1][rr][q]);
+      const float4 ds4 = *reinterpret_cast<const float4*>(&sm.rv[2][rr][q]);
+      const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[0][n][q]);
+      const float4 c4 = *reinterpret_cast<const float4*>(&sm.bc[1][n][q]);
+      const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
+      const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
+      const float dsq[4] = {ds4.x, ds4.y, ds4.z, ds4.w};
+      const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
+      const float cq[4] = {c4.x, c4.y, c4.z, c4.w};
+      float o0[4], o1[4], o2[4], o3[4];
+#pragma unroll
+      for (int j = 3; j >= 0; --j) {
+        const float l = __builtin_fmaf(dsq[j], cq[j], lam);
+        const float hc = __builtin_fmaf(dxq[j], bq[j], qv[q + j]);
+        const float p = l * qv[q + j];
+        dA_acc = __builtin_fmaf(p, dlq[j], dA_acc);
+        o0[j] = p * Ar;
+        o1[j] = l * bq[j];
+        o2[j] = l * dxq[j];
+        o3[j] = dsq[j] * hc;
+        lam = av[q + j] * l;
+      }
+      *reinterpret_cast<float4*>(sp0 + q) = make_float4(o0[0], o0[1], o0[2], o0[3]);
+      *reinterpret_cast<float4*>(sp1 + q) = make_float4(o1[0], o1[1], o1[2], o1[3]);
+      *reinterpret_cast<float4*>(pb0 + q) = make_float4(o2[0], o2[1], o2[2], o2[3]);
+      *reinterpret_cast<float4*>(pb1 + q) = make_float4(o3[0], o3[1], o3[2], o3[3]);
+    }
+    bw_barrier();
+
+    if (role_a) {
+      // sum over states: ddelta and dx of (row sr, step st)
+      float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int m = 0; m < BW_N; ++m) {
+        s1 += sm.sp[0][sr * BW_RS + m * BW_TS + st];
+        s2 += sm.sp[1][sr * BW_RS + m * BW_TS + st];
+      }
+      const int64_t t = k * BW_T + st;
+      if (live) {
+        const float ddl = (s1 + mine.x * s2) * sg;
+        const int64_t i = srow * L + t;
+        a.ddelta[i] = ddl;
+        a.dx[i] = __builtin_fmaf(dlv, s2, ds * Dsk);
+        if constexpr (GATED) a.dz[i] = mine.dy * mine.s * gp;
+        dD_acc = __builtin_fmaf(ds, mine.x, dD_acc);
+        db_acc += ddl;
+      }
+    } else {
+      // sum over the 16 rows: this workgroup's share of dB and dC at (step bt, state bn)
+      float sb = 0.f, sc = 0.f;
+#pragma unroll
+      for (int m = 0; m < BW_ROWS; ++m) {
+        sb += sm.pb[0][m * BW_RS + bn * BW_TS + bt];
+        sc += sm.pb[1][m * BW_RS + bn * BW_TS + bt];
+      }
+      const int64_t t = k * BW_T + bt;
+      if (t < L) {
+        const int64_t i = ((b * G + g) * L + t) * BW_N + bn;
+        w.dB_p[i] = sb;
+        w.dC_p[i] = sc;
+      }
+    }
+    bw_barrier();
+  }
+
+  if (dok && nok) {
+    if (a.dh0) a.dh0[row * N + n] = lam;
+    w.dA_p[row * BW_N + n] = dA_acc;
+  }
+  // per-row sums of the step slots (8 consecutive lanes of role a)
+  if (role_a) {
+#pragma unroll
+    for (int off = 1; off < BW_T; off *= 2) {
+      dD_acc += __shfl_xor(dD_acc, off);
+      db_acc += __shfl_xor(db_acc, off);
+    }
+    if (st == 0 && sdok) {
+      w.dD_p[srow] = dD_acc;
+      w.db_p[srow] = db_acc;
+    }
+  }
+}
+
+// Adds the shares in a fixed order: dB, dC over the workgroups of a batch;
+// dA, dDskip, ddelta_bias over the batch.
+__global__ __launch_bounds__(256) void selective_bwd_reduce_kernel(const BwdArgs a,
+                                                                   const BwWork w, int64_t G) {
+  const int64_t B = a.B, D = a.D, N = a.N, L = a.L;
+  const int64_t nbc = B * L * N;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nbc; i += stride) {
+    const int64_t nn = i % N, bt = i / N;  // bt = b*L + t
+    const int64_t b = bt / L, t = bt - b * L;
+    float sb = 0.f, sc = 0.f;
+    for (int64_t g = 0; g < G; ++g) {
+      const int64_t j = ((b * G + g) * L + t) * BW_N + nn;
+      sb += w.dB_p[j];
+      sc += w.dC_p[j];
+    }
+    a.dB[i] = sb;
+    a.dC[i] = sc;
+  }
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < D * N; i += stride) {
+    const int64_t d = i / N, nn = i - d * N;
+    float s = 0.f;
+    for (int64_t b = 0; b < B; ++b) s += w.dA_p[(b * D + d) * BW_N + nn];
+    a.dA[i] = s;
+  }
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < D; i += stride) {
+    float sd = 0.f, sbias = 0.f;
+    for (int64_t b = 0; b < B; ++b) {
+      sd += w.dD_p[b * D + i];
+      sbias += w.db_p[b * D + i];
+    }
+    if (a.dDskip) a.dDskip[i] = sd;
+    if (a.ddelta_bias) a.ddelta_bias[i] = sbias;
+  }
+}
+
+}  // namespace
+
+int selective_bwd(const BwdArgs& a) {
+  if (a.N > BW_N)
+    return fail(SW_ERR_UNSUPPORTED, "the backward pass supports N <= %d (got %lld)", BW_N,
+                (long long)a.N);
+  hipStream_t s = current_stream();
+  const int64_t B = a.B, D = a.D, L = a.L;
+  const int64_t G = (D + BW_ROWS - 1) / BW_ROWS;
+  const int64_t ntile = (L + BW_T - 1) / BW_T;
+  const int64_t grid = B * G;
+  if (grid >= ((int64_t)1 << 31))
+    return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
+  const size_t R = (size_t)(B * D);
+  const size_t n_ck = R * (size_t)ntile * BW_N, n_s = a.z ? R * (size_t)L : 0;
+  const size_t n_dA = R * BW_N, n_bc = (size_t)(B * G) * (size_t)L * BW_N;
+  const size_t total = n_ck + n_s + n_dA + 2 * R + 2 * n_bc;
+  void* base = nullptr;
+  int st = workspace_alloc(&base, total * sizeof(float), s);
+  if (st != SW_OK) return st;
+  float* f = static_cast<float*>(base);
+  BwWork w;
+  w.ck = f;
+  f += n_ck;
+  float* s_pre = a.z ? f : nullptr;
+  w.s = s_pre;
+  f += n_s;
+  w.dA_p = f;
+  f += n_dA;
+  w.dD_p = f;
+  f += R;
+  w.db_p = f;
+  f += R;
+  w.dB_p = f;
+  f += n_bc;
+  w.dC_p = f;
+  if (a.z) {
+    // the pre-gate output: the forward pass without the gate
+    SelArgs fa{};
+    fa.x = a.x;
+    fa.delta = a.delta;
+    fa.Bm = a.Bm;
+    fa.Cm = a.Cm;
+    fa.A = a.A;
+    fa.Dskip = a.Dskip;
+    fa.delta_bias = a.delta_bias;
+    fa.h0 = a.h0;
+    fa.y = s_pre;
+    fa.B = B;
+    fa.D = D;
+    fa.N = a.N;
+    fa.L = L;
+    fa.bf16_in = a.bf16_in;
+    fa.softplus = a.softplus;
+    fa.vec = a.vec;
+    st = selective_fwd(fa);
+    if (st != SW_OK) {
+      workspace_free(base, s);
+      return st;
+    }
+  }
+  if (a.bf16_in) {
+    auto kern = a.z ? selective_bwd_kernel<uint16_t, true> : selective_bwd_kernel<uint16_t, false>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile);
+  } else {
+    auto kern = a.z ? selective_bwd_kernel<float, true> : selective_bwd_kernel<float, false>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile);
+  }
+  st = check_launch("selective_bwd_kernel");
+  if (st == SW_OK) {
+    int64_t work = B * L * a.N;
+    if (work < D * a.N) work = D * a.N;
+    int64_t blocks = (work + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(selective_bwd_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, w,
+                       G);
+    st = check_launch("selective_bwd_reduce_kernel");
+  }
+  workspace_free(base, s);
+  return st;
+}
+
+}  // namespace sw

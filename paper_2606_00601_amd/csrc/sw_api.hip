@@ -223,6 +223,79 @@ int selective_common(SelArgs a) {
   return selective_fwd(a);
 }
 
+// Validation of the backward entry point; see include/scanweaver.h.
+int selective_bwd_common(BwdArgs a) {
+  const int64_t B = a.B, D = a.D, N = a.N, L = a.L;
+  if (B < 0 || D < 0 || L < 0 || N < 0)
+    return fail(SW_ERR_INVALID_ARG, "negative size (B=%lld D=%lld N=%lld L=%lld)",
+                (long long)B, (long long)D, (long long)N, (long long)L);
+  if (N < 1 || N > 64) return fail(SW_ERR_UNSUPPORTED, "N=%lld outside [1, 64]", (long long)N);
+  int64_t R, nx, nbc, nh, nan, tmp;
+  if (!mul_ok(B, D, &R) || !mul_ok(R, L, &nx) || !mul_ok(nx, 4, &tmp) || !mul_ok(B, L, &nbc) ||
+      !mul_ok(nbc, N, &nbc) || !mul_ok(nbc, 4, &tmp) || !mul_ok(R, N, &nh) ||
+      !mul_ok(D, N, &nan) || !mul_ok(R, 16 * ((L + 7) / 8 + 1), &tmp) || !mul_ok(tmp, 8, &tmp))
+    return fail(SW_ERR_UNSUPPORTED, "sizes overflow");
+  if (a.dz && !a.z) return fail(SW_ERR_INVALID_ARG, "dz requires z");
+  if (N > 16)
+    return fail(SW_ERR_UNSUPPORTED, "the backward pass supports N <= 16 (got %lld)", (long long)N);
+  int dev, st;
+  if ((st = current_device(&dev)) != SW_OK) return st;
+  const size_t es = a.bf16_in ? 2 : 4, dys = a.dy_bf16 ? 2 : 4;
+  const bool empty = R == 0 || L == 0;
+  // inputs
+  if ((st = check_ptr(a.x, es, "x", !empty, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.delta, es, "delta", !empty, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.A, 4, "A", !empty, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.Bm, es, "Bm", !empty, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.Cm, es, "Cm", !empty, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.Dskip, 4, "Dskip", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.z, es, "z", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.delta_bias, 4, "delta_bias", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.h0, 4, "h0", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.dy, dys, "dy", !empty, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.dh_last, 4, "dh_last", false, dev)) != SW_OK) return st;
+  // outputs
+  if ((st = check_ptr(a.dx, 4, "dx", nx > 0, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.ddelta, 4, "ddelta", nx > 0, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.dA, 4, "dA", nan > 0, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.dB, 4, "dB", nbc > 0, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.dC, 4, "dC", nbc > 0, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.dDskip, 4, "dDskip", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.dz, 4, "dz", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.ddelta_bias, 4, "ddelta_bias", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.dh0, 4, "dh0", false, dev)) != SW_OK) return st;
+  Span outs[] = {{a.dx, (size_t)nx * 4, "dx"},         {a.ddelta, (size_t)nx * 4, "ddelta"},
+                 {a.dA, (size_t)nan * 4, "dA"},        {a.dB, (size_t)nbc * 4, "dB"},
+                 {a.dC, (size_t)nbc * 4, "dC"},        {a.dDskip, (size_t)D * 4, "dDskip"},
+                 {a.dz, (size_t)nx * 4, "dz"},         {a.ddelta_bias, (size_t)D * 4, "ddelta_bias"},
+                 {a.dh0, (size_t)nh * 4, "dh0"}};
+  Span ins[] = {{a.x, (size_t)nx * es, "x"},           {a.delta, (size_t)nx * es, "delta"},
+                {a.A, (size_t)nan * 4, "A"},            {a.Bm, (size_t)nbc * es, "Bm"},
+                {a.Cm, (size_t)nbc * es, "Cm"},         {a.Dskip, (size_t)D * 4, "Dskip"},
+                {a.z, (size_t)nx * es, "z"},            {a.delta_bias, (size_t)D * 4, "delta_bias"},
+                {a.h0, (size_t)nh * 4, "h0"},           {a.dy, (size_t)nx * dys, "dy"},
+                {a.dh_last, (size_t)nh * 4, "dh_last"}};
+  if ((st = check_spans(outs, 9, ins, 11)) != SW_OK) return st;
+  hipStream_t s = current_stream();
+  if (empty) {
+    // no step: every sum is empty, and the initial state's gradient is dh_last
+    uint32_t* zs[] = {reinterpret_cast<uint32_t*>(a.dA), reinterpret_cast<uint32_t*>(a.dB),
+                      reinterpret_cast<uint32_t*>(a.dC), reinterpret_cast<uint32_t*>(a.dDskip),
+                      reinterpret_cast<uint32_t*>(a.ddelta_bias)};
+    const size_t nw[] = {(size_t)nan, (size_t)nbc, (size_t)nbc, (size_t)D, (size_t)D};
+    for (int i = 0; i < 5; ++i)
+      if (zs[i] && (st = zero_words(zs[i], nw[i], s)) != SW_OK) return st;
+    if (a.dh0 && nh > 0) {
+      if (!a.dh_last) return zero_words(reinterpret_cast<uint32_t*>(a.dh0), (size_t)nh, s);
+      hipError_t e = hipMemcpyAsync(a.dh0, a.dh_last, (size_t)nh * 4, hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return fail(SW_ERR_HIP, "dh0 copy: %s", hipGetErrorString(e));
+    }
+    return SW_OK;
+  }
+  a.vec = L % 4 == 0 && all_aligned16({a.x, a.delta});
+  return selective_bwd(a);
+}
+
 SelArgs sel_args(const void* x, const void* delta, const float* A, const void* Bm, const void* Cm,
                  const float* Dskip, void* y, float* h_last, int64_t B, int64_t D, int64_t N,
                  int64_t L, bool bf16_in) {
@@ -337,6 +410,28 @@ int ScratchSession::reserve(size_t carry_words, uint32_t tickets, hipStream_t s)
   return SW_OK;
 }
 
+int workspace_alloc(void** p, size_t bytes, hipStream_t s) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SW_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  {
+    std::lock_guard<std::mutex> g(scratch_mu);
+    keep_pool_memory(dev);
+  }
+  *p = nullptr;
+  e = hipMallocAsync(p, bytes < 256 ? 256 : bytes, s);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(SW_ERR_ALLOC, "hipMallocAsync(%zu bytes): %s", bytes, hipGetErrorString(e));
+  }
+  return SW_OK;
+}
+
+void workspace_free(void* p, hipStream_t s) {
+  if (p) (void)hipFreeAsync(p, s);
+}
+
 int zero_words(uint32_t* p, size_t words, hipStream_t s) {
   if (words == 0) return SW_OK;
   size_t blocks = (words + 255) / 256;
@@ -379,6 +474,49 @@ SW_API int sw_affine_scan_proj_i32(const int32_t* a, const int32_t* b, const int
                                           reinterpret_cast<uint32_t*>(y),
                                           reinterpret_cast<uint32_t*>(h_last), B, D, L,
                                           sw::affine_scan_io_u32);
+}
+
+SW_API int sw_selective_scan_bwd(const void* x, const void* delta, const float* A,
+                                 const void* Bm, const void* Cm, const float* Dskip,
+                                 const void* z, const float* delta_bias, const float* h0,
+                                 const void* dy, const float* dh_last, float* dx, float* ddelta,
+                                 float* dA, float* dB, float* dC, float* dDskip, float* dz,
+                                 float* ddelta_bias, float* dh0, int64_t B, int64_t D, int64_t N,
+                                 int64_t L, int in_dtype, int dy_dtype, int flags) {
+  if ((in_dtype != SW_DTYPE_F32 && in_dtype != SW_DTYPE_BF16) ||
+      (dy_dtype != SW_DTYPE_F32 && dy_dtype != SW_DTYPE_BF16))
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown dtype (in %d, dy %d)", in_dtype, dy_dtype);
+  if (flags & ~(int)SW_DELTA_SOFTPLUS)
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown flags 0x%x", (unsigned)flags);
+  sw::BwdArgs a{};
+  a.x = x;
+  a.delta = delta;
+  a.Bm = Bm;
+  a.Cm = Cm;
+  a.z = z;
+  a.dy = dy;
+  a.A = A;
+  a.Dskip = Dskip;
+  a.delta_bias = delta_bias;
+  a.h0 = h0;
+  a.dh_last = dh_last;
+  a.dx = dx;
+  a.ddelta = ddelta;
+  a.dA = dA;
+  a.dB = dB;
+  a.dC = dC;
+  a.dDskip = dDskip;
+  a.dz = dz;
+  a.ddelta_bias = ddelta_bias;
+  a.dh0 = dh0;
+  a.B = B;
+  a.D = D;
+  a.N = N;
+  a.L = L;
+  a.bf16_in = in_dtype == SW_DTYPE_BF16;
+  a.dy_bf16 = dy_dtype == SW_DTYPE_BF16;
+  a.softplus = (flags & SW_DELTA_SOFTPLUS) != 0;
+  return sw::selective_bwd_common(a);
 }
 
 SW_API int sw_selective_scan_fwd(const float* x, const float* delta, const float* A,

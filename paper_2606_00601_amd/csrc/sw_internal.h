@@ -66,6 +66,25 @@ struct SelArgs {
 };
 int selective_fwd(const SelArgs& a);
 
+// Arguments of one backward call of the fused form, already validated.
+// x, delta, Bm, Cm, z are fp32 or bf16 as `bf16_in` says, dy as `dy_bf16`
+// says; gradients are fp32.  Optional inputs (NULL: absent): Dskip, z,
+// delta_bias, h0, dh_last; optional outputs: dDskip (with Dskip), dz (with z),
+// ddelta_bias (with delta_bias), dh0.
+struct BwdArgs {
+  const void *x, *delta, *Bm, *Cm, *z, *dy;
+  const float *A, *Dskip, *delta_bias, *h0, *dh_last;
+  float *dx, *ddelta, *dA, *dB, *dC, *dDskip, *dz, *ddelta_bias, *dh0;
+  int64_t B, D, N, L;
+  bool bf16_in, dy_bf16, softplus, vec;  // vec: x and delta allow the forward's vector path
+};
+int selective_bwd(const BwdArgs& a);
+
+// Stream-ordered workspace (hipMallocAsync / hipFreeAsync on `s`; freed
+// blocks stay in the device's pool).
+int workspace_alloc(void** p, size_t bytes, hipStream_t s);
+void workspace_free(void* p, hipStream_t s);
+
 // Flags of the fused kernels (runtime, wave-uniform).
 enum : uint32_t { SEL_SOFTPLUS = 1u, SEL_Y_BF16 = 2u, SEL_GATED = 4u };
 

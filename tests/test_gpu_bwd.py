@@ -1,0 +1,189 @@
+"""GPU parity of the fused selective scan's backward pass (through the C ABI)
+against the fp64 backward oracle.
+
+Gate: every gradient element within 1e-4 of its magnitude (the oracle's sum
+of the absolute values of the terms that make it up), the same rule as the
+forward.  Cross-row sums (dA, dB, dC, dDskip, ddelta_bias) are added in a
+fixed order, so repeated calls agree bit for bit.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from gate import assert_gate, fp_gate
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def sw():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_00601_amd as pkg
+    pkg.lib()
+    return pkg
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def _bf16_dev(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to("cuda").view(
+        torch.bfloat16)
+
+
+def _inputs(B, D, N, L, seed, dtype, opts):
+    inp = wl.selective_inputs(B, D, N, L, seed, dtype)
+    rng = np.random.Generator(np.random.PCG64(seed + 5))
+    ex = {"dy": rng.standard_normal((B, D, L)).astype(np.float32)}
+    if "dybf16" in opts:
+        ex["dy_bits"] = wl.bf16_round(ex["dy"])
+        ex["dy"] = wl.bf16_widen(ex["dy_bits"])
+    if "z" in opts:
+        z = (rng.standard_normal((B, D, L)) * 2).astype(np.float32)
+        if dtype == "bf16":
+            ex["z_bits"] = wl.bf16_round(z)
+            z = wl.bf16_widen(ex["z_bits"])
+        ex["z"] = z
+    if "bias" in opts:
+        ex["delta_bias"] = rng.uniform(-2.0, 0.0, size=D).astype(np.float32)
+    if "h0" in opts:
+        ex["h0"] = rng.standard_normal((B, D, N)).astype(np.float32)
+    if "dhl" in opts:
+        ex["dh_last"] = rng.standard_normal((B, D, N)).astype(np.float32)
+    return inp, ex
+
+
+def _run(sw, inp, ex, dtype, opts, with_dskip=True):
+    if dtype == "bf16":
+        x, dl = _bf16_dev(inp["x_bf16"]), _bf16_dev(inp["delta_bf16"])
+        Bm, Cm = _bf16_dev(inp["Bm_bf16"]), _bf16_dev(inp["Cm_bf16"])
+        z = _bf16_dev(ex["z_bits"]) if "z" in ex else None
+    else:
+        x, dl, Bm, Cm = (_dev(inp[k]) for k in ("x", "delta", "Bm", "Cm"))
+        z = _dev(ex["z"]) if "z" in ex else None
+    dy = _bf16_dev(ex["dy_bits"]) if "dy_bits" in ex else _dev(ex["dy"])
+    g = sw.selective_scan_bwd(
+        x, dl, _dev(inp["A"]), Bm, Cm, _dev(inp["Dskip"]) if with_dskip else None, dy,
+        _dev(ex["dh_last"]) if "dh_last" in ex else None, z=z,
+        delta_bias=_dev(ex["delta_bias"]) if "delta_bias" in ex else None,
+        h0=_dev(ex["h0"]) if "h0" in ex else None, delta_softplus="softplus" in opts)
+    torch.cuda.synchronize()
+    return g
+
+
+def _ref(inp, ex, opts, rows=None, with_dskip=True):
+    return oracle.selective_scan_bwd(
+        inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+        inp["Dskip"] if with_dskip else None, ex["dy"], ex.get("dh_last"), z=ex.get("z"),
+        delta_bias=ex.get("delta_bias"), h0=ex.get("h0"), delta_softplus="softplus" in opts,
+        rows=rows, bounds=True)
+
+
+def _check_all(g, o, what, keys):
+    for k in keys:
+        st = fp_gate(g[k].cpu().numpy(), o[k], o["m_" + k])
+        assert_gate(st, f"{what} {k}")
+
+
+# (B, D, N, L): D not a multiple of 16, ragged L, N below 16
+_SHAPES = [(2, 37, 16, 203), (1, 16, 16, 64), (3, 5, 5, 17), (1, 20, 1, 9), (2, 33, 8, 1000)]
+_OPTS = [(), ("z",), ("bias", "softplus"), ("h0", "dhl"), ("dybf16",),
+         ("z", "bias", "softplus", "h0", "dhl")]
+
+
+@pytest.mark.parametrize("shape", _SHAPES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("opts", _OPTS)
+def test_bwd_matches_oracle(sw, shape, dtype, opts):
+    B, D, N, L = shape
+    _say("case bwd", dtype, shape, opts)
+    inp, ex = _inputs(B, D, N, L, 800 + B + D + N + L, dtype, opts)
+    g = _run(sw, inp, ex, dtype, opts)
+    o = _ref(inp, ex, opts)
+    keys = ["dx", "ddelta", "dA", "dB", "dC", "dDskip", "dh0"]
+    if "z" in opts:
+        keys.append("dz")
+    if "bias" in opts:
+        keys.append("ddelta_bias")
+    _check_all(g, o, f"{dtype} {shape} {opts}", keys)
+
+
+def test_bwd_without_dskip_and_dh0(sw):
+    inp, ex = _inputs(2, 19, 16, 77, 901, "f32", ())
+    g = _run(sw, inp, ex, "f32", (), with_dskip=False)
+    assert "dDskip" not in g
+    o = _ref(inp, ex, (), with_dskip=False)
+    _check_all(g, o, "no Dskip", ["dx", "ddelta", "dA", "dB", "dC", "dh0"])
+
+
+def test_bwd_is_deterministic(sw):
+    inp, ex = _inputs(2, 70, 16, 300, 902, "bf16", ("z", "bias", "softplus"))
+    g1 = _run(sw, inp, ex, "bf16", ("z", "bias", "softplus"))
+    g2 = _run(sw, inp, ex, "bf16", ("z", "bias", "softplus"))
+    for k in g1:
+        assert torch.equal(g1[k], g2[k]), k
+
+
+def test_bwd_empty_sequence(sw):
+    B, D, N = 2, 3, 16
+    e = torch.empty((B, D, 0), device="cuda")
+    A = torch.randn((D, N), device="cuda")
+    Bm = torch.empty((B, 0, N), device="cuda")
+    dhl = torch.randn((B, D, N), device="cuda")
+    g = sw.selective_scan_bwd(e, e, A, Bm, Bm, torch.randn(D, device="cuda"), e, dhl)
+    torch.cuda.synchronize()
+    assert torch.equal(g["dh0"], dhl)
+    assert torch.count_nonzero(g["dA"]) == 0 and torch.count_nonzero(g["dDskip"]) == 0
+
+
+def test_bwd_rejects_large_N_and_dz_without_z(sw):
+    from paper_2606_00601_amd import ScanWeaverError
+    x = torch.randn((1, 2, 8), device="cuda")
+    with pytest.raises(ScanWeaverError):
+        sw.selective_scan_bwd(x, x, torch.randn((2, 17), device="cuda"),
+                              torch.randn((1, 8, 17), device="cuda"),
+                              torch.randn((1, 8, 17), device="cuda"), None, x)
+
+
+def test_bwd_full_size_sampled(sw):
+    """The Mamba-130M-like shape (bf16, B=8, D=1536, N=16, L=2048) with the
+    Mamba-block options: every row of one batch (its dB and dC are then
+    complete), and every batch of a sample of channels (their dA, dDskip and
+    ddelta_bias are then complete)."""
+    w = wl.workload("selective_bf16_b8_d1536_n16_l2048")
+    opts = ("z", "bias", "softplus", "dybf16")
+    _say("case bwd full size", w.name, opts)
+    inp, ex = _inputs(w.B, w.D, w.N, w.L, 8181, "bf16", opts)
+    g = _run(sw, inp, ex, "bf16", opts)
+    b0 = 5
+    rng = np.random.Generator(np.random.PCG64(82))
+    ds_ = np.sort(rng.choice(w.D, 24, replace=False))
+    rows_b0 = b0 * w.D + np.arange(w.D)
+    rows_d = (np.arange(w.B)[:, None] * w.D + ds_[None, :]).reshape(-1)
+    o = _ref(inp, ex, opts, rows=rows_b0)
+    for k in ("dx", "ddelta", "dz"):
+        got = g[k].reshape(-1, w.L)[torch.as_tensor(rows_b0, device="cuda")].cpu().numpy()
+        assert_gate(fp_gate(got, o[k], o["m_" + k]), f"full-size {k}")
+    for k in ("dB", "dC"):
+        assert_gate(fp_gate(g[k][b0].cpu().numpy(), o[k][b0], o["m_" + k][b0]), f"full-size {k}")
+    o2 = _ref(inp, ex, opts, rows=rows_d)
+    dA = o2["dA_rows"].reshape(w.B, len(ds_), w.N).sum(0)
+    mA = o2["m_dA_rows"].reshape(w.B, len(ds_), w.N).sum(0)
+    assert_gate(fp_gate(g["dA"][torch.as_tensor(ds_, device="cuda")].cpu().numpy(), dA, mA),
+                "full-size dA")
+    for k in ("dDskip", "ddelta_bias"):
+        ref = o2[k + "_rows"].reshape(w.B, len(ds_)).sum(0)
+        mag = o2["m_" + k + "_rows"].reshape(w.B, len(ds_)).sum(0)
+        got = g[k][torch.as_tensor(ds_, device="cuda")].cpu().numpy()
+        assert_gate(fp_gate(got, ref, mag), f"full-size {k}")
