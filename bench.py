@@ -55,13 +55,16 @@ def algorithmic_bytes(w) -> int:
     return x_dl + bc + a_d + out
 
 
+# the sources the forward kernels are built from (the traffic record is keyed to them)
+FWD_SOURCES = ("selective_common.h", "selective_scan.hip", "selective_scan16.hip", "sw_internal.h")
+
+
 def kernel_source_sha256() -> str:
-    """Hash of every kernel source and header (sorted by name)."""
-    import glob
+    """Hash of the forward kernels' sources and headers (sorted by name)."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_00601_amd", "csrc")
-    for p in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+    for p in sorted(os.path.join(csrc, f) for f in FWD_SOURCES):
         h.update(os.path.basename(p).encode())
         with open(p, "rb") as f:
             h.update(f.read())
@@ -195,6 +198,71 @@ def bench_affine(w, args):
     return 0
 
 
+# slots the backward needs per (b,d,t,n) element: exp2 (4 slots) plus twelve
+# fp32 operations -- delta*A', (delta*x)*B, a*h_{t-1}, the state add, the
+# adjoint FMA, lam*q, the dA FMA, (lam q)*A, lam*B, lam*(delta x), ds*h and
+# a*lam (the forward sweep that rebuilds the tile checkpoints is overhead)
+SLOTS_PER_ELEM_BWD = 16.0
+
+
+def bench_bwd(w, args):
+    """Backward of the fused scan on the same workload: dy in the input dtype,
+    every gradient in fp32."""
+    import torch
+
+    import paper_2606_00601_amd as sw
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sw.lib()
+    inp = w.inputs()
+    rng = np.random.Generator(np.random.PCG64(4242))
+    dy = rng.standard_normal((w.B, w.D, w.L)).astype(np.float32)
+    es = 2 if w.dtype == "bf16" else 4
+    if w.dtype == "bf16":
+        dy_t = torch.from_numpy(wl.bf16_round(dy).view(np.int16)).to(dev).view(torch.bfloat16)
+    else:
+        dy_t = torch.from_numpy(dy).to(dev)
+
+    def to_dev(k):
+        if w.dtype == "bf16" and k in ("x", "delta", "Bm", "Cm"):
+            return torch.from_numpy(inp[k + "_bf16"].view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(inp[k]).to(dev)
+
+    t = {k: to_dev(k) for k in ("x", "delta", "A", "Bm", "Cm", "Dskip")}
+    del inp
+
+    def step(i):
+        sw.selective_scan_bwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], dy_t)
+
+    wall, per = time_launches(step, args.steps, args.warmup)
+    kern = float(per.mean())
+    elems = w.elems
+    # algorithmic bytes: x, delta, dy read; dx, ddelta written (fp32); B, C
+    # read, dB, dC written (fp32); A, Dskip read, dA, dDskip, dh0 written
+    abytes = (3 * es + 8) * w.B * w.D * w.L + (2 * es + 8) * w.B * w.L * w.N \
+        + 8 * w.D * w.N + 8 * w.D + 4 * w.B * w.D * w.N
+    achieved = SLOTS_PER_ELEM_BWD * elems / kern
+    out = {
+        "metric": "selective-scan bwd B*L*D*N elems/s (all gradients), 1 GPU",
+        "value": elems * args.steps / wall, "unit": "elems/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "D": w.D, "N": w.N, "L": w.L,
+                   "pass": "backward", "dy": w.dtype, "gradients": "fp32"},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
+                     "unit": "T fp32-lane-slot/s", "frac": achieved / VALU_PEAK,
+                     "traffic": None, "kernel": "selective_bwd_kernel + selective_bwd_reduce_kernel",
+                     "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
+                                       "median": float(np.median(per)) * 1e6},
+                     "slots_per_elem": SLOTS_PER_ELEM_BWD},
+        "hbm": {"algorithmic_bytes": abytes, "achieved_GBs": abytes / kern / 1e9,
+                "peak_GBs": HBM_PEAK_GBS, "frac": abytes / kern / 1e9 / HBM_PEAK_GBS},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +270,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--pass", dest="which", choices=("fwd", "bwd"), default="fwd",
+                    help="time the forward (default, the headline metric) or the backward")
     ap.add_argument("--sets", type=int, default=0,
                     help="input sets rotated through (default: enough to exceed the MALL)")
     ap.add_argument("--print-kernel-sha", action="store_true",
@@ -238,6 +308,8 @@ def main(argv=None):
     w = wl.workload(args.workload)
     if w.path == "affine":
         return bench_affine(w, args)
+    if args.which == "bwd":
+        return bench_bwd(w, args)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     sw.lib()  # the HIP library must be present: no fallback

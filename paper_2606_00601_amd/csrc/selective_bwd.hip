@@ -37,28 +37,21 @@ namespace {
 
 constexpr int BW_N = 16;                 // state lanes per row
 constexpr int BW_T = 8;                  // steps per tile
-constexpr int BW_TS = 12;                // LDS stride of one [t] run (16-byte aligned)
+constexpr int BW_TS = 8;                 // LDS stride of one [t] run (16-byte aligned)
 constexpr int BW_ROWS = 16;              // (b,d) rows per workgroup
-constexpr int BW_RS = BW_N * BW_TS + 8;  // stride of one row's [n][t] block (8 mod 64 banks)
+// stride of one row's [n][t] block: 8 mod 64 banks, so that the 64 lanes of a
+// role-a reduce (8 rows x 8 steps) read 64 different banks; 42.5 KB of LDS in
+// all lets three workgroups share a CU
+constexpr int BW_RS = BW_N * BW_TS + 8;
+constexpr int BW_RING = 4;               // raw tile registers: loads run 3 tiles ahead
 constexpr float BW_LOG2E = 1.4426950408889634f;
 
 struct BwSmem {
-  float rv[3][BW_ROWS][BW_TS];   // per row and step: delta, delta*x, ds
-  float bc[2][BW_N][BW_TS];      // B, C of the tile as [n][t]
-  float sp[2][BW_ROWS * BW_RS];  // per row [n][t]: lam q A, lam B      (sum over n)
-  float pb[2][BW_ROWS * BW_RS];  // per row [n][t]: lam delta x, ds h   (sum over rows)
+  float rv[2][3][BW_ROWS][BW_TS];  // two tile buffers; per row and step: delta, delta*x, ds
+  float bc[2][2][BW_N][BW_TS];     // two tile buffers; B, C of the tile as [n][t]
+  float sp[2][BW_ROWS * BW_RS];    // per row [n][t]: lam q A, lam B      (sum over n)
+  float pb[2][BW_ROWS * BW_RS];    // per row [n][t]: lam delta x, ds h   (sum over rows)
 };
-
-template <typename T>
-__device__ __forceinline__ float ldf(const T* __restrict__ p, int64_t i);
-template <>
-__device__ __forceinline__ float ldf<float>(const float* __restrict__ p, int64_t i) {
-  return p[i];
-}
-template <>
-__device__ __forceinline__ float ldf<uint16_t>(const uint16_t* __restrict__ p, int64_t i) {
-  return bf16_one(p[i]);
-}
 
 __device__ __forceinline__ float sigmoid_f32(float v) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-v * BW_LOG2E));
@@ -78,15 +71,36 @@ struct BwWork {
   float* db_p;     // (B*D)
   float* dB_p;     // (B, G, L, 16)
   float* dC_p;     // (B, G, L, 16)
+  float* trash;    // 256 floats: the target of stores a lane does not need
 };
 
-// Raw per-(row, step) inputs of one tile, held by the staging thread.
-struct RowStep {
-  float x, dl, dy, z, s;
-  bool live;  // a step of a real row inside the sequence
+// Raw bits of one element as loaded; widened to fp32 only when used, so that
+// the load is not waited for until then.
+template <typename T>
+__device__ __forceinline__ float widen(T r) {
+  if constexpr (sizeof(T) == 4)
+    return r;
+  else
+    return __uint_as_float((uint32_t)r << 16);
+}
+
+// One staging thread's raw inputs of one tile.  Waves 0-1 read x, delta, dy
+// (and z, s) of (row, step); waves 2-3 read B, C of (step, state) through the
+// same two slots r0, r1, so that every thread runs the same straight-line
+// loads (their dy, z, s slots read a valid, unused element).
+template <typename IN, typename DYT>
+struct TileRaw {
+  IN r0, r1, z;
+  DYT dy;
+  float s;
+  bool ok;  // role a: a step of a real row inside the sequence; role b: t < L, n < N
 };
 
-template <typename IN, bool GATED>
+// All global loads below are unconditional, from clamped (always valid)
+// addresses, with the unwanted values replaced afterwards: the loads of the
+// next tile then stay in flight across the current one instead of being
+// waited for inside a branch.
+template <typename IN, typename DYT, bool GATED>
 __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, const BwWork w,
                                                             int64_t G, int64_t ntile) {
   __shared__ __align__(16) BwSmem sm;
@@ -95,10 +109,12 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   const IN* __restrict__ BM = static_cast<const IN*>(a.Bm);
   const IN* __restrict__ CM = static_cast<const IN*>(a.Cm);
   const IN* __restrict__ Z = static_cast<const IN*>(a.z);
+  const DYT* __restrict__ DY = static_cast<const DYT*>(a.dy);
   const int64_t D = a.D, L = a.L, N = a.N;
 
   const int tid = threadIdx.x;
-  const int wv = tid / 64, lane = tid % 64;
+  const int wv = __builtin_amdgcn_readfirstlane(tid / 64);  // wave-uniform
+  const int lane = tid % 64;
   const int rr = 4 * wv + lane / 16;  // compute role: row within the workgroup
   const int n = lane % 16;            // ... and state
   const int64_t b = blockIdx.x / G;
@@ -109,35 +125,41 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   const bool nok = n < N;
   const int64_t row = b * D + (dok ? d : D - 1);
 
-  // staging / reduce roles: threads 0..127 own (row sr, step st); threads
-  // 128..255 own (step bt, state bn)
-  const bool role_a = tid < 128;
-  const int sr = tid / BW_T, st = tid % BW_T;
-  const int bt = (tid - 128) / BW_N, bn = (tid - 128) % BW_N;
+  // staging / reduce roles (by wavefront): waves 0-1 own (row sr, step st),
+  // waves 2-3 own (step bt, state bn)
+  const bool role_a = wv < 2;
+  const int sr = (tid % 128) / BW_T, st = tid % BW_T;
+  const int bt = (tid % 128) / BW_N, bn = tid % BW_N;
   const int64_t sd = d0 + sr;
-  const bool sdok = role_a && sd < D;
-  const int64_t srow = b * D + (sd < D ? sd : D - 1);
+  const bool sdok = sd < D;
+  const int64_t srow = b * D + (sdok ? sd : D - 1);
 
-  const float Ar = nok ? a.A[(dok ? d : D - 1) * N + n] : 0.0f;
+  const float Ar = a.A[(dok ? d : D - 1) * N + (nok ? n : 0)] * (nok ? 1.0f : 0.0f);
   const float Al = Ar * BW_LOG2E;
-  const float dbias = (a.delta_bias && role_a) ? a.delta_bias[sd < D ? sd : D - 1] : 0.0f;
-  const float Dsk = (a.Dskip && role_a) ? a.Dskip[sd < D ? sd : D - 1] : 0.0f;
+  const float dbias = a.delta_bias ? a.delta_bias[sdok ? sd : D - 1] : 0.0f;
+  const float Dsk = a.Dskip ? a.Dskip[sdok ? sd : D - 1] : 0.0f;
 
   // --- staging helpers -----------------------------------------------------
-  auto load_rowstep = [&](int64_t k, RowStep& v) {
-    const int64_t t = k * BW_T + st;
-    const bool ok = sdok && t < L;
-    v.live = ok;
-    const int64_t i = srow * L + (ok ? t : 0);
-    v.x = ok ? ldf<IN>(X, i) : 0.0f;
-    v.dl = ok ? ldf<IN>(DL, i) : 0.0f;
-    if (a.dy_bf16)
-      v.dy = ok ? bf16_one(static_cast<const uint16_t*>(a.dy)[i]) : 0.0f;
-    else
-      v.dy = ok ? static_cast<const float*>(a.dy)[i] : 0.0f;
+  const IN* __restrict__ P0 = role_a ? X : BM;
+  const IN* __restrict__ P1 = role_a ? DL : CM;
+  using Raw = TileRaw<IN, DYT>;
+  auto load_tile = [&](int64_t k, Raw& v) {
+    // every address is clamped into range, so tiles past either end (the
+    // read-ahead) load valid, unused elements
+    const int64_t ta = k * BW_T + st;
+    const int64_t tca = ta < 0 ? 0 : (ta < L ? ta : L - 1);
+    const int64_t ia = srow * L + tca;
+    const int64_t tb = k * BW_T + bt;
+    const int64_t tcb = tb < 0 ? 0 : (tb < L ? tb : L - 1);
+    const int64_t ib = (b * L + tcb) * N + (bn < N ? bn : N - 1);
+    v.ok = role_a ? (sdok && ta >= 0 && ta < L) : (tb >= 0 && tb < L && bn < N);
+    const int64_t i01 = role_a ? ia : ib;
+    v.r0 = P0[i01];
+    v.r1 = P1[i01];
+    v.dy = DY[ia];
     if constexpr (GATED) {
-      v.z = ok ? ldf<IN>(Z, i) : 0.0f;
-      v.s = ok ? w.s[i] : 0.0f;
+      v.z = Z[ia];
+      v.s = w.s[ia];
     }
   };
   // delta after bias and softplus, and d delta / d raw (1 without softplus)
@@ -150,39 +172,44 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
     }
     dlv = live ? v : 0.0f;
   };
-  auto load_bc = [&](int64_t k, float& bv, float& cv) {
-    const int64_t t = k * BW_T + bt;
-    const bool ok = !role_a && t < L && bn < N;
-    const int64_t i = (b * L + (ok ? t : 0)) * N + (ok ? bn : 0);
-    bv = ok ? ldf<IN>(BM, i) : 0.0f;
-    cv = ok ? ldf<IN>(CM, i) : 0.0f;
+  auto bc_val = [&](IN r, bool ok) { return ok ? widen<IN>(r) : 0.0f; };
+  const int64_t ck_row = row * ntile;
+  auto ck_at = [&](int64_t k) {
+    const int64_t kc = k < 0 ? 0 : (k < ntile ? k : ntile - 1);
+    return w.ck + (ck_row + kc) * BW_N + n;
   };
+
+  // Raw inputs of tile j live in ring[j % BW_RING]: loads run BW_RING - 1
+  // tiles ahead of their use.
+  Raw ring[BW_RING];
 
   // --- 1. forward sweep: checkpoints ---------------------------------------
   float h = (a.h0 && dok && nok) ? a.h0[row * N + n] : 0.0f;
-  {
-    RowStep nx;
-    float nb_ = 0.f, nc_ = 0.f;
-    if (role_a) load_rowstep(0, nx);
-    else load_bc(0, nb_, nc_);
-    for (int64_t k = 0; k < ntile; ++k) {
+#pragma unroll
+  for (int u = 0; u < BW_RING - 1; ++u) load_tile(u, ring[u]);
+  for (int64_t k0 = 0; k0 < ntile; k0 += BW_RING) {
+#pragma unroll
+    for (int u = 0; u < BW_RING; ++u) {
+      const int64_t k = k0 + u;
+      if (k >= ntile) break;
+      const int buf = u & 1;  // BW_RING is even, so this is k & 1
+      Raw& cur = ring[u];
       if (role_a) {
         float dlv, sg;
-        widen_delta(nx.dl, nx.live, dlv, sg);
-        sm.rv[0][sr][st] = dlv;
-        sm.rv[1][sr][st] = dlv * nx.x;
-        if (k + 1 < ntile) load_rowstep(k + 1, nx);
+        widen_delta(widen<IN>(cur.r1), cur.ok, dlv, sg);
+        sm.rv[buf][0][sr][st] = dlv;
+        sm.rv[buf][1][sr][st] = cur.ok ? dlv * widen<IN>(cur.r0) : 0.0f;
       } else {
-        sm.bc[0][bn][bt] = nb_;
-        if (k + 1 < ntile) load_bc(k + 1, nb_, nc_);
+        sm.bc[buf][0][bn][bt] = bc_val(cur.r0, cur.ok);
       }
-      bw_barrier();
-      if (dok) w.ck[(row * ntile + k) * BW_N + n] = h;
+      load_tile(k + BW_RING - 1, ring[(u + BW_RING - 1) % BW_RING]);
+      bw_barrier();  // one per tile: the other buffer is the one staged next
+      *(dok ? w.ck + (ck_row + k) * BW_N + n : w.trash + tid) = h;
 #pragma unroll
       for (int q = 0; q < BW_T; q += 4) {
-        const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[0][rr][q]);
-        const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[1][rr][q]);
-        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[0][n][q]);
+        const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[buf][0][rr][q]);
+        const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[buf][1][rr][q]);
+        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][q]);
         const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
         const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
         const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
@@ -190,137 +217,155 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         for (int j = 0; j < 4; ++j)
           h = __builtin_fmaf(__builtin_amdgcn_exp2f(dlq[j] * Al), h, dxq[j] * bq[j]);
       }
-      bw_barrier();
     }
   }
+  bw_barrier();  // the reverse sweep restages the buffers of the last tiles
 
   // --- 2./3. reverse sweep ---------------------------------------------------
   float lam = (a.dh_last && dok && nok) ? a.dh_last[row * N + n] : 0.0f;
   float dA_acc = 0.0f;
   float dD_acc = 0.0f, db_acc = 0.0f;  // role a: this thread's (row, step slot)
-  RowStep cur;
-  float cb = 0.f, cc = 0.f;
-  if (role_a) load_rowstep(ntile - 1, cur);
-  else load_bc(ntile - 1, cb, cc);
-  for (int64_t k = ntile - 1; k >= 0; --k) {
-    // stage tile k
-    float dlv = 0.f, sg = 1.f, ds = 0.f, gp = 0.f;
-    const bool live = role_a && cur.live;
-    if (role_a) {
-      widen_delta(cur.dl, live, dlv, sg);
-      float gt = 1.0f;
-      if constexpr (GATED) {
-        const float sz = sigmoid_f32(cur.z);
-        gt = cur.z * sz;
-        gp = sz * (1.0f + cur.z * (1.0f - sz));
+  float hring[BW_RING];
+#pragma unroll
+  for (int u = 0; u < BW_RING - 1; ++u) {
+    load_tile(ntile - 1 - u, ring[u]);
+    hring[u] = *ck_at(ntile - 1 - u);
+  }
+  for (int64_t k0 = ntile - 1; k0 >= 0; k0 -= BW_RING) {
+#pragma unroll
+    for (int u = 0; u < BW_RING; ++u) {
+      const int64_t k = k0 - u;
+      if (k < 0) break;
+      // tile k is in ring[u] (its index counted down from the last tile)
+      const int buf = (int)(k & 1);
+      Raw& cur = ring[u];
+      float dlv = 0.f, sg = 1.f, ds = 0.f, gp = 0.f, xv = 0.f, dyv = 0.f, sv = 0.f;
+      const bool live = role_a && cur.ok;
+      if (role_a) {
+        widen_delta(widen<IN>(cur.r1), live, dlv, sg);
+        xv = widen<IN>(cur.r0);
+        dyv = widen<DYT>(cur.dy);
+        float gt = 1.0f;
+        if constexpr (GATED) {
+          const float zv = widen<IN>(cur.z);
+          const float sz = sigmoid_f32(zv);
+          gt = zv * sz;
+          gp = sz * (1.0f + zv * (1.0f - sz));
+          sv = cur.s;
+        }
+        ds = live ? dyv * gt : 0.0f;
+        sm.rv[buf][0][sr][st] = dlv;
+        sm.rv[buf][1][sr][st] = live ? dlv * xv : 0.0f;
+        sm.rv[buf][2][sr][st] = ds;
+      } else {
+        sm.bc[buf][0][bn][bt] = bc_val(cur.r0, cur.ok);
+        sm.bc[buf][1][bn][bt] = bc_val(cur.r1, cur.ok);
       }
-      ds = cur.dy * gt;
-      sm.rv[0][sr][st] = dlv;
-      sm.rv[1][sr][st] = dlv * cur.x;
-      sm.rv[2][sr][st] = ds;
-    } else {
-      sm.bc[0][bn][bt] = cb;
-      sm.bc[1][bn][bt] = cc;
-    }
-    const RowStep mine = cur;
-    if (k > 0) {
-      if (role_a) load_rowstep(k - 1, cur);
-      else load_bc(k - 1, cb, cc);
-    }
-    const float hck = dok ? w.ck[(row * ntile + k) * BW_N + n] : 0.0f;
-    bw_barrier();
+      const float hstart = dok ? hring[u] : 0.0f;
+      load_tile(k - (BW_RING - 1), ring[(u + BW_RING - 1) % BW_RING]);
+      hring[(u + BW_RING - 1) % BW_RING] = *ck_at(k - (BW_RING - 1));
+      bw_barrier();
 
-    // recompute a_t and q_t = a_t h_{t-1} of the tile
-    float av[BW_T], qv[BW_T];
-    {
-      float hh = hck;
+      // recompute a_t and q_t = a_t h_{t-1} of the tile
+      float av[BW_T], qv[BW_T];
+      {
+        float hh = hstart;
 #pragma unroll
-      for (int q = 0; q < BW_T; q += 4) {
-        const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[0][rr][q]);
-        const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[1][rr][q]);
-        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[0][n][q]);
-        const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
-        const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
-        const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
+        for (int q = 0; q < BW_T; q += 4) {
+          const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[buf][0][rr][q]);
+          const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[buf][1][rr][q]);
+          const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][q]);
+          const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
+          const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
+          const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          av[q + j] = __builtin_amdgcn_exp2f(dlq[j] * Al);
-          qv[q + j] = av[q + j] * hh;
-          hh = __builtin_fmaf(dxq[j], bq[j], qv[q + j]);
+          for (int j = 0; j < 4; ++j) {
+            av[q + j] = __builtin_amdgcn_exp2f(dlq[j] * Al);
+            qv[q + j] = av[q + j] * hh;
+            hh = __builtin_fmaf(dxq[j], bq[j], qv[q + j]);
+          }
         }
       }
-    }
-    // walk the tile backwards
-    float* const sp0 = &sm.sp[0][rr * BW_RS + n * BW_TS];
-    float* const sp1 = &sm.sp[1][rr * BW_RS + n * BW_TS];
-    float* const pb0 = &sm.pb[0][rr * BW_RS + n * BW_TS];
-    float* const pb1 = &sm.pb[1][rr * BW_RS + n * BW_TS];
+      // walk the tile backwards
+      float* const sp0 = &sm.sp[0][rr * BW_RS + n * BW_TS];
+      float* const sp1 = &sm.sp[1][rr * BW_RS + n * BW_TS];
+      float* const pb0 = &sm.pb[0][rr * BW_RS + n * BW_TS];
+      float* const pb1 = &sm.pb[1][rr * BW_RS + n * BW_TS];
 #pragma unroll
-    for (int q = BW_T - 4; q >= 0; q -= 4) {
-      const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[0][rr][q]);
-      const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[1][rr][q]);
-      const float4 ds4 = *reinterpret_cast<const float4*>(&sm.rv[2][rr][q]);
-      const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[0][n][q]);
-      const float4 c4 = *reinterpret_cast<const float4*>(&sm.bc[1][n][q]);
-      const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
-      const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
-      const float dsq[4] = {ds4.x, ds4.y, ds4.z, ds4.w};
-      const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
-      const float cq[4] = {c4.x, c4.y, c4.z, c4.w};
-      float o0[4], o1[4], o2[4], o3[4];
+      for (int q = BW_T - 4; q >= 0; q -= 4) {
+        const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[buf][0][rr][q]);
+        const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[buf][1][rr][q]);
+        const float4 ds4 = *reinterpret_cast<const float4*>(&sm.rv[buf][2][rr][q]);
+        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][q]);
+        const float4 c4 = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n][q]);
+        const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
+        const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
+        const float dsq[4] = {ds4.x, ds4.y, ds4.z, ds4.w};
+        const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
+        const float cq[4] = {c4.x, c4.y, c4.z, c4.w};
+        float o0[4], o1[4], o2[4], o3[4];
 #pragma unroll
-      for (int j = 3; j >= 0; --j) {
-        const float l = __builtin_fmaf(dsq[j], cq[j], lam);
-        const float hc = __builtin_fmaf(dxq[j], bq[j], qv[q + j]);
-        const float p = l * qv[q + j];
-        dA_acc = __builtin_fmaf(p, dlq[j], dA_acc);
-        o0[j] = p * Ar;
-        o1[j] = l * bq[j];
-        o2[j] = l * dxq[j];
-        o3[j] = dsq[j] * hc;
-        lam = av[q + j] * l;
+        for (int j = 3; j >= 0; --j) {
+          const float l = __builtin_fmaf(dsq[j], cq[j], lam);
+          const float hc = __builtin_fmaf(dxq[j], bq[j], qv[q + j]);
+          const float p = l * qv[q + j];
+          dA_acc = __builtin_fmaf(p, dlq[j], dA_acc);
+          o0[j] = p * Ar;
+          o1[j] = l * bq[j];
+          o2[j] = l * dxq[j];
+          o3[j] = dsq[j] * hc;
+          lam = av[q + j] * l;
+        }
+        *reinterpret_cast<float4*>(sp0 + q) = make_float4(o0[0], o0[1], o0[2], o0[3]);
+        *reinterpret_cast<float4*>(sp1 + q) = make_float4(o1[0], o1[1], o1[2], o1[3]);
+        *reinterpret_cast<float4*>(pb0 + q) = make_float4(o2[0], o2[1], o2[2], o2[3]);
+        *reinterpret_cast<float4*>(pb1 + q) = make_float4(o3[0], o3[1], o3[2], o3[3]);
       }
-      *reinterpret_cast<float4*>(sp0 + q) = make_float4(o0[0], o0[1], o0[2], o0[3]);
-      *reinterpret_cast<float4*>(sp1 + q) = make_float4(o1[0], o1[1], o1[2], o1[3]);
-      *reinterpret_cast<float4*>(pb0 + q) = make_float4(o2[0], o2[1], o2[2], o2[3]);
-      *reinterpret_cast<float4*>(pb1 + q) = make_float4(o3[0], o3[1], o3[2], o3[3]);
-    }
-    bw_barrier();
+      bw_barrier();  // the partials are complete; the next tile stages the other buffer
 
-    if (role_a) {
-      // sum over states: ddelta and dx of (row sr, step st)
-      float s1 = 0.f, s2 = 0.f;
+      // Role a sums over the states (ddelta, dx of row sr, step st), role b
+      // over the 16 rows (this workgroup's share of dB, dC at step bt, state
+      // bn).  The stores are the same instructions for every lane, aimed at
+      // the trash slots where a lane has nothing to store.
+      float v0, v1, v2 = 0.f;
+      float *p0, *p1, *p2 = w.trash + tid;
+      if (role_a) {
+        float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-      for (int m = 0; m < BW_N; ++m) {
-        s1 += sm.sp[0][sr * BW_RS + m * BW_TS + st];
-        s2 += sm.sp[1][sr * BW_RS + m * BW_TS + st];
-      }
-      const int64_t t = k * BW_T + st;
-      if (live) {
-        const float ddl = (s1 + mine.x * s2) * sg;
-        const int64_t i = srow * L + t;
-        a.ddelta[i] = ddl;
-        a.dx[i] = __builtin_fmaf(dlv, s2, ds * Dsk);
-        if constexpr (GATED) a.dz[i] = mine.dy * mine.s * gp;
-        dD_acc = __builtin_fmaf(ds, mine.x, dD_acc);
+        for (int m = 0; m < BW_N; ++m) {
+          s1 += sm.sp[0][sr * BW_RS + m * BW_TS + st];
+          s2 += sm.sp[1][sr * BW_RS + m * BW_TS + st];
+        }
+        const float ddl = live ? (s1 + xv * s2) * sg : 0.0f;
+        v0 = ddl;
+        v1 = __builtin_fmaf(dlv, s2, ds * Dsk);
+        const int64_t i = srow * L + (live ? k * BW_T + st : 0);
+        p0 = live ? a.ddelta + i : w.trash + tid;
+        p1 = live ? a.dx + i : w.trash + tid;
+        if constexpr (GATED) {
+          v2 = dyv * sv * gp;
+          p2 = live ? a.dz + i : w.trash + tid;
+        }
+        dD_acc = __builtin_fmaf(ds, xv, dD_acc);
         db_acc += ddl;
-      }
-    } else {
-      // sum over the 16 rows: this workgroup's share of dB and dC at (step bt, state bn)
-      float sb = 0.f, sc = 0.f;
+      } else {
+        float sb = 0.f, sc = 0.f;
 #pragma unroll
-      for (int m = 0; m < BW_ROWS; ++m) {
-        sb += sm.pb[0][m * BW_RS + bn * BW_TS + bt];
-        sc += sm.pb[1][m * BW_RS + bn * BW_TS + bt];
+        for (int m = 0; m < BW_ROWS; ++m) {
+          sb += sm.pb[0][m * BW_RS + bn * BW_TS + bt];
+          sc += sm.pb[1][m * BW_RS + bn * BW_TS + bt];
+        }
+        const int64_t t = k * BW_T + bt;
+        const int64_t i = ((b * G + g) * L + (t < L ? t : 0)) * BW_N + bn;
+        v0 = sb;
+        v1 = sc;
+        p0 = t < L ? w.dB_p + i : w.trash + tid;
+        p1 = t < L ? w.dC_p + i : w.trash + tid;
       }
-      const int64_t t = k * BW_T + bt;
-      if (t < L) {
-        const int64_t i = ((b * G + g) * L + t) * BW_N + bn;
-        w.dB_p[i] = sb;
-        w.dC_p[i] = sc;
-      }
+      *p0 = v0;
+      *p1 = v1;
+      if constexpr (GATED) *p2 = v2;
     }
-    bw_barrier();
   }
 
   if (dok && nok) {
@@ -377,6 +422,27 @@ __global__ __launch_bounds__(256) void selective_bwd_reduce_kernel(const BwdArgs
   }
 }
 
+template <typename IN>
+void launch_bwd_in(const BwdArgs& a, const BwWork& w, int64_t G, int64_t ntile, int64_t grid,
+                   hipStream_t s) {
+  if (a.dy_bf16) {
+    auto kern = a.z ? selective_bwd_kernel<IN, uint16_t, true>
+                    : selective_bwd_kernel<IN, uint16_t, false>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile);
+  } else {
+    auto kern = a.z ? selective_bwd_kernel<IN, float, true> : selective_bwd_kernel<IN, float, false>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile);
+  }
+}
+
+void launch_bwd(const BwdArgs& a, const BwWork& w, int64_t G, int64_t ntile, int64_t grid,
+                hipStream_t s) {
+  if (a.bf16_in)
+    launch_bwd_in<uint16_t>(a, w, G, ntile, grid, s);
+  else
+    launch_bwd_in<float>(a, w, G, ntile, grid, s);
+}
+
 }  // namespace
 
 int selective_bwd(const BwdArgs& a) {
@@ -393,7 +459,7 @@ int selective_bwd(const BwdArgs& a) {
   const size_t R = (size_t)(B * D);
   const size_t n_ck = R * (size_t)ntile * BW_N, n_s = a.z ? R * (size_t)L : 0;
   const size_t n_dA = R * BW_N, n_bc = (size_t)(B * G) * (size_t)L * BW_N;
-  const size_t total = n_ck + n_s + n_dA + 2 * R + 2 * n_bc;
+  const size_t total = n_ck + n_s + n_dA + 2 * R + 2 * n_bc + 256;
   void* base = nullptr;
   int st = workspace_alloc(&base, total * sizeof(float), s);
   if (st != SW_OK) return st;
@@ -413,6 +479,8 @@ int selective_bwd(const BwdArgs& a) {
   w.dB_p = f;
   f += n_bc;
   w.dC_p = f;
+  f += n_bc;
+  w.trash = f;
   if (a.z) {
     // the pre-gate output: the forward pass without the gate
     SelArgs fa{};
@@ -438,13 +506,7 @@ int selective_bwd(const BwdArgs& a) {
       return st;
     }
   }
-  if (a.bf16_in) {
-    auto kern = a.z ? selective_bwd_kernel<uint16_t, true> : selective_bwd_kernel<uint16_t, false>;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile);
-  } else {
-    auto kern = a.z ? selective_bwd_kernel<float, true> : selective_bwd_kernel<float, false>;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile);
-  }
+  launch_bwd(a, w, G, ntile, grid, s);
   st = check_launch("selective_bwd_kernel");
   if (st == SW_OK) {
     int64_t work = B * L * a.N;
