@@ -46,6 +46,11 @@ constexpr int BW_RS = BW_N * BW_TS + 8;
 constexpr int BW_RING = 4;               // raw tile registers: loads run 3 tiles ahead
 constexpr float BW_LOG2E = 1.4426950408889634f;
 
+// Position of step t of state n inside its 8-step run: the two 4-step halves
+// trade places for n >= 8, so that the 16 states of a row (float4 accesses)
+// and the 16 x 4 (state, step) lanes of the reduces fall on 64 different banks.
+__device__ __forceinline__ int swz(int n, int t) { return t ^ ((n >> 1) & 4); }
+
 struct BwSmem {
   float rv[2][3][BW_ROWS][BW_TS];  // two tile buffers; per row and step: delta, delta*x, ds
   float bc[2][2][BW_N][BW_TS];     // two tile buffers; B, C of the tile as [n][t]
@@ -200,7 +205,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         sm.rv[buf][0][sr][st] = dlv;
         sm.rv[buf][1][sr][st] = cur.ok ? dlv * widen<IN>(cur.r0) : 0.0f;
       } else {
-        sm.bc[buf][0][bn][bt] = bc_val(cur.r0, cur.ok);
+        sm.bc[buf][0][bn][swz(bn, bt)] = bc_val(cur.r0, cur.ok);
       }
       load_tile(k + BW_RING - 1, ring[(u + BW_RING - 1) % BW_RING]);
       bw_barrier();  // one per tile: the other buffer is the one staged next
@@ -209,7 +214,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
       for (int q = 0; q < BW_T; q += 4) {
         const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[buf][0][rr][q]);
         const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[buf][1][rr][q]);
-        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][q]);
+        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][swz(n, q)]);
         const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
         const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
         const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
@@ -258,8 +263,8 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         sm.rv[buf][1][sr][st] = live ? dlv * xv : 0.0f;
         sm.rv[buf][2][sr][st] = ds;
       } else {
-        sm.bc[buf][0][bn][bt] = bc_val(cur.r0, cur.ok);
-        sm.bc[buf][1][bn][bt] = bc_val(cur.r1, cur.ok);
+        sm.bc[buf][0][bn][swz(bn, bt)] = bc_val(cur.r0, cur.ok);
+        sm.bc[buf][1][bn][swz(bn, bt)] = bc_val(cur.r1, cur.ok);
       }
       const float hstart = dok ? hring[u] : 0.0f;
       load_tile(k - (BW_RING - 1), ring[(u + BW_RING - 1) % BW_RING]);
@@ -274,7 +279,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         for (int q = 0; q < BW_T; q += 4) {
           const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[buf][0][rr][q]);
           const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[buf][1][rr][q]);
-          const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][q]);
+          const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][swz(n, q)]);
           const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
           const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
           const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
@@ -296,8 +301,8 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[buf][0][rr][q]);
         const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[buf][1][rr][q]);
         const float4 ds4 = *reinterpret_cast<const float4*>(&sm.rv[buf][2][rr][q]);
-        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][q]);
-        const float4 c4 = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n][q]);
+        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][swz(n, q)]);
+        const float4 c4 = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n][swz(n, q)]);
         const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
         const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
         const float dsq[4] = {ds4.x, ds4.y, ds4.z, ds4.w};
@@ -316,10 +321,11 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
           o3[j] = dsq[j] * hc;
           lam = av[q + j] * l;
         }
-        *reinterpret_cast<float4*>(sp0 + q) = make_float4(o0[0], o0[1], o0[2], o0[3]);
-        *reinterpret_cast<float4*>(sp1 + q) = make_float4(o1[0], o1[1], o1[2], o1[3]);
-        *reinterpret_cast<float4*>(pb0 + q) = make_float4(o2[0], o2[1], o2[2], o2[3]);
-        *reinterpret_cast<float4*>(pb1 + q) = make_float4(o3[0], o3[1], o3[2], o3[3]);
+        const int qs = swz(n, q);
+        *reinterpret_cast<float4*>(sp0 + qs) = make_float4(o0[0], o0[1], o0[2], o0[3]);
+        *reinterpret_cast<float4*>(sp1 + qs) = make_float4(o1[0], o1[1], o1[2], o1[3]);
+        *reinterpret_cast<float4*>(pb0 + qs) = make_float4(o2[0], o2[1], o2[2], o2[3]);
+        *reinterpret_cast<float4*>(pb1 + qs) = make_float4(o3[0], o3[1], o3[2], o3[3]);
       }
       bw_barrier();  // the partials are complete; the next tile stages the other buffer
 
@@ -333,8 +339,8 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         float s1 = 0.f, s2 = 0.f;
 #pragma unroll
         for (int m = 0; m < BW_N; ++m) {
-          s1 += sm.sp[0][sr * BW_RS + m * BW_TS + st];
-          s2 += sm.sp[1][sr * BW_RS + m * BW_TS + st];
+          s1 += sm.sp[0][sr * BW_RS + m * BW_TS + swz(m, st)];
+          s2 += sm.sp[1][sr * BW_RS + m * BW_TS + swz(m, st)];
         }
         const float ddl = live ? (s1 + xv * s2) * sg : 0.0f;
         v0 = ddl;
@@ -352,8 +358,8 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         float sb = 0.f, sc = 0.f;
 #pragma unroll
         for (int m = 0; m < BW_ROWS; ++m) {
-          sb += sm.pb[0][m * BW_RS + bn * BW_TS + bt];
-          sc += sm.pb[1][m * BW_RS + bn * BW_TS + bt];
+          sb += sm.pb[0][m * BW_RS + bn * BW_TS + swz(bn, bt)];
+          sc += sm.pb[1][m * BW_RS + bn * BW_TS + swz(bn, bt)];
         }
         const int64_t t = k * BW_T + bt;
         const int64_t i = ((b * G + g) * L + (t < L ? t : 0)) * BW_N + bn;
@@ -386,24 +392,53 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   }
 }
 
-// Adds the shares in a fixed order: dB, dC over the workgroups of a batch;
-// dA, dDskip, ddelta_bias over the batch.
+// Adds the shares in a fixed order: dB, dC over the workgroups of a batch
+// (one thread per 4 states of one (b, t) and one of dB / dC, float4 loads,
+// eight in flight, summed in workgroup order); dA, dDskip, ddelta_bias over
+// the batch.
 __global__ __launch_bounds__(256) void selective_bwd_reduce_kernel(const BwdArgs a,
                                                                    const BwWork w, int64_t G) {
   const int64_t B = a.B, D = a.D, N = a.N, L = a.L;
-  const int64_t nbc = B * L * N;
+  const int64_t nq = B * L * (BW_N / 4);  // float4 chunks of one of dB / dC
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nbc; i += stride) {
-    const int64_t nn = i % N, bt = i / N;  // bt = b*L + t
-    const int64_t b = bt / L, t = bt - b * L;
-    float sb = 0.f, sc = 0.f;
-    for (int64_t g = 0; g < G; ++g) {
-      const int64_t j = ((b * G + g) * L + t) * BW_N + nn;
-      sb += w.dB_p[j];
-      sc += w.dC_p[j];
+  const int64_t gstep = L * (BW_N / 4);   // float4 stride between workgroup shares
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < 2 * nq; i += stride) {
+    const bool isC = i >= nq;
+    const int64_t r = isC ? i - nq : i;  // r = (b*L + t)*4 + c
+    const int64_t c = r % (BW_N / 4), bt = r / (BW_N / 4);
+    const int64_t b = bt / L;
+    const float4* __restrict__ src =
+        reinterpret_cast<const float4*>(isC ? w.dC_p : w.dB_p) + b * G * gstep + (bt - b * L) * 4 + c;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    int64_t g = 0;
+    for (; g + 8 <= G; g += 8) {
+      float4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = src[(g + u) * gstep];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        acc.x += v[u].x;
+        acc.y += v[u].y;
+        acc.z += v[u].z;
+        acc.w += v[u].w;
+      }
     }
-    a.dB[i] = sb;
-    a.dC[i] = sc;
+    for (; g < G; ++g) {
+      const float4 v = src[g * gstep];
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    float* const dst = (isC ? a.dC : a.dB) + bt * N;
+    const float av[4] = {acc.x, acc.y, acc.z, acc.w};
+    if (N == BW_N && (((uintptr_t)a.dB | (uintptr_t)a.dC) & 15) == 0) {
+      *reinterpret_cast<float4*>(dst + 4 * c) = acc;
+    } else {
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (4 * c + u < N) dst[4 * c + u] = av[u];
+    }
   }
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < D * N; i += stride) {
     const int64_t d = i / N, nn = i - d * N;
@@ -509,7 +544,7 @@ int selective_bwd(const BwdArgs& a) {
   launch_bwd(a, w, G, ntile, grid, s);
   st = check_launch("selective_bwd_kernel");
   if (st == SW_OK) {
-    int64_t work = B * L * a.N;
+    int64_t work = 2 * B * L * (BW_N / 4);
     if (work < D * a.N) work = D * a.N;
     int64_t blocks = (work + 255) / 256;
     if (blocks > 8192) blocks = 8192;
