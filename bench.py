@@ -172,7 +172,10 @@ def bench_affine(w, args):
 
     def step(i):
         a, bx, h = sets[i % nsets]
-        sw.affine_scan(a, bx, out=h)
+        if args.schedule == "default":
+            sw.affine_scan(a, bx, out=h)
+        else:
+            sw.affine_scan_schedule(a, bx, out=h, schedule=args.schedule)
 
     wall, per = time_launches(step, args.steps, args.warmup)
     kern = float(per.mean())
@@ -182,13 +185,16 @@ def bench_affine(w, args):
     cus = torch.cuda.get_device_properties(dev).multi_processor_count
     kname = ("affine_rows_kernel" if w.L > 2048 and w.B * w.D >= 8 * cus
              else "affine_scan_kernel")
+    if args.schedule == "blelloch":
+        kname = "affine_blelloch_kernel"
     out = {
         "metric": "affine-scan fwd B*L*D elems/s (+ achieved HBM GB/s vs peak), 1 GPU",
         "value": w.elems * args.steps / wall, "unit": "elems/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "B": w.B, "D": w.D, "L": w.L, "input_sets_rotated": nsets},
+        "config": {"workload": w.name, "B": w.B, "D": w.D, "L": w.L, "input_sets_rotated": nsets,
+                   "schedule": args.schedule},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS, "traffic": None, "kernel": kname,
                      "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
@@ -272,6 +278,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--pass", dest="which", choices=("fwd", "bwd"), default="fwd",
                     help="time the forward (default, the headline metric) or the backward")
+    ap.add_argument("--schedule", choices=("default", "blelloch"), default="default",
+                    help="scan schedule of the bare-scan workloads (schedule ablation)")
     ap.add_argument("--sets", type=int, default=0,
                     help="input sets rotated through (default: enough to exceed the MALL)")
     ap.add_argument("--print-kernel-sha", action="store_true",

@@ -80,6 +80,28 @@ int sw_affine_scan(const float* a, const float* bx, const float* h0, float* h_ou
 int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t* h0, int32_t* h_out,
                        int64_t B, int64_t D, int64_t L);
 
+/* Scan schedules of sw_affine_scan_schedule. */
+enum {
+  SW_SCHED_DEFAULT = 0,  /* the library's: lane-sequential composition, DPP wavefront scan,
+                            LDS combine, decoupled look-back (what sw_affine_scan runs) */
+  SW_SCHED_BLELLOCH = 1  /* the paper's (Sec. 3.3): a Blelloch upsweep / root / downsweep tree
+                            over 2048-pair chunks in LDS, then affine-prefix reconstruction;
+                            one workgroup per row, chunk carries in registers */
+};
+
+/*
+ * sw_affine_scan (fp32) and sw_affine_scan_i32 with an explicit scan
+ * schedule, for comparing schedules on the same recurrence.  Same arguments,
+ * layout, results (bit-identical in int32; within fp32 rounding in fp32) and
+ * errors, plus SW_ERR_INVALID_ARG for an unknown schedule.  The Blelloch
+ * schedule gives each (b,d) row one workgroup, so it fills the GPU only when
+ * there are many rows.
+ */
+int sw_affine_scan_schedule(const float* a, const float* bx, const float* h0, float* h_out,
+                            int64_t B, int64_t D, int64_t L, int schedule);
+int sw_affine_scan_schedule_i32(const int32_t* a, const int32_t* bx, const int32_t* h0,
+                                int32_t* h_out, int64_t B, int64_t D, int64_t L, int schedule);
+
 /*
  * Recurrence with input and output projections, elementwise (Eq. (3)-(4)):
  *   h[b,d,t] = a[b,d,t] * h[b,d,t-1] + b[b,d,t] * x[b,d,t]      (h[b,d,-1] = h0)

@@ -19,7 +19,8 @@ import torch
 
 from ._lib import ScanWeaverError, check, last_error, lib, status_string  # noqa: F401
 
-__all__ = ["affine_scan", "affine_scan_i32", "affine_scan_proj", "affine_scan_proj_i32",
+__all__ = ["affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
+           "affine_scan_proj", "affine_scan_proj_i32",
            "selective_scan_fwd", "selective_scan_bwd", "ScanWeaverError",
            "version"]
 
@@ -75,6 +76,24 @@ def affine_scan(a, bx, h0=None, out=None):
 def affine_scan_i32(a, bx, h0=None, out=None):
     """The recurrence in Z/2^32 on int32 tensors (bit-exact for any schedule)."""
     return _affine(lib().sw_affine_scan_i32, "sw_affine_scan_i32", torch.int32, a, bx, h0, out)
+
+
+_SCHEDULES = {"default": 0, "blelloch": 1}
+
+
+def affine_scan_schedule(a, bx, h0=None, out=None, *, schedule="default"):
+    """:func:`affine_scan` with an explicit scan schedule ("default" or
+    "blelloch", the paper's upsweep / downsweep tree)."""
+    sched = _SCHEDULES[schedule]
+    fn = lambda *args: lib().sw_affine_scan_schedule(*args, sched)  # noqa: E731
+    return _affine(fn, "sw_affine_scan_schedule", torch.float32, a, bx, h0, out)
+
+
+def affine_scan_schedule_i32(a, bx, h0=None, out=None, *, schedule="default"):
+    """:func:`affine_scan_i32` with an explicit scan schedule."""
+    sched = _SCHEDULES[schedule]
+    fn = lambda *args: lib().sw_affine_scan_schedule_i32(*args, sched)  # noqa: E731
+    return _affine(fn, "sw_affine_scan_schedule_i32", torch.int32, a, bx, h0, out)
 
 
 def _affine_proj(fn, where, dtype, a, b, x, c, h0, y, want_h_last):

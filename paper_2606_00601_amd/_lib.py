@@ -19,6 +19,8 @@ SW_ERR_ALLOC = 4
 SW_DTYPE_F32 = 0
 SW_DTYPE_BF16 = 1
 SW_DELTA_SOFTPLUS = 1
+SW_SCHED_DEFAULT = 0
+SW_SCHED_BLELLOCH = 1
 
 # name -> (restype, argtypes), mirroring include/scanweaver.h
 _vp, _i64, _int = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
@@ -26,6 +28,8 @@ SIGNATURES = {
     "sw_version": (_int, []),
     "sw_affine_scan": (_int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64]),
     "sw_affine_scan_i32": (_int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64]),
+    "sw_affine_scan_schedule": (_int, [_vp] * 4 + [_i64] * 3 + [_int]),
+    "sw_affine_scan_schedule_i32": (_int, [_vp] * 4 + [_i64] * 3 + [_int]),
     "sw_affine_scan_proj": (_int, [_vp] * 7 + [_i64] * 3),
     "sw_selective_scan_bwd": (_int, [_vp] * 20 + [_i64] * 4 + [_int] * 3),
     "sw_affine_scan_proj_i32": (_int, [_vp] * 7 + [_i64] * 3),

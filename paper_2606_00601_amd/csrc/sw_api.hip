@@ -17,6 +17,10 @@ int affine_scan_f32(const float* a, const float* bx, const float* h0, float* h, 
                     int64_t L, bool vec);
 int affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
                     int64_t R, int64_t L, bool vec);
+int affine_blelloch_f32(const float* a, const float* bx, const float* h0, float* h, int64_t R,
+                        int64_t L, bool vec);
+int affine_blelloch_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
+                        int64_t R, int64_t L, bool vec);
 int affine_scan_io_f32(const float* a, const float* b, const float* x, const float* c,
                        const float* h0, float* y, float* h_last, int64_t R, int64_t L, bool vec);
 int affine_scan_io_u32(const uint32_t* a, const uint32_t* b, const uint32_t* x, const uint32_t* c,
@@ -458,6 +462,27 @@ SW_API int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t
                                      reinterpret_cast<const uint32_t*>(h0),
                                      reinterpret_cast<uint32_t*>(h_out), B, D, L,
                                      sw::affine_scan_u32);
+}
+
+SW_API int sw_affine_scan_schedule(const float* a, const float* bx, const float* h0,
+                                  float* h_out, int64_t B, int64_t D, int64_t L, int schedule) {
+  if (schedule == SW_SCHED_DEFAULT) return sw_affine_scan(a, bx, h0, h_out, B, D, L);
+  if (schedule != SW_SCHED_BLELLOCH)
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown schedule %d", schedule);
+  return sw::affine_common<float>(a, bx, h0, h_out, B, D, L, sw::affine_blelloch_f32);
+}
+
+SW_API int sw_affine_scan_schedule_i32(const int32_t* a, const int32_t* bx, const int32_t* h0,
+                                      int32_t* h_out, int64_t B, int64_t D, int64_t L,
+                                      int schedule) {
+  if (schedule == SW_SCHED_DEFAULT) return sw_affine_scan_i32(a, bx, h0, h_out, B, D, L);
+  if (schedule != SW_SCHED_BLELLOCH)
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown schedule %d", schedule);
+  return sw::affine_common<uint32_t>(reinterpret_cast<const uint32_t*>(a),
+                                     reinterpret_cast<const uint32_t*>(bx),
+                                     reinterpret_cast<const uint32_t*>(h0),
+                                     reinterpret_cast<uint32_t*>(h_out), B, D, L,
+                                     sw::affine_blelloch_u32);
 }
 
 SW_API int sw_affine_scan_proj(const float* a, const float* b, const float* x, const float* c,

@@ -65,6 +65,11 @@ def test_validation_without_gpu(lib):
     # overflowing sizes are refused
     big = 1 << 40
     assert lib.sw_affine_scan(None, None, None, None, big, big, 4) == 2
+    # schedules: unknown ones are refused; the Blelloch one validates like the default
+    assert lib.sw_affine_scan_schedule(None, None, None, None, 1, 1, 4, 7) == 1
+    assert "schedule" in lib.sw_last_error().decode()
+    assert lib.sw_affine_scan_schedule(None, None, None, None, -1, 1, 4, 1) == 1
+    assert lib.sw_affine_scan_schedule_i32(None, None, None, None, 0, 1, 4, 1) == 0
     # the projection form: negative sizes, then empty shapes are a no-op
     assert lib.sw_affine_scan_proj(*([None] * 7), -1, 1, 1) == 1
     assert lib.sw_affine_scan_proj_i32(*([None] * 7), 1, 1, -1) == 1

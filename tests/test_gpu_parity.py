@@ -533,3 +533,53 @@ def test_proj_empty_and_L0(sw):
     e = torch.empty((0, 3, 5), device="cuda")
     y, hl = sw.affine_scan_proj(e, e)
     assert y.shape == (0, 3, 5) and hl.shape == (0, 3)
+
+
+# -------------------------------------- the paper's schedule (Blelloch tree)
+
+# (B, D, L): one chunk, ragged tails, several chunks, many rows
+_SCHED_SHAPES = [(1, 1, 1), (2, 3, 5), (1, 4, 2048), (1, 3, 2049), (2, 5, 6151), (1, 2, 100001),
+                 (3, 700, 3 * 2048 + 4)]
+
+
+@pytest.mark.parametrize("B,D,L", _SCHED_SHAPES)
+def test_blelloch_schedule_i32_bitexact(sw, B, D, L):
+    _say("case blelloch i32", B, D, L)
+    inp = wl.affine_inputs_i32(B, D, L, 7000 + L, "odd")
+    h0 = wl.affine_inputs_i32(B, D, 1, 7100 + L, "h0")["h0"]
+    h = sw.affine_scan_schedule_i32(dev(inp["a"]), dev(inp["bx"]), dev(h0),
+                                    schedule="blelloch").cpu().numpy()
+    assert np.array_equal(h, oracle.affine_scan_i32(inp["a"], inp["bx"], h0))
+
+
+@pytest.mark.parametrize("B,D,L", _SCHED_SHAPES)
+def test_blelloch_schedule_f32(sw, B, D, L):
+    _say("case blelloch f32", B, D, L)
+    inp = wl.affine_inputs(B, D, L, 7200 + L, with_h0=True)
+    h = sw.affine_scan_schedule(dev(inp["a"]), dev(inp["bx"]), dev(inp["h0"]),
+                                schedule="blelloch").cpu().numpy()
+    ref, mag, sens = oracle.affine_scan(inp["a"], inp["bx"], inp["h0"], bounds=True)
+    assert_gate(fp_gate(h, ref, mag, sens), f"blelloch f32 {B}x{D}x{L}")
+
+
+def test_blelloch_schedule_workloads(sw):
+    """The paper's schedule on the bare-scan workloads: int32 bit-identical to
+    the default schedule (the ring is exact), fp32 within the gate."""
+    w = wl.workload("affine_f32_b1_d64_l1024")
+    inp = w.inputs()
+    h = sw.affine_scan_schedule(dev(inp["a"]), dev(inp["bx"]), schedule="blelloch").cpu().numpy()
+    ref, mag, sens = oracle.affine_scan(inp["a"], inp["bx"], bounds=True)
+    assert_gate(fp_gate(h, ref, mag, sens), w.name)
+    for variant in ("uniform", "odd", "h0"):
+        ii = wl.affine_inputs_i32(1, 64, 1024, wl.INT_SEEDS[variant], variant)
+        args = (dev(ii["a"]), dev(ii["bx"]), None if ii["h0"] is None else dev(ii["h0"]))
+        assert torch.equal(sw.affine_scan_schedule_i32(*args, schedule="blelloch"),
+                           sw.affine_scan_i32(*args))
+    w = wl.workload("affine_f32_b1_d5120_l65536")
+    inp = w.inputs()
+    h = sw.affine_scan_schedule(dev(inp["a"]), dev(inp["bx"]), schedule="blelloch")
+    rows = _sample_rows(w.B * w.D, 32, 99)
+    got = h.reshape(-1, w.L)[torch.from_numpy(rows).to("cuda")].cpu().numpy()
+    ref, mag, sens = oracle.affine_scan(inp["a"].reshape(-1, w.L)[rows],
+                                        inp["bx"].reshape(-1, w.L)[rows], bounds=True)
+    assert_gate(fp_gate(got, ref, mag, sens), w.name + " blelloch")

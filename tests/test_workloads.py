@@ -58,4 +58,7 @@ def test_workload_table():
     w = wl.workload("selective_bf16_b8_d1536_n16_l2048")
     assert (w.B, w.D, w.N, w.L, w.dtype) == (8, 1536, 16, 2048, "bf16")
     assert w.elems == 8 * 1536 * 16 * 2048
-    assert len(wl.WORKLOADS) == 6
+    # six configurations of the target workload, two shapes of the schedule ablation
+    assert len(wl.WORKLOADS) == 8
+    assert {k for k in wl.WORKLOADS if "ablation" in wl.WORKLOADS[k].note} == {
+        "affine_f32_b1_d64_l65536", "affine_f32_b8_d1536_l2048"}

@@ -158,6 +158,10 @@ WORKLOADS = {
                  note="bare affine scan, fp32 (int32 variants use seeds 11, 12, 13)"),
         Workload("affine_f32_b1_d5120_l65536", "affine", 1, 5120, 65536, 1, "f32", 6,
                  note="bare affine scan at the long-sequence shape (bandwidth figure)"),
+        Workload("affine_f32_b1_d64_l65536", "affine", 1, 64, 65536, 1, "f32", 7,
+                 note="bare affine scan, few rows and a long sequence (schedule ablation)"),
+        Workload("affine_f32_b8_d1536_l2048", "affine", 8, 1536, 2048, 1, "f32", 8,
+                 note="bare affine scan at the Mamba-130M-like (b,d,t) shape (schedule ablation)"),
         Workload("selective_f32_b2_d256_n16_l512", "selective", 2, 256, 512, 16, "f32", 2,
                  note="Mamba-style selective scan, fp32"),
         Workload("selective_bf16_b8_d1536_n16_l2048", "selective", 8, 1536, 2048, 16, "bf16",
