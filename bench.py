@@ -343,8 +343,12 @@ def main(argv=None):
 
     def step(i):
         s = sets[i % nsets]
-        sw.selective_scan_fwd(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"], s["Dskip"],
-                              y=s["y"], h_last=s["h"])
+        if args.schedule == "default":
+            sw.selective_scan_fwd(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"], s["Dskip"],
+                                  y=s["y"], h_last=s["h"])
+        else:
+            sw.selective_scan_fwd_schedule(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"],
+                                           s["Dskip"], schedule=args.schedule)
 
     for i in range(args.warmup):
         step(i)
@@ -384,7 +388,7 @@ def main(argv=None):
         "config": {
             "workload": w.name, "B": w.B, "D": w.D, "N": w.N, "L": w.L,
             "inputs": ("bf16 x/delta/Bm/Cm, fp32 A/Dskip" if w.dtype == "bf16" else "fp32"),
-            "state_and_output": "fp32", "input_sets_rotated": nsets,
+            "state_and_output": "fp32", "input_sets_rotated": nsets, "schedule": args.schedule,
         },
         "roofline": {
             "bound": "alu",
@@ -392,8 +396,9 @@ def main(argv=None):
             "peak": VALU_PEAK / 1e12,
             "unit": "T fp32-lane-slot/s",
             "frac": alu_achieved / VALU_PEAK,
-            "traffic": measured_traffic(w),
-            "kernel": ("selective_row16_kernel" if w.N == 16 else "selective_fwd_kernel"),
+            "traffic": measured_traffic(w) if args.schedule == "default" else None,
+            "kernel": ("selective_blelloch_kernel" if args.schedule == "blelloch" else
+                       "selective_row16_kernel" if w.N == 16 else "selective_fwd_kernel"),
             "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
                               "median": float(np.median(per)) * 1e6},
             "slots_per_elem": SLOTS_PER_ELEM,

@@ -103,6 +103,22 @@ int sw_affine_scan_schedule_i32(const int32_t* a, const int32_t* bx, const int32
                                 int32_t* h_out, int64_t B, int64_t D, int64_t L, int schedule);
 
 /*
+ * The fused selective scan (plain form: fp32 y, zero initial state, no
+ * options) with an explicit schedule.  SW_SCHED_DEFAULT is
+ * sw_selective_scan_fwd / _bf16 (in_dtype F32 / BF16).  SW_SCHED_BLELLOCH
+ * scans every (b,d,n) recurrence over t with the paper's Blelloch tree in LDS
+ * (2048-step chunks, one workgroup per row looping over the states,
+ * y accumulated in registers), for comparing schedules on the method's own
+ * workload.  Arguments, layouts, results (within fp32 rounding) and errors
+ * as for sw_selective_scan_fwd, plus SW_ERR_INVALID_ARG for an unknown dtype
+ * or schedule.
+ */
+int sw_selective_scan_fwd_schedule(const void* x, const void* delta, const float* A,
+                                   const void* Bm, const void* Cm, const float* Dskip, float* y,
+                                   float* h_last, int64_t B, int64_t D, int64_t N, int64_t L,
+                                   int in_dtype, int schedule);
+
+/*
  * Recurrence with input and output projections, elementwise (Eq. (3)-(4)):
  *   h[b,d,t] = a[b,d,t] * h[b,d,t-1] + b[b,d,t] * x[b,d,t]      (h[b,d,-1] = h0)
  *   y[b,d,t] = c[b,d,t] * h[b,d,t]

@@ -21,7 +21,8 @@ from ._lib import ScanWeaverError, check, last_error, lib, status_string  # noqa
 
 __all__ = ["affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
            "affine_scan_proj", "affine_scan_proj_i32",
-           "selective_scan_fwd", "selective_scan_bwd", "ScanWeaverError",
+           "selective_scan_fwd", "selective_scan_fwd_schedule", "selective_scan_bwd",
+           "ScanWeaverError",
            "version"]
 
 
@@ -198,6 +199,39 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
                 _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
                 _ptr(delta_bias), _ptr(h0), _ptr(y), _ptr(h_last), B, D, N, L, in_dt, out_dt,
                 flags), "sw_selective_scan_fwd_ex")
+    return y, h_last
+
+
+def selective_scan_fwd_schedule(x, delta, A, Bm, Cm, Dskip=None, *, schedule="default",
+                                want_h_last=True):
+    """The plain fused forward (fp32 y) with an explicit scan schedule
+    ("default" or "blelloch", the paper's tree); returns ``(y, h_last)``."""
+    if not isinstance(x, torch.Tensor) or x.dim() != 3:
+        raise ValueError("x must be a (B, D, L) tensor")
+    dt = x.dtype
+    if dt not in (torch.float32, torch.bfloat16):
+        raise TypeError("x must be float32 or bfloat16")
+    B, D, L = x.shape
+    _need(x, "x", dt)
+    _need(delta, "delta", dt, (B, D, L))
+    _need(A, "A", torch.float32)
+    if A.dim() != 2 or A.shape[0] != D:
+        raise ValueError("A must have shape (D, N)")
+    N = A.shape[1]
+    _need(Bm, "Bm", dt, (B, L, N))
+    _need(Cm, "Cm", dt, (B, L, N))
+    if Dskip is not None:
+        _need(Dskip, "Dskip", torch.float32, (D,))
+    y = torch.empty((B, D, L), dtype=torch.float32, device=x.device)
+    h_last = torch.empty((B, D, N), dtype=torch.float32, device=x.device) if want_h_last else None
+    from ._lib import SW_DTYPE_BF16, SW_DTYPE_F32
+    in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
+    with torch.cuda.device(x.device):
+        _bind_stream(x.device)
+        check(lib().sw_selective_scan_fwd_schedule(
+            _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(y),
+            _ptr(h_last), B, D, N, L, in_dt, _SCHEDULES[schedule]),
+            "sw_selective_scan_fwd_schedule")
     return y, h_last
 
 

@@ -224,7 +224,7 @@ int selective_common(SelArgs a) {
                 {a.h0, (size_t)nh * 4, "h0"}};
   if ((st = check_spans(outs, 2, ins, 9)) != SW_OK) return st;
   a.vec = L % 4 == 0 && all_aligned16({a.x, a.delta, a.y, a.z});
-  return selective_fwd(a);
+  return a.blelloch ? selective_blelloch_fwd(a) : selective_fwd(a);
 }
 
 // Validation of the backward entry point; see include/scanweaver.h.
@@ -483,6 +483,20 @@ SW_API int sw_affine_scan_schedule_i32(const int32_t* a, const int32_t* bx, cons
                                      reinterpret_cast<const uint32_t*>(h0),
                                      reinterpret_cast<uint32_t*>(h_out), B, D, L,
                                      sw::affine_blelloch_u32);
+}
+
+SW_API int sw_selective_scan_fwd_schedule(const void* x, const void* delta, const float* A,
+                                          const void* Bm, const void* Cm, const float* Dskip,
+                                          float* y, float* h_last, int64_t B, int64_t D, int64_t N,
+                                          int64_t L, int in_dtype, int schedule) {
+  if (in_dtype != SW_DTYPE_F32 && in_dtype != SW_DTYPE_BF16)
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown dtype %d", in_dtype);
+  if (schedule != SW_SCHED_DEFAULT && schedule != SW_SCHED_BLELLOCH)
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown schedule %d", schedule);
+  sw::SelArgs a = sw::sel_args(x, delta, A, Bm, Cm, Dskip, y, h_last, B, D, N, L,
+                               in_dtype == SW_DTYPE_BF16);
+  a.blelloch = schedule == SW_SCHED_BLELLOCH;
+  return sw::selective_common(a);
 }
 
 SW_API int sw_affine_scan_proj(const float* a, const float* b, const float* x, const float* c,

@@ -63,8 +63,10 @@ struct SelArgs {
   float* h_last;
   int64_t B, D, N, L;
   bool bf16_in, y_bf16, softplus, vec;
+  bool blelloch = false;  // the paper's schedule (plain form only)
 };
 int selective_fwd(const SelArgs& a);
+int selective_blelloch_fwd(const SelArgs& a);
 
 // Arguments of one backward call of the fused form, already validated.
 // x, delta, Bm, Cm, z are fp32 or bf16 as `bf16_in` says, dy as `dy_bf16`

@@ -583,3 +583,37 @@ def test_blelloch_schedule_workloads(sw):
     ref, mag, sens = oracle.affine_scan(inp["a"].reshape(-1, w.L)[rows],
                                         inp["bx"].reshape(-1, w.L)[rows], bounds=True)
     assert_gate(fp_gate(got, ref, mag, sens), w.name + " blelloch")
+
+
+@pytest.mark.parametrize("B,D,N,L", [(1, 3, 16, 37), (2, 5, 16, 2048), (1, 2, 5, 2049),
+                                     (2, 3, 64, 100), (1, 2, 16, 5000)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_selective_blelloch_schedule(sw, B, D, N, L, dtype):
+    """The fused form with the paper's schedule against the oracle."""
+    _say("case selective blelloch", dtype, B, D, N, L)
+    inp = wl.selective_inputs(B, D, N, L, 7300 + N + L, dtype)
+    if dtype == "bf16":
+        args = (bf16_dev(inp["x_bf16"]), bf16_dev(inp["delta_bf16"]), dev(inp["A"]),
+                bf16_dev(inp["Bm_bf16"]), bf16_dev(inp["Cm_bf16"]), dev(inp["Dskip"]))
+    else:
+        args = tuple(dev(inp[k]) for k in ("x", "delta", "A", "Bm", "Cm", "Dskip"))
+    y, hl = sw.selective_scan_fwd_schedule(*args, schedule="blelloch")
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                              inp["Dskip"], bounds=True)
+    assert_gate(fp_gate(y.cpu().numpy(), o["y"], o["y_mag"], o["y_sens"]), "blelloch y")
+    assert_gate(fp_gate(hl.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]), "blelloch h_last")
+
+
+def test_selective_blelloch_schedule_full_size(sw):
+    w = wl.workload("selective_bf16_b8_d1536_n16_l2048")
+    _say("case selective blelloch full size")
+    inp = w.inputs()
+    y, _ = sw.selective_scan_fwd_schedule(
+        bf16_dev(inp["x_bf16"]), bf16_dev(inp["delta_bf16"]), dev(inp["A"]),
+        bf16_dev(inp["Bm_bf16"]), bf16_dev(inp["Cm_bf16"]), dev(inp["Dskip"]),
+        schedule="blelloch", want_h_last=False)
+    rows = _sample_rows(w.B * w.D, 96, 71)
+    got = y.reshape(-1, w.L)[torch.as_tensor(rows, device="cuda")].cpu().numpy()
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                              inp["Dskip"], rows=rows, bounds=True)
+    assert_gate(fp_gate(got, o["y"], o["y_mag"], o["y_sens"]), "blelloch full size")
