@@ -237,8 +237,16 @@ def bench_bwd(w, args):
     t = {k: to_dev(k) for k in ("x", "delta", "A", "Bm", "Cm", "Dskip")}
     del inp
 
+    ck = None
+    if args.ckpt:
+        # the forward's checkpoints, as a training step would hand them over
+        ck = sw.new_ckpt(t["x"], w.N)
+        sw.selective_scan_fwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], ckpt=ck)
+        torch.cuda.synchronize()
+
     def step(i):
-        sw.selective_scan_bwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], dy_t)
+        sw.selective_scan_bwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], dy_t,
+                              ckpt=ck)
 
     wall, per = time_launches(step, args.steps, args.warmup)
     kern = float(per.mean())
@@ -255,7 +263,8 @@ def bench_bwd(w, args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "D": w.D, "N": w.N, "L": w.L,
-                   "pass": "backward", "dy": w.dtype, "gradients": "fp32"},
+                   "pass": "backward", "dy": w.dtype, "gradients": "fp32",
+                   "forward_checkpoints": bool(args.ckpt)},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                      "unit": "T fp32-lane-slot/s", "frac": achieved / VALU_PEAK,
                      "traffic": None, "kernel": "selective_bwd_kernel + selective_bwd_reduce_kernel",
@@ -280,6 +289,8 @@ def main(argv=None):
                     help="time the forward (default, the headline metric) or the backward")
     ap.add_argument("--schedule", choices=("default", "blelloch"), default="default",
                     help="scan schedule of the bare-scan workloads (schedule ablation)")
+    ap.add_argument("--ckpt", action="store_true",
+                    help="backward: take the forward's 8-step checkpoints (training mode)")
     ap.add_argument("--sets", type=int, default=0,
                     help="input sets rotated through (default: enough to exceed the MALL)")
     ap.add_argument("--print-kernel-sha", action="store_true",

@@ -219,6 +219,21 @@ int sw_selective_scan_fwd_ex(const void* x, const void* delta, const float* A, c
                              int out_dtype, int flags);
 
 /*
+ * sw_selective_scan_fwd_ex that also keeps what the backward pass needs
+ * (training): ckpt (B, D, ceil(L/8), 16) fp32, required, receives the state
+ * h[b,d,8k-1,n] before step 8k (h0, or zero, for k = 0) in slot
+ * [b, d, k, n]; slots n >= N hold no state.  N <= 16 (SW_ERR_UNSUPPORTED
+ * above).  Handing ckpt to sw_selective_scan_bwd with the same inputs spares
+ * the backward its own forward sweep.  Otherwise as
+ * sw_selective_scan_fwd_ex.
+ */
+int sw_selective_scan_fwd_train(const void* x, const void* delta, const float* A, const void* Bm,
+                                const void* Cm, const float* Dskip, const void* z,
+                                const float* delta_bias, const float* h0, void* y, float* h_last,
+                                float* ckpt, int64_t B, int64_t D, int64_t N, int64_t L,
+                                int in_dtype, int out_dtype, int flags);
+
+/*
  * Backward of sw_selective_scan_fwd_ex: the gradients of
  *   sum_{b,d,t} dy[b,d,t] y[b,d,t] + sum_{b,d,n} dh_last[b,d,n] h_last[b,d,n]
  * with respect to every input, by the chain rule through Eq. (3).  The
@@ -231,6 +246,8 @@ int sw_selective_scan_fwd_ex(const void* x, const void* delta, const float* A, c
  * Inputs: as for sw_selective_scan_fwd_ex (same dtypes, same flags), plus
  *   dy      : (B, D, L) of dy_dtype (fp32 or bf16), required
  *   dh_last : (B, D, N) fp32 or NULL (zero)
+ *   ckpt    : the ckpt of sw_selective_scan_fwd_train on the same inputs,
+ *             or NULL (the backward then rebuilds it in its workspace)
  * Outputs (fp32, overwritten, never accumulated into):
  *   dx, ddelta : (B, D, L), required; ddelta is with respect to the delta
  *                passed in (before bias and softplus)
@@ -243,14 +260,15 @@ int sw_selective_scan_fwd_ex(const void* x, const void* delta, const float* A, c
  * With L == 0 (or B*D == 0) the sums are zero and dh0 = dh_last.
  * Results are deterministic: cross-row sums are added in a fixed order.
  * Supports N <= 16 (SW_ERR_UNSUPPORTED above).  A workspace of about
- * (B*D*L*8 + B*ceil(D/16)*L*128 + B*D*L*4 if z) bytes is taken from the
+ * (B*D*L*8 without ckpt + B*ceil(D/16)*L*128 + B*D*L*4 if z) bytes is taken from the
  * device's stream-ordered pool for the call.  Other conventions (and
  * errors) as for sw_selective_scan_fwd_ex.
  */
 int sw_selective_scan_bwd(const void* x, const void* delta, const float* A, const void* Bm,
                           const void* Cm, const float* Dskip, const void* z,
                           const float* delta_bias, const float* h0, const void* dy,
-                          const float* dh_last, float* dx, float* ddelta, float* dA, float* dB,
+                          const float* dh_last, const float* ckpt, float* dx, float* ddelta,
+                          float* dA, float* dB,
                           float* dC, float* dDskip, float* dz, float* ddelta_bias, float* dh0,
                           int64_t B, int64_t D, int64_t N, int64_t L, int in_dtype, int dy_dtype,
                           int flags);

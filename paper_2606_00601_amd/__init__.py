@@ -21,7 +21,7 @@ from ._lib import ScanWeaverError, check, last_error, lib, status_string  # noqa
 
 __all__ = ["affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
            "affine_scan_proj", "affine_scan_proj_i32",
-           "selective_scan_fwd", "selective_scan_fwd_schedule", "selective_scan_bwd",
+           "selective_scan_fwd", "selective_scan_fwd_schedule", "selective_scan_bwd", "new_ckpt",
            "ScanWeaverError",
            "version"]
 
@@ -135,7 +135,7 @@ def affine_scan_proj_i32(a, b, x=None, c=None, h0=None, *, y=None, want_h_last=T
 
 def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
                        want_h_last=True, z=None, delta_bias=None, h0=None,
-                       delta_softplus=False, y_dtype=torch.float32):
+                       delta_softplus=False, y_dtype=torch.float32, ckpt=None):
     """Fused selective scan forward; returns ``(y, h_last)`` (h_last None if not wanted).
 
     x, delta: (B, D, L); A: (D, N) fp32; Bm, Cm: (B, L, N); Dskip: (D,) fp32 or None.
@@ -184,9 +184,16 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
     in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
     out_dt = SW_DTYPE_F32 if y_dtype == torch.float32 else SW_DTYPE_BF16
     flags = SW_DELTA_SOFTPLUS if delta_softplus else 0
+    if ckpt is not None:
+        _need(ckpt, "ckpt", torch.float32, (B, D, (L + 7) // 8, 16))
     with torch.cuda.device(x.device):
         _bind_stream(x.device)
-        if z is None and delta_bias is None and h0 is None and not flags \
+        if ckpt is not None:
+            check(lib().sw_selective_scan_fwd_train(
+                _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
+                _ptr(delta_bias), _ptr(h0), _ptr(y), _ptr(h_last), _ptr(ckpt), B, D, N, L,
+                in_dt, out_dt, flags), "sw_selective_scan_fwd_train")
+        elif z is None and delta_bias is None and h0 is None and not flags \
                 and out_dt == SW_DTYPE_F32:
             fn = lib().sw_selective_scan_fwd if dt == torch.float32 \
                 else lib().sw_selective_scan_fwd_bf16
@@ -235,8 +242,15 @@ def selective_scan_fwd_schedule(x, delta, A, Bm, Cm, Dskip=None, *, schedule="de
     return y, h_last
 
 
+def new_ckpt(x, N):
+    """An empty checkpoint buffer for :func:`selective_scan_fwd` (``ckpt=``)
+    and :func:`selective_scan_bwd`: (B, D, ceil(L/8), 16) fp32."""
+    B, D, L = x.shape
+    return torch.empty((B, D, (L + 7) // 8, 16), dtype=torch.float32, device=x.device)
+
+
 def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, delta_bias=None,
-                       h0=None, delta_softplus=False, want_dh0=True):
+                       h0=None, delta_softplus=False, want_dh0=True, ckpt=None):
     """Backward of :func:`selective_scan_fwd`: gradients of sum(dy * y) +
     sum(dh_last * h_last) with respect to every input.
 
@@ -273,6 +287,8 @@ def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, 
     _need(dy, "dy", dy.dtype, (B, D, L))
     if dh_last is not None:
         _need(dh_last, "dh_last", torch.float32, (B, D, N))
+    if ckpt is not None:
+        _need(ckpt, "ckpt", torch.float32, (B, D, (L + 7) // 8, 16))
     dev = x.device
     f32 = dict(dtype=torch.float32, device=dev)
     out = {"dx": torch.empty((B, D, L), **f32), "ddelta": torch.empty((B, D, L), **f32),
@@ -289,7 +305,7 @@ def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, 
         _bind_stream(dev)
         check(lib().sw_selective_scan_bwd(
             _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
-            _ptr(delta_bias), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(out["dx"]),
+            _ptr(delta_bias), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(ckpt), _ptr(out["dx"]),
             _ptr(out["ddelta"]), _ptr(out["dA"]), _ptr(out["dB"]), _ptr(out["dC"]),
             _ptr(out["dDskip"]), _ptr(out["dz"]), _ptr(out["ddelta_bias"]), _ptr(out["dh0"]),
             B, D, N, L, in_dt, dy_dt, SW_DELTA_SOFTPLUS if delta_softplus else 0),

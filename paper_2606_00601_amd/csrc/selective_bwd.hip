@@ -188,15 +188,16 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   // tiles ahead of their use.
   Raw ring[BW_RING];
 
-  // --- 1. forward sweep: checkpoints ---------------------------------------
+  // --- 1. forward sweep: checkpoints (unless the forward pass supplied them)
   float h = (a.h0 && dok && nok) ? a.h0[row * N + n] : 0.0f;
+  const int64_t ntile1 = a.ckpt ? 0 : ntile;
 #pragma unroll
   for (int u = 0; u < BW_RING - 1; ++u) load_tile(u, ring[u]);
-  for (int64_t k0 = 0; k0 < ntile; k0 += BW_RING) {
+  for (int64_t k0 = 0; k0 < ntile1; k0 += BW_RING) {
 #pragma unroll
     for (int u = 0; u < BW_RING; ++u) {
       const int64_t k = k0 + u;
-      if (k >= ntile) break;
+      if (k >= ntile1) break;
       const int buf = u & 1;  // BW_RING is even, so this is k & 1
       Raw& cur = ring[u];
       if (role_a) {
@@ -492,7 +493,8 @@ int selective_bwd(const BwdArgs& a) {
   if (grid >= ((int64_t)1 << 31))
     return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
   const size_t R = (size_t)(B * D);
-  const size_t n_ck = R * (size_t)ntile * BW_N, n_s = a.z ? R * (size_t)L : 0;
+  // without the forward's checkpoints the kernel rebuilds them in a workspace
+  const size_t n_ck = a.ckpt ? 0 : R * (size_t)ntile * BW_N, n_s = a.z ? R * (size_t)L : 0;
   const size_t n_dA = R * BW_N, n_bc = (size_t)(B * G) * (size_t)L * BW_N;
   const size_t total = n_ck + n_s + n_dA + 2 * R + 2 * n_bc + 256;
   void* base = nullptr;
@@ -500,7 +502,7 @@ int selective_bwd(const BwdArgs& a) {
   if (st != SW_OK) return st;
   float* f = static_cast<float*>(base);
   BwWork w;
-  w.ck = f;
+  w.ck = a.ckpt ? const_cast<float*>(a.ckpt) : f;  // read-only when given
   f += n_ck;
   float* s_pre = a.z ? f : nullptr;
   w.s = s_pre;

@@ -241,7 +241,9 @@ __device__ __forceinline__ void compute_blk(const Blk<NPL>& k, const float (&Al)
 
 // OPT: the optional Mamba-block inputs (flags, z, delta bias) are read;
 // without it the kernel is the plain form (an initial state is always taken).
-template <typename IN, int NPL, bool VEC, bool NPADDED, bool OPT>
+// CK (with OPT, N <= 16): the state at every 8-step boundary goes to ck,
+// laid out as (B*D, nT8, 16), for the backward pass.
+template <typename IN, int NPL, bool VEC, bool NPADDED, bool OPT, bool CK>
 __global__ __launch_bounds__(64) void selective_fwd_kernel(
     const IN* __restrict__ x, const IN* __restrict__ delta, const float* __restrict__ A,
     const IN* __restrict__ Bm, const IN* __restrict__ Cm, const float* __restrict__ Dskip,
@@ -249,7 +251,8 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
     void* __restrict__ yv, float* __restrict__ h_last, int64_t D, int N, int64_t L, int64_t ndb,
     int64_t nrb, int64_t Lc, int64_t nchunks, uint32_t ntasks,
     unsigned long long* __restrict__ carry, uint32_t* __restrict__ ticket, uint32_t tbase,
-    uint32_t epoch, uint32_t flags_in) {
+    uint32_t epoch, uint32_t flags_in, float* __restrict__ ck, int64_t nT8) {
+  static_assert(!CK || NPL <= 2, "checkpoints hold 16 states per row");
   constexpr int T = SS_T;
   const uint32_t flags = OPT ? flags_in : 0u;
   constexpr int TS = SS_TS;
@@ -474,6 +477,16 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
         // keep the read-ahead where it is: the scheduler would otherwise sink
         // the reads next to their use and expose the LDS latency
         __builtin_amdgcn_sched_barrier(0);
+        if constexpr (CK) {
+          // the state before step tb + kt*T + 4*bi (states past N and rows
+          // past D write to their own unused slots / row D-1's, same values)
+          const int64_t t8 = (tb + (int64_t)kt * T + 4 * bi) / 8;
+          if ((bi & 1) == 0 && t8 < nT8) {
+#pragma unroll
+            for (int j = 0; j < NPL; ++j)
+              ck[((b * D + dcl) * nT8 + t8) * 16 + g * NPL + j] = hs[j];
+          }
+        }
         compute_blk(ops[bi % NS], Al, hs, p_w + 4 * bi);
         if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, ydp, gtp);
         __builtin_amdgcn_sched_barrier(0);
@@ -568,7 +581,7 @@ int make_plan(int64_t B, int64_t D, int64_t L, Plan* p) {
 
 template <typename IN, int NPL, bool VEC, bool NPADDED>
 int launch_cfg(const SelArgs& a, hipStream_t s) {
-  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16;
+  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.ckpt;
   Plan p;
   int st = make_plan(a.B, a.D, a.L, &p);
   if (st != SW_OK) return st;
@@ -578,13 +591,19 @@ int launch_cfg(const SelArgs& a, hipStream_t s) {
   if (st != SW_OK) return st;
   const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.y_bf16 ? SEL_Y_BF16 : 0u) |
                          (a.z ? SEL_GATED : 0u);
-  auto kern = opt ? selective_fwd_kernel<IN, NPL, VEC, NPADDED, true>
-                  : selective_fwd_kernel<IN, NPL, VEC, NPADDED, false>;
+  auto kern = opt ? selective_fwd_kernel<IN, NPL, VEC, NPADDED, true, false>
+                  : selective_fwd_kernel<IN, NPL, VEC, NPADDED, false, false>;
+  if constexpr (NPL <= 2) {
+    if (a.ckpt) kern = selective_fwd_kernel<IN, NPL, VEC, NPADDED, true, true>;
+  } else {
+    if (a.ckpt) return fail(SW_ERR_UNSUPPORTED, "checkpoints need N <= 16");
+  }
   hipLaunchKernelGGL(kern, dim3((unsigned)p.grid), dim3(64), 0, s, static_cast<const IN*>(a.x),
                      static_cast<const IN*>(a.delta), a.A, static_cast<const IN*>(a.Bm),
                      static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
                      a.delta_bias, a.h0, a.y, a.h_last, a.D, (int)a.N, a.L, p.ndb, p.nrb, p.Lc,
-                     p.nchunks, p.ntasks, ss.carry, ss.ticket, ss.ticket_base, ss.epoch, flags);
+                     p.nchunks, p.ntasks, ss.carry, ss.ticket, ss.ticket_base, ss.epoch, flags,
+                     a.ckpt, (a.L + 7) / 8);
   st = check_launch("selective_fwd_kernel");
   if (st != SW_OK) ss.invalidate();
   return st;

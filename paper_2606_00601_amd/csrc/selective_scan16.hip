@@ -93,13 +93,15 @@ struct R16Ops {
 
 // OPT: the optional Mamba-block inputs (flags, z, delta bias) are read;
 // without it the kernel is the plain form (an initial state is always taken).
-template <typename IN, bool OPT>
+// CK (with OPT): the state at every 8-step boundary goes to ck, laid out as
+// (B*D, nT8, 16), for the backward pass.
+template <typename IN, bool OPT, bool CK>
 __global__ __launch_bounds__(256) void selective_row16_kernel(
     const IN* __restrict__ x, const IN* __restrict__ delta, const float* __restrict__ A,
     const IN* __restrict__ Bm, const IN* __restrict__ Cm, const float* __restrict__ Dskip,
     const IN* __restrict__ z, const float* __restrict__ dbias, const float* __restrict__ h0,
     void* __restrict__ yv, float* __restrict__ h_last, int64_t D, int64_t L, int64_t ndb,
-    uint32_t flags_in) {
+    uint32_t flags_in, float* __restrict__ ck, int64_t nT8) {
   constexpr int ES = (int)sizeof(IN);
   const uint32_t flags = OPT ? flags_in : 0u;
   constexpr int V = 16 / ES;              // steps a lane holds of a super-tile
@@ -273,6 +275,12 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
       else if (has_next)
         read_ops(ops[nb % R16_NS], nbuf, nb - R16_NB);
       __builtin_amdgcn_sched_barrier(0);
+      if constexpr (CK) {
+        // the state before step kt*T + 4*bi; rows past D write the same
+        // values as row D-1 to row D-1's slots
+        const int64_t t8 = (kt * R16_T + 4 * bi) / 8;
+        if ((bi & 1) == 0 && t8 < nT8) ck[((b * D + dcl) * nT8 + t8) * R16_N + n] = h;
+      }
       const R16Ops& o = ops[bi % R16_NS];
       const float bq[4] = {o.b.x, o.b.y, o.b.z, o.b.w};
       const float cq[4] = {o.c.x, o.c.y, o.c.z, o.c.w};
@@ -357,18 +365,21 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
 
 template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s) {
-  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16;
+  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.ckpt;
   const int64_t ndb = (a.D + R16_ROWS - 1) / R16_ROWS;
   const int64_t grid = a.B * ndb;
   if (grid >= ((int64_t)1 << 31))
     return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
   const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.y_bf16 ? SEL_Y_BF16 : 0u) |
                          (a.z ? SEL_GATED : 0u);
-  auto kern = opt ? selective_row16_kernel<IN, true> : selective_row16_kernel<IN, false>;
+  auto kern = a.ckpt ? selective_row16_kernel<IN, true, true>
+              : opt    ? selective_row16_kernel<IN, true, false>
+                       : selective_row16_kernel<IN, false, false>;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, static_cast<const IN*>(a.x),
                      static_cast<const IN*>(a.delta), a.A, static_cast<const IN*>(a.Bm),
                      static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
-                     a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L, ndb, flags);
+                     a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L, ndb, flags, a.ckpt,
+                     (a.L + 7) / 8);
   return check_launch("selective_row16_kernel");
 }
 

@@ -187,3 +187,66 @@ def test_bwd_full_size_sampled(sw):
         mag = o2["m_" + k + "_rows"].reshape(w.B, len(ds_)).sum(0)
         got = g[k][torch.as_tensor(ds_, device="cuda")].cpu().numpy()
         assert_gate(fp_gate(got, ref, mag), f"full-size {k}")
+
+
+# ------------------------------------------- checkpoints handed over by the forward
+
+@pytest.mark.parametrize("shape,layout", [((2, 37, 16, 203), "8"), ((2, 21, 16, 512), "16"),
+                                          ((1, 9, 5, 96), "8")])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_forward_checkpoints_and_backward_with_them(sw, monkeypatch, shape, layout, dtype):
+    """The forward's training mode stores the state before every 8th step;
+    each slot matches the oracle's final state of the sequence cut there, and
+    the backward fed with them gives the oracle's gradients, bit-identical to
+    the backward that rebuilds them itself."""
+    monkeypatch.setenv("SW_SS_LAYOUT", layout)
+    B, D, N, L = shape
+    opts = ("z", "bias", "softplus", "h0", "dhl")
+    _say("case ckpt", dtype, shape, layout)
+    inp, ex = _inputs(B, D, N, L, 930 + L, dtype, opts)
+    if dtype == "bf16":
+        x, dl = _bf16_dev(inp["x_bf16"]), _bf16_dev(inp["delta_bf16"])
+        Bm, Cm = _bf16_dev(inp["Bm_bf16"]), _bf16_dev(inp["Cm_bf16"])
+        z = _bf16_dev(ex["z_bits"])
+    else:
+        x, dl, Bm, Cm = (_dev(inp[k]) for k in ("x", "delta", "Bm", "Cm"))
+        z = _dev(ex["z"])
+    kw = dict(z=z, delta_bias=_dev(ex["delta_bias"]), h0=_dev(ex["h0"]), delta_softplus=True)
+    ck = sw.new_ckpt(x, N)
+    y, hl = sw.selective_scan_fwd(x, dl, _dev(inp["A"]), Bm, Cm, _dev(inp["Dskip"]), ckpt=ck,
+                                  **kw)
+    torch.cuda.synchronize()
+    ckn = ck.cpu().numpy()
+    nt8 = (L + 7) // 8
+    for k in sorted({0, 1, nt8 // 2, nt8 - 1}):
+        if k == 0:
+            ref, mag, sens = ex["h0"], np.abs(ex["h0"]), np.zeros_like(ex["h0"])
+        else:
+            cut = lambda a: np.ascontiguousarray(a[..., :8 * k])  # noqa: E731
+            o = oracle.selective_scan(cut(inp["x"]), cut(inp["delta"]), inp["A"],
+                                      np.ascontiguousarray(inp["Bm"][:, :8 * k]),
+                                      np.ascontiguousarray(inp["Cm"][:, :8 * k]), inp["Dskip"],
+                                      bounds=True, z=cut(ex["z"]), delta_bias=ex["delta_bias"],
+                                      h0=ex["h0"], delta_softplus=True)
+            ref, mag, sens = o["h_last"], o["h_mag"], o["h_sens"]
+        assert_gate(fp_gate(ckn[:, :, k, :N], ref, mag, sens), f"ckpt slot {k}")
+    dy = _dev(ex["dy"])
+    dhl = _dev(ex["dh_last"])
+    args = (x, dl, _dev(inp["A"]), Bm, Cm, _dev(inp["Dskip"]), dy, dhl)
+    g1 = sw.selective_scan_bwd(*args, ckpt=ck, **kw)
+    g0 = sw.selective_scan_bwd(*args, **kw)
+    torch.cuda.synchronize()
+    o = _ref(inp, ex, opts)
+    _check_all(g1, o, f"bwd with ckpt {dtype} {shape}",
+               ["dx", "ddelta", "dA", "dB", "dC", "dDskip", "dz", "ddelta_bias", "dh0"])
+    for k in g0:
+        assert torch.equal(g0[k], g1[k]), k
+
+
+def test_forward_checkpoints_reject_large_N(sw):
+    from paper_2606_00601_amd import ScanWeaverError
+    x = torch.randn((1, 2, 8), device="cuda")
+    with pytest.raises(ScanWeaverError):
+        sw.selective_scan_fwd(x, x, torch.randn((2, 17), device="cuda"),
+                              torch.randn((1, 8, 17), device="cuda"),
+                              torch.randn((1, 8, 17), device="cuda"), ckpt=sw.new_ckpt(x, 17))
