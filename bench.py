@@ -161,18 +161,28 @@ def bench_affine(w, args):
     torch.cuda.set_device(dev)
     sw.lib()
     inp = w.inputs()
-    abytes = 12 * w.elems
+    proj = args.form == "proj"
+    # bare: a, bx read, h written; projection form (Eq. (3)-(4)): a, b, x, c
+    # read, y written, h_last written once per row
+    abytes = (20 if proj else 12) * w.elems + (4 * w.B * w.D if proj else 0)
     nsets = args.sets or max(1, min(4, int(np.ceil(2 * MALL_BYTES / abytes)) + 1))
+    if proj:
+        rng = np.random.Generator(np.random.PCG64(w.seed + 100))
+        xc = [rng.standard_normal(size=(w.B, w.D, w.L)).astype(np.float32) for _ in range(2)]
     sets = []
     for i in range(nsets):
         a = torch.from_numpy(inp["a"]).to(dev)
         bx = torch.from_numpy(inp["bx"]).to(dev)
-        sets.append((a, bx, torch.empty_like(a)))
+        extra = tuple(torch.from_numpy(v).to(dev) for v in xc) if proj else ()
+        sets.append((a, bx, torch.empty_like(a)) + extra)
     del inp
 
     def step(i):
-        a, bx, h = sets[i % nsets]
-        if args.schedule == "default":
+        st = sets[i % nsets]
+        a, bx, h = st[:3]
+        if proj:
+            sw.affine_scan_proj(a, bx, st[3], st[4], y=h)
+        elif args.schedule == "default":
             sw.affine_scan(a, bx, out=h)
         else:
             sw.affine_scan_schedule(a, bx, out=h, schedule=args.schedule)
@@ -187,14 +197,18 @@ def bench_affine(w, args):
              else "affine_scan_kernel")
     if args.schedule == "blelloch":
         kname = "affine_blelloch_kernel"
+    if proj:
+        kname += " (projection variant)"
     out = {
-        "metric": "affine-scan fwd B*L*D elems/s (+ achieved HBM GB/s vs peak), 1 GPU",
+        "metric": ("affine-scan fwd, projection form y = c*h, h = a*h + b*x, B*L*D elems/s "
+                   "(+ achieved HBM GB/s vs peak), 1 GPU" if proj else
+                   "affine-scan fwd B*L*D elems/s (+ achieved HBM GB/s vs peak), 1 GPU"),
         "value": w.elems * args.steps / wall, "unit": "elems/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "D": w.D, "L": w.L, "input_sets_rotated": nsets,
-                   "schedule": args.schedule},
+                   "schedule": args.schedule, "form": args.form},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS, "traffic": None, "kernel": kname,
                      "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
@@ -290,7 +304,13 @@ def main(argv=None):
     ap.add_argument("--schedule", choices=("default", "blelloch"), default="default",
                     help="scan schedule of the bare-scan workloads (schedule ablation)")
     ap.add_argument("--ckpt", action="store_true",
-                    help="backward: take the forward's 8-step checkpoints (training mode)")
+                    help="training mode: the forward writes 8-step checkpoints, the backward "
+                         "takes them")
+    ap.add_argument("--options", action="store_true",
+                    help="forward with the Mamba-block inputs (gate, delta bias + softplus, "
+                         "initial state, y in the input dtype)")
+    ap.add_argument("--form", choices=("bare", "proj"), default="bare",
+                    help="bare-scan workloads: the plain scan or the Eq. (3)-(4) projection form")
     ap.add_argument("--sets", type=int, default=0,
                     help="input sets rotated through (default: enough to exceed the MALL)")
     ap.add_argument("--print-kernel-sha", action="store_true",
@@ -335,6 +355,13 @@ def main(argv=None):
 
     inp = w.inputs()
     abytes = algorithmic_bytes(w)
+    es = 2 if w.dtype == "bf16" else 4
+    if args.options:
+        # + z read, h0 read, delta_bias read; y written in the input dtype
+        abytes += es * w.B * w.D * w.L + 4 * w.B * w.D * w.N + 4 * w.D
+        abytes -= (4 - es) * w.B * w.D * w.L
+    if args.ckpt:
+        abytes += 4 * w.B * w.D * ((w.L + 7) // 8) * 16  # the checkpoints written
     nsets = args.sets or max(2, int(np.ceil(2 * MALL_BYTES / abytes)) + 1)
     nsets = min(nsets, 8)
 
@@ -344,11 +371,31 @@ def main(argv=None):
         return torch.from_numpy(inp[k]).to(dev)
 
     base = {k: to_dev(k) for k in ("x", "delta", "A", "Bm", "Cm", "Dskip")}
+    opt = {}
+    y_dtype = torch.float32
+    if args.options:
+        # the Mamba-block inputs: gate z, delta bias with softplus, initial state,
+        # y in the input dtype
+        rng = np.random.Generator(np.random.PCG64(w.seed + 200))
+        z = rng.standard_normal(size=(w.B, w.D, w.L)).astype(np.float32)
+        if w.dtype == "bf16":
+            opt["z"] = torch.from_numpy(wl.bf16_round(z).view(np.int16)).to(dev).view(
+                torch.bfloat16)
+            y_dtype = torch.bfloat16
+        else:
+            opt["z"] = torch.from_numpy(z).to(dev)
+        opt["delta_bias"] = torch.from_numpy(
+            rng.uniform(-2.0, 0.0, size=w.D).astype(np.float32)).to(dev)
+        opt["h0"] = torch.from_numpy(
+            rng.standard_normal(size=(w.B, w.D, w.N)).astype(np.float32)).to(dev)
+        opt["delta_softplus"] = True
     sets = []
     for i in range(nsets):
         s = {k: (v if i == 0 else v.clone()) for k, v in base.items()}
-        s["y"] = torch.empty((w.B, w.D, w.L), dtype=torch.float32, device=dev)
+        s["y"] = torch.empty((w.B, w.D, w.L), dtype=y_dtype, device=dev)
         s["h"] = torch.empty((w.B, w.D, w.N), dtype=torch.float32, device=dev)
+        if args.ckpt:
+            s["ck"] = sw.new_ckpt(s["x"], w.N)
         sets.append(s)
     torch.cuda.synchronize()
 
@@ -356,7 +403,8 @@ def main(argv=None):
         s = sets[i % nsets]
         if args.schedule == "default":
             sw.selective_scan_fwd(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"], s["Dskip"],
-                                  y=s["y"], h_last=s["h"])
+                                  y=s["y"], h_last=s["h"], y_dtype=y_dtype, ckpt=s.get("ck"),
+                                  **opt)
         else:
             sw.selective_scan_fwd_schedule(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"],
                                            s["Dskip"], schedule=args.schedule)
@@ -399,7 +447,11 @@ def main(argv=None):
         "config": {
             "workload": w.name, "B": w.B, "D": w.D, "N": w.N, "L": w.L,
             "inputs": ("bf16 x/delta/Bm/Cm, fp32 A/Dskip" if w.dtype == "bf16" else "fp32"),
-            "state_and_output": "fp32", "input_sets_rotated": nsets, "schedule": args.schedule,
+            "state_and_output": "fp32" if y_dtype == torch.float32 else "fp32 state, bf16 y",
+            "input_sets_rotated": nsets, "schedule": args.schedule,
+            "options": ("gate z, delta bias + softplus, initial state" if args.options
+                        else "none"),
+            "forward_checkpoints": bool(args.ckpt),
         },
         "roofline": {
             "bound": "alu",
@@ -407,7 +459,8 @@ def main(argv=None):
             "peak": VALU_PEAK / 1e12,
             "unit": "T fp32-lane-slot/s",
             "frac": alu_achieved / VALU_PEAK,
-            "traffic": measured_traffic(w) if args.schedule == "default" else None,
+            "traffic": (measured_traffic(w) if args.schedule == "default" and not args.options
+                        and not args.ckpt else None),
             "kernel": ("selective_blelloch_kernel" if args.schedule == "blelloch" else
                        "selective_row16_kernel" if w.N == 16 else "selective_fwd_kernel"),
             "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,

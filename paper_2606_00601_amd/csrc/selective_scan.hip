@@ -241,7 +241,7 @@ __device__ __forceinline__ void compute_blk(const Blk<NPL>& k, const float (&Al)
 
 // OPT: the optional Mamba-block inputs (flags, z, delta bias) are read;
 // without it the kernel is the plain form (an initial state is always taken).
-// CK (with OPT, N <= 16): the state at every 8-step boundary goes to ck,
+// CK (N <= 16): the state at every 8-step boundary goes to ck,
 // laid out as (B*D, nT8, 16), for the backward pass.
 template <typename IN, int NPL, bool VEC, bool NPADDED, bool OPT, bool CK>
 __global__ __launch_bounds__(64) void selective_fwd_kernel(
@@ -581,7 +581,7 @@ int make_plan(int64_t B, int64_t D, int64_t L, Plan* p) {
 
 template <typename IN, int NPL, bool VEC, bool NPADDED>
 int launch_cfg(const SelArgs& a, hipStream_t s) {
-  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.ckpt;
+  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16;
   Plan p;
   int st = make_plan(a.B, a.D, a.L, &p);
   if (st != SW_OK) return st;
@@ -594,7 +594,9 @@ int launch_cfg(const SelArgs& a, hipStream_t s) {
   auto kern = opt ? selective_fwd_kernel<IN, NPL, VEC, NPADDED, true, false>
                   : selective_fwd_kernel<IN, NPL, VEC, NPADDED, false, false>;
   if constexpr (NPL <= 2) {
-    if (a.ckpt) kern = selective_fwd_kernel<IN, NPL, VEC, NPADDED, true, true>;
+    if (a.ckpt)
+      kern = opt ? selective_fwd_kernel<IN, NPL, VEC, NPADDED, true, true>
+                 : selective_fwd_kernel<IN, NPL, VEC, NPADDED, false, true>;
   } else {
     if (a.ckpt) return fail(SW_ERR_UNSUPPORTED, "checkpoints need N <= 16");
   }

@@ -93,7 +93,7 @@ struct R16Ops {
 
 // OPT: the optional Mamba-block inputs (flags, z, delta bias) are read;
 // without it the kernel is the plain form (an initial state is always taken).
-// CK (with OPT): the state at every 8-step boundary goes to ck, laid out as
+// CK: the state at every 8-step boundary goes to ck, laid out as
 // (B*D, nT8, 16), for the backward pass.
 template <typename IN, bool OPT, bool CK>
 __global__ __launch_bounds__(256) void selective_row16_kernel(
@@ -365,16 +365,17 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
 
 template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s) {
-  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.ckpt;
+  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16;
   const int64_t ndb = (a.D + R16_ROWS - 1) / R16_ROWS;
   const int64_t grid = a.B * ndb;
   if (grid >= ((int64_t)1 << 31))
     return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
   const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.y_bf16 ? SEL_Y_BF16 : 0u) |
                          (a.z ? SEL_GATED : 0u);
-  auto kern = a.ckpt ? selective_row16_kernel<IN, true, true>
-              : opt    ? selective_row16_kernel<IN, true, false>
-                       : selective_row16_kernel<IN, false, false>;
+  auto kern = opt ? (a.ckpt ? selective_row16_kernel<IN, true, true>
+                            : selective_row16_kernel<IN, true, false>)
+                  : (a.ckpt ? selective_row16_kernel<IN, false, true>
+                            : selective_row16_kernel<IN, false, false>);
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, static_cast<const IN*>(a.x),
                      static_cast<const IN*>(a.delta), a.A, static_cast<const IN*>(a.Bm),
                      static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
