@@ -259,7 +259,8 @@ int sw_selective_scan_fwd_train(const void* x, const void* delta, const float* A
  *                (h0, or the zero state when h0 is NULL)
  * With L == 0 (or B*D == 0) the sums are zero and dh0 = dh_last.
  * Results are deterministic: cross-row sums are added in a fixed order.
- * Supports N <= 16 (SW_ERR_UNSUPPORTED above).  A workspace of about
+ * N in [1, 64] (states above 16 run as further passes over the sequence,
+ * 16 states each); with ckpt, N <= 16.  A workspace of about
  * (B*D*L*8 without ckpt + B*ceil(D/16)*L*128 + B*D*L*4 if z) bytes is taken from the
  * device's stream-ordered pool for the call.  Other conventions (and
  * errors) as for sw_selective_scan_fwd_ex.

@@ -107,7 +107,7 @@ struct TileRaw {
 // waited for inside a branch.
 template <typename IN, typename DYT, bool GATED>
 __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, const BwWork w,
-                                                            int64_t G, int64_t ntile) {
+                                                            int64_t G, int64_t ntile, int n0) {
   __shared__ __align__(16) BwSmem sm;
   const IN* __restrict__ X = static_cast<const IN*>(a.x);
   const IN* __restrict__ DL = static_cast<const IN*>(a.delta);
@@ -127,7 +127,11 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   const int64_t d0 = g * BW_ROWS;
   const int64_t d = d0 + rr;
   const bool dok = d < D;
-  const bool nok = n < N;
+  // this launch's states are n0 .. n0+15 (groups of 16 for N > 16); the
+  // first group also adds the terms that do not depend on the state
+  const int ns = n0 + n;  // the lane's state
+  const bool nok = ns < N;
+  const bool first = n0 == 0;
   const int64_t row = b * D + (dok ? d : D - 1);
 
   // staging / reduce roles (by wavefront): waves 0-1 own (row sr, step st),
@@ -139,7 +143,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   const bool sdok = sd < D;
   const int64_t srow = b * D + (sdok ? sd : D - 1);
 
-  const float Ar = a.A[(dok ? d : D - 1) * N + (nok ? n : 0)] * (nok ? 1.0f : 0.0f);
+  const float Ar = a.A[(dok ? d : D - 1) * N + (nok ? ns : 0)] * (nok ? 1.0f : 0.0f);
   const float Al = Ar * BW_LOG2E;
   const float dbias = a.delta_bias ? a.delta_bias[sdok ? sd : D - 1] : 0.0f;
   const float Dsk = a.Dskip ? a.Dskip[sdok ? sd : D - 1] : 0.0f;
@@ -156,8 +160,8 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
     const int64_t ia = srow * L + tca;
     const int64_t tb = k * BW_T + bt;
     const int64_t tcb = tb < 0 ? 0 : (tb < L ? tb : L - 1);
-    const int64_t ib = (b * L + tcb) * N + (bn < N ? bn : N - 1);
-    v.ok = role_a ? (sdok && ta >= 0 && ta < L) : (tb >= 0 && tb < L && bn < N);
+    const int64_t ib = (b * L + tcb) * N + (n0 + bn < N ? n0 + bn : N - 1);
+    v.ok = role_a ? (sdok && ta >= 0 && ta < L) : (tb >= 0 && tb < L && n0 + bn < N);
     const int64_t i01 = role_a ? ia : ib;
     v.r0 = P0[i01];
     v.r1 = P1[i01];
@@ -189,7 +193,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   Raw ring[BW_RING];
 
   // --- 1. forward sweep: checkpoints (unless the forward pass supplied them)
-  float h = (a.h0 && dok && nok) ? a.h0[row * N + n] : 0.0f;
+  float h = (a.h0 && dok && nok) ? a.h0[row * N + ns] : 0.0f;
   const int64_t ntile1 = a.ckpt ? 0 : ntile;
 #pragma unroll
   for (int u = 0; u < BW_RING - 1; ++u) load_tile(u, ring[u]);
@@ -228,7 +232,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   bw_barrier();  // the reverse sweep restages the buffers of the last tiles
 
   // --- 2./3. reverse sweep ---------------------------------------------------
-  float lam = (a.dh_last && dok && nok) ? a.dh_last[row * N + n] : 0.0f;
+  float lam = (a.dh_last && dok && nok) ? a.dh_last[row * N + ns] : 0.0f;
   float dA_acc = 0.0f;
   float dD_acc = 0.0f, db_acc = 0.0f;  // role a: this thread's (row, step slot)
   float hring[BW_RING];
@@ -345,7 +349,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         }
         const float ddl = live ? (s1 + xv * s2) * sg : 0.0f;
         v0 = ddl;
-        v1 = __builtin_fmaf(dlv, s2, ds * Dsk);
+        v1 = __builtin_fmaf(dlv, s2, first ? ds * Dsk : 0.0f);
         const int64_t i = srow * L + (live ? k * BW_T + st : 0);
         p0 = live ? a.ddelta + i : w.trash + tid;
         p1 = live ? a.dx + i : w.trash + tid;
@@ -353,7 +357,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
           v2 = dyv * sv * gp;
           p2 = live ? a.dz + i : w.trash + tid;
         }
-        dD_acc = __builtin_fmaf(ds, xv, dD_acc);
+        if (first) dD_acc = __builtin_fmaf(ds, xv, dD_acc);
         db_acc += ddl;
       } else {
         float sb = 0.f, sc = 0.f;
@@ -369,14 +373,20 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         p0 = t < L ? w.dB_p + i : w.trash + tid;
         p1 = t < L ? w.dC_p + i : w.trash + tid;
       }
+      if (role_a && !first) {  // later state groups add to the sums over the states
+        v0 += *p0;
+        v1 += *p1;
+      }
       *p0 = v0;
       *p1 = v1;
-      if constexpr (GATED) *p2 = v2;
+      if constexpr (GATED) {
+        if (first) *p2 = v2;
+      }
     }
   }
 
   if (dok && nok) {
-    if (a.dh0) a.dh0[row * N + n] = lam;
+    if (a.dh0) a.dh0[row * N + ns] = lam;
     w.dA_p[row * BW_N + n] = dA_acc;
   }
   // per-row sums of the step slots (8 consecutive lanes of role a)
@@ -387,8 +397,12 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
       db_acc += __shfl_xor(db_acc, off);
     }
     if (st == 0 && sdok) {
-      w.dD_p[srow] = dD_acc;
-      w.db_p[srow] = db_acc;
+      if (first) {
+        w.dD_p[srow] = dD_acc;
+        w.db_p[srow] = db_acc;
+      } else {
+        w.db_p[srow] += db_acc;
+      }
     }
   }
 }
@@ -397,9 +411,14 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
 // (one thread per 4 states of one (b, t) and one of dB / dC, float4 loads,
 // eight in flight, summed in workgroup order); dA, dDskip, ddelta_bias over
 // the batch.
+// With state groups (N > 16) it runs after each group's main kernel and
+// writes that group's states n0 .. n0+15; dDskip and ddelta_bias after the
+// last group (last = true).
 __global__ __launch_bounds__(256) void selective_bwd_reduce_kernel(const BwdArgs a,
-                                                                   const BwWork w, int64_t G) {
+                                                                   const BwWork w, int64_t G,
+                                                                   int n0, bool last) {
   const int64_t B = a.B, D = a.D, N = a.N, L = a.L;
+  const int64_t ng = N - n0 < BW_N ? N - n0 : BW_N;  // states of this group
   const int64_t nq = B * L * (BW_N / 4);  // float4 chunks of one of dB / dC
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const int64_t gstep = L * (BW_N / 4);   // float4 stride between workgroup shares
@@ -431,22 +450,23 @@ __global__ __launch_bounds__(256) void selective_bwd_reduce_kernel(const BwdArgs
       acc.z += v.z;
       acc.w += v.w;
     }
-    float* const dst = (isC ? a.dC : a.dB) + bt * N;
+    float* const dst = (isC ? a.dC : a.dB) + bt * N + n0;
     const float av[4] = {acc.x, acc.y, acc.z, acc.w};
     if (N == BW_N && (((uintptr_t)a.dB | (uintptr_t)a.dC) & 15) == 0) {
       *reinterpret_cast<float4*>(dst + 4 * c) = acc;
     } else {
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        if (4 * c + u < N) dst[4 * c + u] = av[u];
+        if (4 * c + u < ng) dst[4 * c + u] = av[u];
     }
   }
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < D * N; i += stride) {
-    const int64_t d = i / N, nn = i - d * N;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < D * ng; i += stride) {
+    const int64_t d = i / ng, nn = i - d * ng;
     float s = 0.f;
     for (int64_t b = 0; b < B; ++b) s += w.dA_p[(b * D + d) * BW_N + nn];
-    a.dA[i] = s;
+    a.dA[d * N + n0 + nn] = s;
   }
+  if (!last) return;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < D; i += stride) {
     float sd = 0.f, sbias = 0.f;
     for (int64_t b = 0; b < B; ++b) {
@@ -460,31 +480,30 @@ __global__ __launch_bounds__(256) void selective_bwd_reduce_kernel(const BwdArgs
 
 template <typename IN>
 void launch_bwd_in(const BwdArgs& a, const BwWork& w, int64_t G, int64_t ntile, int64_t grid,
-                   hipStream_t s) {
+                   int n0, hipStream_t s) {
   if (a.dy_bf16) {
     auto kern = a.z ? selective_bwd_kernel<IN, uint16_t, true>
                     : selective_bwd_kernel<IN, uint16_t, false>;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile, n0);
   } else {
     auto kern = a.z ? selective_bwd_kernel<IN, float, true> : selective_bwd_kernel<IN, float, false>;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile, n0);
   }
 }
 
 void launch_bwd(const BwdArgs& a, const BwWork& w, int64_t G, int64_t ntile, int64_t grid,
-                hipStream_t s) {
+                int n0, hipStream_t s) {
   if (a.bf16_in)
-    launch_bwd_in<uint16_t>(a, w, G, ntile, grid, s);
+    launch_bwd_in<uint16_t>(a, w, G, ntile, grid, n0, s);
   else
-    launch_bwd_in<float>(a, w, G, ntile, grid, s);
+    launch_bwd_in<float>(a, w, G, ntile, grid, n0, s);
 }
 
 }  // namespace
 
 int selective_bwd(const BwdArgs& a) {
-  if (a.N > BW_N)
-    return fail(SW_ERR_UNSUPPORTED, "the backward pass supports N <= %d (got %lld)", BW_N,
-                (long long)a.N);
+  if (a.ckpt && a.N > BW_N)
+    return fail(SW_ERR_UNSUPPORTED, "checkpoints hold 16 states (N=%lld)", (long long)a.N);
   hipStream_t s = current_stream();
   const int64_t B = a.B, D = a.D, L = a.L;
   const int64_t G = (D + BW_ROWS - 1) / BW_ROWS;
@@ -543,16 +562,19 @@ int selective_bwd(const BwdArgs& a) {
       return st;
     }
   }
-  launch_bwd(a, w, G, ntile, grid, s);
-  st = check_launch("selective_bwd_kernel");
-  if (st == SW_OK) {
+  // the states in groups of 16: each group's main kernel, then its reduction
+  // (dA, dB, dC of its states; the sums over the states accumulate)
+  for (int n0 = 0; n0 < a.N && st == SW_OK; n0 += BW_N) {
+    launch_bwd(a, w, G, ntile, grid, n0, s);
+    st = check_launch("selective_bwd_kernel");
+    if (st != SW_OK) break;
     int64_t work = 2 * B * L * (BW_N / 4);
-    if (work < D * a.N) work = D * a.N;
+    if (work < D * BW_N) work = D * BW_N;
     int64_t blocks = (work + 255) / 256;
     if (blocks > 8192) blocks = 8192;
     if (blocks < 1) blocks = 1;
     hipLaunchKernelGGL(selective_bwd_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, w,
-                       G);
+                       G, n0, n0 + BW_N >= a.N);
     st = check_launch("selective_bwd_reduce_kernel");
   }
   workspace_free(base, s);

@@ -245,8 +245,8 @@ int selective_bwd_common(BwdArgs a) {
       !mul_ok(D, N, &nan) || !mul_ok(R, 16 * ((L + 7) / 8 + 1), &tmp) || !mul_ok(tmp, 8, &tmp))
     return fail(SW_ERR_UNSUPPORTED, "sizes overflow");
   if (a.dz && !a.z) return fail(SW_ERR_INVALID_ARG, "dz requires z");
-  if (N > 16)
-    return fail(SW_ERR_UNSUPPORTED, "the backward pass supports N <= 16 (got %lld)", (long long)N);
+  if (a.ckpt && N > 16)
+    return fail(SW_ERR_UNSUPPORTED, "checkpoints hold 16 states (got N=%lld)", (long long)N);
   int dev, st;
   if ((st = current_device(&dev)) != SW_OK) return st;
   const size_t es = a.bf16_in ? 2 : 4, dys = a.dy_bf16 ? 2 : 4;

@@ -147,13 +147,28 @@ def test_bwd_empty_sequence(sw):
     assert torch.count_nonzero(g["dA"]) == 0 and torch.count_nonzero(g["dDskip"]) == 0
 
 
-def test_bwd_rejects_large_N_and_dz_without_z(sw):
+def test_bwd_rejects_N_above_64(sw):
     from paper_2606_00601_amd import ScanWeaverError
     x = torch.randn((1, 2, 8), device="cuda")
     with pytest.raises(ScanWeaverError):
-        sw.selective_scan_bwd(x, x, torch.randn((2, 17), device="cuda"),
-                              torch.randn((1, 8, 17), device="cuda"),
-                              torch.randn((1, 8, 17), device="cuda"), None, x)
+        sw.selective_scan_bwd(x, x, torch.randn((2, 65), device="cuda"),
+                              torch.randn((1, 8, 65), device="cuda"),
+                              torch.randn((1, 8, 65), device="cuda"), None, x)
+
+
+# N above 16: the states run as several passes of 16
+@pytest.mark.parametrize("shape", [(2, 19, 17, 70), (1, 16, 32, 64), (2, 7, 64, 33), (1, 5, 40, 130)])
+@pytest.mark.parametrize("opts", [(), ("z", "bias", "softplus", "h0", "dhl")])
+def test_bwd_more_than_16_states(sw, shape, opts):
+    B, D, N, L = shape
+    _say("case bwd N>16", shape, opts)
+    inp, ex = _inputs(B, D, N, L, 960 + N + L, "f32", opts)
+    g = _run(sw, inp, ex, "f32", opts)
+    o = _ref(inp, ex, opts)
+    keys = ["dx", "ddelta", "dA", "dB", "dC", "dDskip", "dh0"]
+    if "z" in opts:
+        keys += ["dz", "ddelta_bias"]
+    _check_all(g, o, f"N>16 {shape} {opts}", keys)
 
 
 def test_bwd_full_size_sampled(sw):
