@@ -22,6 +22,7 @@ from ._lib import ScanWeaverError, check, last_error, lib, status_string  # noqa
 __all__ = ["affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
            "affine_scan_proj", "affine_scan_proj_i32",
            "selective_scan_fwd", "selective_scan_fwd_schedule", "selective_scan_bwd", "new_ckpt",
+           "selective_scan_fn",
            "ScanWeaverError",
            "version"]
 
@@ -311,3 +312,42 @@ def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, 
             B, D, N, L, in_dt, dy_dt, SW_DELTA_SOFTPLUS if delta_softplus else 0),
             "sw_selective_scan_bwd")
     return {k: v for k, v in out.items() if v is not None}
+
+
+class _SelectiveScanFn(torch.autograd.Function):
+    """Autograd glue: the forward keeps its 8-step checkpoints (N <= 16) and the
+    backward runs sw_selective_scan_bwd; no arithmetic happens here."""
+
+    @staticmethod
+    def forward(ctx, x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, delta_softplus):
+        N = A.shape[1]
+        ck = new_ckpt(x, N) if N <= 16 else None
+        y, h_last = selective_scan_fwd(x, delta, A, Bm, Cm, Dskip, z=z, delta_bias=delta_bias,
+                                       h0=h0, delta_softplus=delta_softplus, ckpt=ck,
+                                       y_dtype=torch.float32)
+        ctx.save_for_backward(x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, ck)
+        ctx.delta_softplus = delta_softplus
+        ctx.mark_non_differentiable(h_last)
+        return y, h_last
+
+    @staticmethod
+    def backward(ctx, dy, _dh_last):
+        x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, ck = ctx.saved_tensors
+        dy = dy.contiguous().to(torch.float32)
+        g = selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, z=z, delta_bias=delta_bias,
+                               h0=h0, delta_softplus=ctx.delta_softplus,
+                               want_dh0=h0 is not None and h0.requires_grad, ckpt=ck)
+        cast = lambda t, like: None if t is None else t.to(like.dtype)  # noqa: E731
+        return (cast(g["dx"], x), cast(g["ddelta"], delta), g["dA"], cast(g["dB"], Bm),
+                cast(g["dC"], Cm), g.get("dDskip"), cast(g.get("dz"), z) if z is not None else None,
+                g.get("ddelta_bias"), g.get("dh0"), None)
+
+
+def selective_scan_fn(x, delta, A, Bm, Cm, Dskip=None, z=None, delta_bias=None, h0=None,
+                      delta_softplus=False, return_last_state=False):
+    """Differentiable fused selective scan (fp32 y): :func:`selective_scan_fwd`
+    forward, :func:`selective_scan_bwd` backward through torch autograd.
+    Gradients come back in each input's dtype; h_last is not differentiated."""
+    y, h_last = _SelectiveScanFn.apply(x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0,
+                                       bool(delta_softplus))
+    return (y, h_last) if return_last_state else y
