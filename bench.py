@@ -92,10 +92,11 @@ def measured_traffic(w):
         return None
 
 
-def cpu_baseline(w, inp, target_s: float = 12.0, max_rows: int | None = None):
-    """Time the fp64 oracle (as it stands) on all host cores over a sample of rows."""
+def cpu_baseline(w, inp, target_s: float = 12.0, max_rows: int | None = None, threads: int = 0):
+    """Time the fp64 oracle (as it stands) on the host cores (all of them, or
+    `threads`) over a sample of rows."""
     import oracle
-    cores = len(os.sched_getaffinity(0))
+    cores = threads if threads > 0 else len(os.sched_getaffinity(0))
     R = w.B * w.D
     rows = 64
 
@@ -117,18 +118,77 @@ def cpu_baseline(w, inp, target_s: float = 12.0, max_rows: int | None = None):
                               inp["Dskip"], rows=ridx, threads=cores)
         return time.perf_counter() - t
 
+    rows = min(rows, R)
     dt = run(rows)
     while dt < target_s / 4 and rows < R and (max_rows is None or rows < max_rows):
         rows = min(R, rows * 4, max_rows or R)
         dt = run(rows)
-    elems = rows * w.L * w.N
+    reps = 1
+    while dt < 0.25:  # the whole workload is short: repeat it
+        reps *= 4
+        dt = sum(run(rows) for _ in range(reps))
+    elems = rows * w.L * w.N * reps
     import oracle as _o
     return {
         "value": elems / dt, "unit": "elems/s", "cores": _o.threads_used(cores, rows),
         "kind": "oracle",
-        "sample": f"{rows} of {R} (b,d) rows x L={w.L} x N={w.N} of {w.name}, fp64, "
-                  f"{dt:.1f} s wall",
+        "sample": f"{rows} of {R} (b,d) rows x L={w.L} x N={w.N} of {w.name}"
+                  + (f", {reps} repeats" if reps > 1 else "") + f", fp64, {dt:.1f} s wall",
     }
+
+
+def cpu_baseline_affine(w, inp, int32: bool, target_s: float = 8.0, threads: int = 0):
+    """Time the bare-scan oracle (fp64, or the uint32 loop) over a sample of rows."""
+    import oracle
+    cores = threads if threads > 0 else len(os.sched_getaffinity(0))
+    R = w.B * w.D
+    a2, b2 = inp["a"].reshape(R, w.L), inp["bx"].reshape(R, w.L)
+    rows, reps = min(R, 8), 1
+
+    def run(nrows, nrep):
+        t = time.perf_counter()
+        for _ in range(nrep):
+            if int32:
+                oracle.affine_scan_i32(a2[:nrows], b2[:nrows], threads=cores)
+            else:
+                oracle.affine_scan(a2[:nrows], b2[:nrows], threads=cores)
+        return time.perf_counter() - t
+
+    dt = run(rows, reps)
+    while dt < target_s / 4:
+        if rows < R:
+            rows = min(R, rows * 4)
+        else:
+            reps *= 4  # the whole workload is short: repeat it
+        dt = run(rows, reps)
+    return {
+        "value": rows * w.L * reps / dt, "unit": "elems/s",
+        "cores": oracle.threads_used(cores, rows), "kind": "oracle",
+        "sample": f"{rows} of {R} rows x L={w.L} of {w.name}"
+                  + (f", {reps} repeats" if reps > 1 else "")
+                  + f", {'uint32' if int32 else 'fp64'}, {dt:.2f} s wall",
+    }
+
+
+def measure_copy_bandwidth(mib: int = 2048, reps: int = 10) -> dict:
+    """A plain device-to-device copy of `mib` MiB, timed with HIP events:
+    bytes read plus bytes written per second."""
+    import torch
+    n = mib << 18
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) * 1e-3 / reps
+    return {"copy_GBs": 2 * n * 4 / sec / 1e9, "copy_MiB": mib, "reps": reps,
+            "frac_of_peak": 2 * n * 4 / sec / 1e9 / HBM_PEAK_GBS}
 
 
 def time_launches(step, steps, warmup):
@@ -161,6 +221,8 @@ def bench_affine(w, args):
     torch.cuda.set_device(dev)
     sw.lib()
     inp = w.inputs()
+    if args.int32:
+        inp = wl.affine_inputs_i32(w.B, w.D, w.L, wl.INT_SEEDS["uniform"], "uniform")
     proj = args.form == "proj"
     # bare: a, bx read, h written; projection form (Eq. (3)-(4)): a, b, x, c
     # read, y written, h_last written once per row
@@ -175,6 +237,8 @@ def bench_affine(w, args):
         bx = torch.from_numpy(inp["bx"]).to(dev)
         extra = tuple(torch.from_numpy(v).to(dev) for v in xc) if proj else ()
         sets.append((a, bx, torch.empty_like(a)) + extra)
+    cpu = None if args.no_cpu or proj else cpu_baseline_affine(w, inp, args.int32,
+                                                               threads=args.cpu_threads)
     del inp
 
     def step(i):
@@ -182,6 +246,8 @@ def bench_affine(w, args):
         a, bx, h = st[:3]
         if proj:
             sw.affine_scan_proj(a, bx, st[3], st[4], y=h)
+        elif args.int32:
+            sw.affine_scan_i32(a, bx, out=h)
         elif args.schedule == "default":
             sw.affine_scan(a, bx, out=h)
         else:
@@ -205,8 +271,8 @@ def bench_affine(w, args):
                    "affine-scan fwd B*L*D elems/s (+ achieved HBM GB/s vs peak), 1 GPU"),
         "value": w.elems * args.steps / wall, "unit": "elems/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32" if args.int32 else "f32", "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "D": w.D, "L": w.L, "input_sets_rotated": nsets,
                    "schedule": args.schedule, "form": args.form},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -214,6 +280,8 @@ def bench_affine(w, args):
                      "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
                                        "median": float(np.median(per)) * 1e6}},
     }
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
     return 0
 
@@ -299,6 +367,12 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="host threads for the CPU oracle baseline (0: all cores)")
+    ap.add_argument("--int32", action="store_true",
+                    help="bare-scan workloads: the int32 wraparound mode")
+    ap.add_argument("--measure-copy", action="store_true",
+                    help="only time a plain 2 GiB device copy and print its bandwidth")
     ap.add_argument("--pass", dest="which", choices=("fwd", "bwd"), default="fwd",
                     help="time the forward (default, the headline metric) or the backward")
     ap.add_argument("--schedule", choices=("default", "blelloch"), default="default",
@@ -341,6 +415,10 @@ def main(argv=None):
         torch.cuda.synchronize()
         print(json.dumps({"calibration": "copy", "bytes_read": n * 4, "bytes_written": n * 4,
                           "launches": 5}), flush=True)
+        return 0
+
+    if args.measure_copy:
+        print(json.dumps(measure_copy_bandwidth()), flush=True)
         return 0
 
     import paper_2606_00601_amd as sw
@@ -471,7 +549,7 @@ def main(argv=None):
                 "frac": hbm_gbs / HBM_PEAK_GBS},
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(w, inp)
+        out["cpu_baseline"] = cpu_baseline(w, inp, threads=args.cpu_threads)
     print(json.dumps(out), flush=True)
     return 0
 
