@@ -33,9 +33,16 @@
  *    (B*D == 0, or L == 0 for the bare scan) returns SW_OK and touches
  *    nothing; pointers are not inspected in that case.
  *  - Outputs must not overlap inputs or each other (SW_ERR_INVALID_ARG).
- *  - Scratch memory (only for sequences split across workgroups) is taken
- *    from the device's stream-ordered pool on the same stream and returned
- *    to it before the call returns; SW_ERR_ALLOC if that fails.
+ *  - Scratch memory: calls whose sequences are split across workgroups use
+ *    a small scratch per (device, stream) -- carry words and a ticket
+ *    counter -- allocated from the device's default stream-ordered pool on
+ *    the first such call on that stream, kept for later calls (grown when a
+ *    call needs more) and never freed by the library.  The backward pass
+ *    takes a per-call workspace from the same pool on the same stream and
+ *    releases it, stream-ordered, before returning.  The library raises that
+ *    pool's release threshold so freed blocks stay cached for the next call
+ *    (a process-wide setting of the device's default pool).  SW_ERR_ALLOC if
+ *    an allocation fails.
  *  - Threads using distinct streams may call concurrently.
  */
 #ifndef SCANWEAVER_H
