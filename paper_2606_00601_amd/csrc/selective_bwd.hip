@@ -20,14 +20,17 @@
 //   2. A reverse sweep over the tiles: the tile's delta, delta*x, ds and
 //      B, C are staged in LDS; every lane reloads its checkpoint, recomputes
 //      the tile's a_t and q_t forward into registers, then walks the tile
-//      backwards carrying lam.  Per step it writes four partial products to
-//      LDS: lam q A and lam B (summed over n, per row and step, into ddelta
-//      and dx) and lam delta x and ds h (summed over the 16 rows, per step and
-//      state, into this workgroup's share of dB and dC).
+//      backwards carrying lam.  Per step it forms four partial products:
+//      lam q A and lam B (summed over n, per row and step, into ddelta and
+//      dx) go to LDS; lam delta x and ds h (summed over the 16 rows, per step
+//      and state, into this workgroup's share of dB and dC) are first summed
+//      over the wavefront's four rows by lane-half exchanges, and only those
+//      sums go to LDS.
 //   3. Half of the workgroup sums the first pair per (row, step), the other
-//      half the second pair per (step, state); the shares of dB / dC, dA,
-//      dDskip and ddelta_bias go to a workspace, and a second kernel adds the
-//      shares in a fixed order (no atomics: the result is reproducible).
+//      half adds the four wavefronts' row sums per (step, state); the shares
+//      of dB / dC, dA, dDskip and ddelta_bias go to a workspace, and a second
+//      kernel adds the shares in a fixed order (no atomics: the result is
+//      reproducible).
 // The pre-gate output s needed by dz comes from the forward kernel run
 // without the gate.
 #include "selective_common.h"
@@ -40,8 +43,7 @@ constexpr int BW_T = 8;                  // steps per tile
 constexpr int BW_TS = 8;                 // LDS stride of one [t] run (16-byte aligned)
 constexpr int BW_ROWS = 16;              // (b,d) rows per workgroup
 // stride of one row's [n][t] block: 8 mod 64 banks, so that the 64 lanes of a
-// role-a reduce (8 rows x 8 steps) read 64 different banks; 42.5 KB of LDS in
-// all lets three workgroups share a CU
+// role-a reduce (8 rows x 8 steps) read 64 different banks
 constexpr int BW_RS = BW_N * BW_TS + 8;
 constexpr int BW_RING = 4;               // raw tile registers: loads run 3 tiles ahead
 constexpr float BW_LOG2E = 1.4426950408889634f;
@@ -55,8 +57,35 @@ struct BwSmem {
   float rv[2][3][BW_ROWS][BW_TS];  // two tile buffers; per row and step: delta, delta*x, ds
   float bc[2][2][BW_N][BW_TS];     // two tile buffers; B, C of the tile as [n][t]
   float sp[2][BW_ROWS * BW_RS];    // per row [n][t]: lam q A, lam B      (sum over n)
-  float pb[2][BW_ROWS * BW_RS];    // per row [n][t]: lam delta x, ds h   (sum over rows)
+  float pw[4][64 * 4];             // per wavefront and lane: four row sums (rows4_sum)
 };
+
+// Sums over the four 16-lane rows of a wavefront, by the two lane-half
+// exchanges of gfx950: v_permlane32_swap trades lanes 32-63 of its first
+// operand with lanes 0-31 of its second, v_permlane16_swap the odd 16-lane
+// rows of the first with the even rows of the second.  In: a lane's
+// lam delta x (dx) and ds h (dh) at the tile's 8 steps.  Out: lane l holds,
+// for state l % 16, the sums over the four rows of dx (l < 32) or dh
+// (l >= 32) at steps 4 ((l / 16) & 1) + 0..3.
+__device__ __forceinline__ void rows4_sum(const float (&dx)[8], const float (&dh)[8],
+                                          float (&out)[4]) {
+  float r[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    // lanes 0-31 get dx of lanes l and l+32, lanes 32-63 dh of l-32 and l
+    const auto v = __builtin_amdgcn_permlane32_swap(__float_as_uint(dx[t]),
+                                                    __float_as_uint(dh[t]), false, false);
+    r[t] = __uint_as_float(v[0]) + __uint_as_float(v[1]);
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    // row 0 of the wavefront gets rows 0 + 1 of r[t], row 1 rows 0 + 1 of
+    // r[t+4], rows 2 and 3 likewise from rows 2 + 3
+    const auto v = __builtin_amdgcn_permlane16_swap(__float_as_uint(r[t]),
+                                                    __float_as_uint(r[t + 4]), false, false);
+    out[t] = __uint_as_float(v[0]) + __uint_as_float(v[1]);
+  }
+}
 
 __device__ __forceinline__ float sigmoid_f32(float v) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-v * BW_LOG2E));
@@ -276,8 +305,9 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
       hring[(u + BW_RING - 1) % BW_RING] = *ck_at(k - (BW_RING - 1));
       bw_barrier();
 
-      // recompute a_t and q_t = a_t h_{t-1} of the tile
-      float av[BW_T], qv[BW_T];
+      // recompute a_t, q_t = a_t h_{t-1} and h_t of the tile; delta, delta*x
+      // and B stay in registers for the backward walk
+      float av[BW_T], qv[BW_T], hv[BW_T], dlr[BW_T], dxr[BW_T], br[BW_T];
       {
         float hh = hstart;
 #pragma unroll
@@ -290,54 +320,55 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
           const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
+            dlr[q + j] = dlq[j];
+            dxr[q + j] = dxq[j];
+            br[q + j] = bq[j];
             av[q + j] = __builtin_amdgcn_exp2f(dlq[j] * Al);
             qv[q + j] = av[q + j] * hh;
             hh = __builtin_fmaf(dxq[j], bq[j], qv[q + j]);
+            hv[q + j] = hh;
           }
         }
       }
       // walk the tile backwards
       float* const sp0 = &sm.sp[0][rr * BW_RS + n * BW_TS];
       float* const sp1 = &sm.sp[1][rr * BW_RS + n * BW_TS];
-      float* const pb0 = &sm.pb[0][rr * BW_RS + n * BW_TS];
-      float* const pb1 = &sm.pb[1][rr * BW_RS + n * BW_TS];
+      float pdx[BW_T], pdh[BW_T];  // lam delta x and ds h, summed over rows below
 #pragma unroll
       for (int q = BW_T - 4; q >= 0; q -= 4) {
-        const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[buf][0][rr][q]);
-        const float4 dx4 = *reinterpret_cast<const float4*>(&sm.rv[buf][1][rr][q]);
         const float4 ds4 = *reinterpret_cast<const float4*>(&sm.rv[buf][2][rr][q]);
-        const float4 b4 = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n][swz(n, q)]);
         const float4 c4 = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n][swz(n, q)]);
-        const float dlq[4] = {dl4.x, dl4.y, dl4.z, dl4.w};
-        const float dxq[4] = {dx4.x, dx4.y, dx4.z, dx4.w};
         const float dsq[4] = {ds4.x, ds4.y, ds4.z, ds4.w};
-        const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
         const float cq[4] = {c4.x, c4.y, c4.z, c4.w};
-        float o0[4], o1[4], o2[4], o3[4];
+        float o0[4], o1[4];
 #pragma unroll
         for (int j = 3; j >= 0; --j) {
+          const int t = q + j;
           const float l = __builtin_fmaf(dsq[j], cq[j], lam);
-          const float hc = __builtin_fmaf(dxq[j], bq[j], qv[q + j]);
-          const float p = l * qv[q + j];
-          dA_acc = __builtin_fmaf(p, dlq[j], dA_acc);
+          const float p = l * qv[t];
+          dA_acc = __builtin_fmaf(p, dlr[t], dA_acc);
           o0[j] = p * Ar;
-          o1[j] = l * bq[j];
-          o2[j] = l * dxq[j];
-          o3[j] = dsq[j] * hc;
-          lam = av[q + j] * l;
+          o1[j] = l * br[t];
+          pdx[t] = l * dxr[t];
+          pdh[t] = dsq[j] * hv[t];
+          lam = av[t] * l;
         }
         const int qs = swz(n, q);
         *reinterpret_cast<float4*>(sp0 + qs) = make_float4(o0[0], o0[1], o0[2], o0[3]);
         *reinterpret_cast<float4*>(sp1 + qs) = make_float4(o1[0], o1[1], o1[2], o1[3]);
-        *reinterpret_cast<float4*>(pb0 + qs) = make_float4(o2[0], o2[1], o2[2], o2[3]);
-        *reinterpret_cast<float4*>(pb1 + qs) = make_float4(o3[0], o3[1], o3[2], o3[3]);
+      }
+      {
+        float o[4];
+        rows4_sum(pdx, pdh, o);
+        *reinterpret_cast<float4*>(&sm.pw[wv][lane * 4]) = make_float4(o[0], o[1], o[2], o[3]);
       }
       bw_barrier();  // the partials are complete; the next tile stages the other buffer
 
       // Role a sums over the states (ddelta, dx of row sr, step st), role b
-      // over the 16 rows (this workgroup's share of dB, dC at step bt, state
-      // bn).  The stores are the same instructions for every lane, aimed at
-      // the trash slots where a lane has nothing to store.
+      // over the four wavefronts' row sums (this workgroup's share of dB, dC
+      // at step bt, state bn).  The stores are the same instructions for
+      // every lane, aimed at the trash slots where a lane has nothing to
+      // store.
       float v0, v1, v2 = 0.f;
       float *p0, *p1, *p2 = w.trash + tid;
       if (role_a) {
@@ -360,11 +391,14 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         if (first) dD_acc = __builtin_fmaf(ds, xv, dD_acc);
         db_acc += ddl;
       } else {
+        // lane (bt / 4) * 16 + bn of each wavefront holds the dB sums of
+        // steps 4 (bt / 4) .. +3 at state bn, lane 32 more the dC sums
+        const int lb = (bt >> 2) * 16 + bn, tb = bt & 3;
         float sb = 0.f, sc = 0.f;
 #pragma unroll
-        for (int m = 0; m < BW_ROWS; ++m) {
-          sb += sm.pb[0][m * BW_RS + bn * BW_TS + swz(bn, bt)];
-          sc += sm.pb[1][m * BW_RS + bn * BW_TS + swz(bn, bt)];
+        for (int m = 0; m < 4; ++m) {
+          sb += sm.pw[m][lb * 4 + tb];
+          sc += sm.pw[m][(32 + lb) * 4 + tb];
         }
         const int64_t t = k * BW_T + bt;
         const int64_t i = ((b * G + g) * L + (t < L ? t : 0)) * BW_N + bn;
