@@ -130,11 +130,24 @@ struct TileRaw {
   bool ok;  // role a: a step of a real row inside the sequence; role b: t < L, n < N
 };
 
-// All global loads below are unconditional, from clamped (always valid)
-// addresses, with the unwanted values replaced afterwards: the loads of the
-// next tile then stay in flight across the current one instead of being
-// waited for inside a branch.
-template <typename IN, typename DYT, bool GATED>
+// One element of type T at byte offset voff + soff of a raw buffer resource
+// (zero past the resource's end).
+template <typename T>
+__device__ __forceinline__ T buf_ld(__amdgpu_buffer_rsrc_t r, int32_t voff, int32_t soff) {
+  if constexpr (sizeof(T) == 4)
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+  else
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
+}
+
+// All global loads below are unconditional, from valid addresses, with the
+// unwanted values replaced afterwards: the loads of the next tile then stay in
+// flight across the current one instead of being waited for inside a branch.
+// BUF: the loads go through raw buffer resources over the workgroup's rows
+// (and its batch's B, C), so that a tile's address is a per-lane offset fixed
+// for the whole kernel plus a scalar one (every offset below 2^31, checked by
+// the host); without it, 64-bit addresses clamped into range.
+template <typename IN, typename DYT, bool GATED, bool BUF>
 __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, const BwWork w,
                                                             int64_t G, int64_t ntile, int n0) {
   __shared__ __align__(16) BwSmem sm;
@@ -181,7 +194,50 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   const IN* __restrict__ P0 = role_a ? X : BM;
   const IN* __restrict__ P1 = role_a ? DL : CM;
   using Raw = TileRaw<IN, DYT>;
+  // BUF: resources and per-lane element offsets.  Role a (and the dy, z, s
+  // loads of every lane) index (row - d0) * L + t of the workgroup's rows,
+  // role b (t * N + n) of the batch's B, C.
+  const int64_t row0 = b * D + d0;
+  const int64_t nrows = imin(BW_ROWS, D - d0);
+  const int32_t ea = (int32_t)(((sdok ? sd : D - 1) - d0) * L) + st;
+  const int32_t eb = bt * (int32_t)N + (n0 + bn < N ? n0 + bn : (int32_t)N - 1);
+  const int32_t e01 = role_a ? ea : eb;
+  const int32_t ts01 = role_a ? BW_T : BW_T * (int32_t)N;  // elements per tile
+  // (built in both variants; only BUF uses them)
+  const uint32_t rows_b = (uint32_t)(nrows * L * (int64_t)sizeof(IN));
+  const uint32_t bc_b = (uint32_t)(L * N * (int64_t)sizeof(IN));
+  const __amdgpu_buffer_rsrc_t r0s =
+      buffer_rsrc(role_a ? (const void*)(X + row0 * L) : (const void*)(BM + b * L * N),
+                  role_a ? rows_b : bc_b);
+  const __amdgpu_buffer_rsrc_t r1s =
+      buffer_rsrc(role_a ? (const void*)(DL + row0 * L) : (const void*)(CM + b * L * N),
+                  role_a ? rows_b : bc_b);
+  const __amdgpu_buffer_rsrc_t rdy =
+      buffer_rsrc(DY + row0 * L, (uint32_t)(nrows * L * (int64_t)sizeof(DYT)));
+  const __amdgpu_buffer_rsrc_t rz = buffer_rsrc(GATED ? Z + row0 * L : X, GATED ? rows_b : 0u);
+  const __amdgpu_buffer_rsrc_t rs =
+      buffer_rsrc(GATED ? w.s + row0 * L : w.trash, GATED ? (uint32_t)(nrows * L * 4) : 0u);
+  const __amdgpu_buffer_rsrc_t rck =
+      buffer_rsrc(w.ck + row0 * ntile * BW_N, (uint32_t)(nrows * ntile * BW_N * 4));
+  const int32_t eck = (int32_t)(((dok ? d : D - 1) - d0) * ntile * BW_N) + n;
   auto load_tile = [&](int64_t k, Raw& v) {
+    if constexpr (BUF) {
+      // a tile before the start reads tile 0 (unused); past the end, the
+      // offsets run out of the resources or into other rows (unused)
+      const int64_t kc = k < 0 ? 0 : k;
+      const int64_t rem = L - k * BW_T;
+      const int32_t lim = k < 0 ? 0 : (int32_t)(rem < 0 ? 0 : (rem < BW_T ? rem : BW_T));
+      v.ok = role_a ? (sdok && st < lim) : (bt < lim && n0 + bn < N);
+      const int32_t tk = (int32_t)kc * BW_T;  // first step of the tile
+      v.r0 = buf_ld<IN>(r0s, e01 * (int32_t)sizeof(IN), tk * (ts01 / BW_T) * (int32_t)sizeof(IN));
+      v.r1 = buf_ld<IN>(r1s, e01 * (int32_t)sizeof(IN), tk * (ts01 / BW_T) * (int32_t)sizeof(IN));
+      v.dy = buf_ld<DYT>(rdy, ea * (int32_t)sizeof(DYT), tk * (int32_t)sizeof(DYT));
+      if constexpr (GATED) {
+        v.z = buf_ld<IN>(rz, ea * (int32_t)sizeof(IN), tk * (int32_t)sizeof(IN));
+        v.s = buf_ld<float>(rs, ea * 4, tk * 4);
+      }
+      return;
+    }
     // every address is clamped into range, so tiles past either end (the
     // read-ahead) load valid, unused elements
     const int64_t ta = k * BW_T + st;
@@ -215,6 +271,15 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   auto ck_at = [&](int64_t k) {
     const int64_t kc = k < 0 ? 0 : (k < ntile ? k : ntile - 1);
     return w.ck + (ck_row + kc) * BW_N + n;
+  };
+  // the checkpoint of tile k (clamped into range; the ones outside are unused)
+  auto ck_load = [&](int64_t k) {
+    if constexpr (BUF) {
+      const int64_t kc = k < 0 ? 0 : (k < ntile ? k : ntile - 1);
+      return buf_ld<float>(rck, eck * 4, (int32_t)kc * (BW_N * 4));
+    } else {
+      return *ck_at(k);
+    }
   };
 
   // Raw inputs of tile j live in ring[j % BW_RING]: loads run BW_RING - 1
@@ -268,7 +333,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
 #pragma unroll
   for (int u = 0; u < BW_RING - 1; ++u) {
     load_tile(ntile - 1 - u, ring[u]);
-    hring[u] = *ck_at(ntile - 1 - u);
+    hring[u] = ck_load(ntile - 1 - u);
   }
   for (int64_t k0 = ntile - 1; k0 >= 0; k0 -= BW_RING) {
 #pragma unroll
@@ -302,7 +367,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
       }
       const float hstart = dok ? hring[u] : 0.0f;
       load_tile(k - (BW_RING - 1), ring[(u + BW_RING - 1) % BW_RING]);
-      hring[(u + BW_RING - 1) % BW_RING] = *ck_at(k - (BW_RING - 1));
+      hring[(u + BW_RING - 1) % BW_RING] = ck_load(k - (BW_RING - 1));
       bw_barrier();
 
       // recompute a_t, q_t = a_t h_{t-1} and h_t of the tile; delta, delta*x
@@ -512,25 +577,39 @@ __global__ __launch_bounds__(256) void selective_bwd_reduce_kernel(const BwdArgs
   }
 }
 
-template <typename IN>
-void launch_bwd_in(const BwdArgs& a, const BwWork& w, int64_t G, int64_t ntile, int64_t grid,
+// True when every byte offset of the buffer-resource path stays below 2^31:
+// a workgroup's rows of x, delta, dy, z and s, a batch's B and C, and a
+// workgroup's checkpoints, with the read-ahead tiles past the end.
+bool bwd_buf_fits(const BwdArgs& a, int64_t ntile) {
+  const int64_t lim = (int64_t)1 << 31;
+  const int64_t Lp = a.L + 4 * BW_RING * BW_T;
+  return BW_ROWS * Lp * 4 < lim && Lp * a.N * 4 < lim && BW_ROWS * (ntile + 2 * BW_RING) * BW_N * 4 < lim;
+}
+
+template <typename IN, typename DYT>
+void launch_bwd_dy(const BwdArgs& a, const BwWork& w, int64_t G, int64_t ntile, int64_t grid,
                    int n0, hipStream_t s) {
-  if (a.dy_bf16) {
-    auto kern = a.z ? selective_bwd_kernel<IN, uint16_t, true>
-                    : selective_bwd_kernel<IN, uint16_t, false>;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile, n0);
-  } else {
-    auto kern = a.z ? selective_bwd_kernel<IN, float, true> : selective_bwd_kernel<IN, float, false>;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile, n0);
-  }
+  const bool buf = bwd_buf_fits(a, ntile);
+  auto kern = a.z ? (buf ? selective_bwd_kernel<IN, DYT, true, true>
+                         : selective_bwd_kernel<IN, DYT, true, false>)
+                  : (buf ? selective_bwd_kernel<IN, DYT, false, true>
+                         : selective_bwd_kernel<IN, DYT, false, false>);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, a, w, G, ntile, n0);
 }
 
 void launch_bwd(const BwdArgs& a, const BwWork& w, int64_t G, int64_t ntile, int64_t grid,
                 int n0, hipStream_t s) {
-  if (a.bf16_in)
-    launch_bwd_in<uint16_t>(a, w, G, ntile, grid, n0, s);
-  else
-    launch_bwd_in<float>(a, w, G, ntile, grid, n0, s);
+  if (a.bf16_in) {
+    if (a.dy_bf16)
+      launch_bwd_dy<uint16_t, uint16_t>(a, w, G, ntile, grid, n0, s);
+    else
+      launch_bwd_dy<uint16_t, float>(a, w, G, ntile, grid, n0, s);
+  } else {
+    if (a.dy_bf16)
+      launch_bwd_dy<float, uint16_t>(a, w, G, ntile, grid, n0, s);
+    else
+      launch_bwd_dy<float, float>(a, w, G, ntile, grid, n0, s);
+  }
 }
 
 }  // namespace

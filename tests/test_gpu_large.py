@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 
 import oracle
+import workloads as wl
 from gate import assert_gate, fp_gate
 
 torch = pytest.importorskip("torch")
@@ -78,3 +79,27 @@ def test_selective_f32_past_2_31_elements(sw):
     assert_gate(fp_gate(got, o["y"], o["y_mag"], o["y_sens"]), "large selective y")
     hg = hl[0].index_select(0, ri).cpu().numpy()[None]
     assert_gate(fp_gate(hg, o["h_last"], o["h_mag"], o["h_sens"]), "large selective h_last")
+
+
+@pytest.mark.parametrize("L", [(1 << 24) - 200, (1 << 24) + 40])
+def test_selective_bwd_long_row_both_addressing_paths(sw, L):
+    """Backward over rows of about 2^24 steps: just below the length where a
+    workgroup's 8-step checkpoints (16 rows x ceil(L/8) x 16 states x 4
+    bytes, with the read-ahead) stop fitting 31-bit byte offsets, where the
+    kernel reads through buffer resources, and just above it, where it falls
+    back to 64-bit addresses.  Every gradient against the oracle."""
+    B, D, N = 1, 3, 4
+    _say("case selective bwd long row", B, D, N, L)
+    inp = wl.selective_inputs(B, D, N, L, 31, "f32")
+    rng = np.random.Generator(np.random.PCG64(36))
+    dy = rng.standard_normal((B, D, L)).astype(np.float32)
+    dev = lambda v: torch.from_numpy(np.ascontiguousarray(v)).to("cuda")
+    g = sw.selective_scan_bwd(dev(inp["x"]), dev(inp["delta"]), dev(inp["A"]), dev(inp["Bm"]),
+                              dev(inp["Cm"]), dev(inp["Dskip"]), dev(dy), None)
+    torch.cuda.synchronize()
+    o = oracle.selective_scan_bwd(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                                  inp["Dskip"], dy, None, bounds=True)
+    for k in ("dx", "ddelta", "dA", "dB", "dC", "dDskip", "dh0"):
+        if k not in o or g.get(k) is None:
+            continue
+        assert_gate(fp_gate(g[k].cpu().numpy(), o[k], o["m_" + k]), f"long-row bwd {k}")
