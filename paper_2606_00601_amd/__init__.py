@@ -8,10 +8,23 @@ non-OK status; every step of the computation runs in the HIP kernels.
 * ``affine_scan(a, bx, h0=None)``: h_t = a_t h_{t-1} + bx_t over the last
   axis of (B, D, L) fp32 tensors (ScanWeaver Sec. 3.1, Eq. (3)).
 * ``affine_scan_i32(a, bx, h0=None)``: the same in the int32 wraparound ring.
+* ``affine_scan_proj(a, b, x=None, c=None, h0=None)`` (and ``_i32``): the
+  elementwise form of Eq. (3)-(4), u = b x and y = c h, returning
+  ``(y, h_last)``; with x = c = None it is the weighted prefix of Eq. (10).
+* ``affine_scan_schedule(a, bx, h0=None, schedule=...)`` (and ``_i32``): the
+  bare scan with the library's schedule or the paper's Blelloch tree
+  (Sec. 3.3), for the schedule ablation.
 * ``selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, ...)``: the
   Mamba-style fused form, returning ``(y, h_last)``; x/delta/Bm/Cm may be fp32
   or bf16, with optional output gate, delta bias and softplus, initial state
-  and bf16 y.
+  and bf16 y; with ``ckpt=new_ckpt(x, N)`` it also keeps the 8-step
+  checkpoints the backward can reuse.
+* ``selective_scan_fwd_schedule(...)``: the plain fused form with either
+  schedule.
+* ``selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, ...)``:
+  every gradient of the fused form (fp32), deterministic.
+* ``selective_scan_fn(...)``: the fused form as a torch autograd function
+  (forward with checkpoints, the library's backward).
 """
 from __future__ import annotations
 
