@@ -340,14 +340,18 @@ class _SelectiveScanFn(torch.autograd.Function):
                                        y_dtype=torch.float32)
         ctx.save_for_backward(x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, ck)
         ctx.delta_softplus = delta_softplus
-        ctx.mark_non_differentiable(h_last)
+        ctx.set_materialize_grads(False)
         return y, h_last
 
     @staticmethod
-    def backward(ctx, dy, _dh_last):
+    def backward(ctx, dy, dh_last):
         x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, ck = ctx.saved_tensors
+        if dy is None:  # only h_last reached the loss
+            dy = torch.zeros(x.shape, dtype=torch.float32, device=x.device)
         dy = dy.contiguous().to(torch.float32)
-        g = selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, z=z, delta_bias=delta_bias,
+        if dh_last is not None:
+            dh_last = dh_last.contiguous().to(torch.float32)
+        g = selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last, z=z, delta_bias=delta_bias,
                                h0=h0, delta_softplus=ctx.delta_softplus,
                                want_dh0=h0 is not None and h0.requires_grad, ckpt=ck)
         cast = lambda t, like: None if t is None else t.to(like.dtype)  # noqa: E731
@@ -360,7 +364,9 @@ def selective_scan_fn(x, delta, A, Bm, Cm, Dskip=None, z=None, delta_bias=None, 
                       delta_softplus=False, return_last_state=False):
     """Differentiable fused selective scan (fp32 y): :func:`selective_scan_fwd`
     forward, :func:`selective_scan_bwd` backward through torch autograd.
-    Gradients come back in each input's dtype; h_last is not differentiated."""
+    Gradients come back in each input's dtype.  With ``return_last_state``
+    the final state h_last is differentiable too, so segments chained through
+    ``h0`` = the previous segment's h_last train end to end."""
     y, h_last = _SelectiveScanFn.apply(x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0,
                                        bool(delta_softplus))
     return (y, h_last) if return_last_state else y

@@ -288,3 +288,31 @@ def test_autograd_function_matches_oracle(sw):
            "dz": z.grad, "ddelta_bias": bias.grad, "dh0": h0.grad}
     for k, v in got.items():
         assert_gate(fp_gate(v.cpu().numpy(), o[k], o["m_" + k]), f"autograd {k}")
+
+
+def test_autograd_chained_segments_match_one_call(sw):
+    """Two segments chained through h0 = the first segment's h_last, under
+    autograd with a loss on both y and the final state, give the gradients
+    of one call over the whole sequence (the oracle's, with dh_last)."""
+    B, D, N, L, L1 = 2, 19, 16, 260, 96
+    opts = ("dhl",)
+    inp, ex = _inputs(B, D, N, L, 4242, "f32", opts)
+    leaves = {k: _dev(inp[k]).requires_grad_() for k in ("x", "delta", "A", "Bm", "Cm", "Dskip")}
+    xs, ds = leaves["x"], leaves["delta"]
+    y1, h1 = sw.selective_scan_fn(xs[:, :, :L1].contiguous(), ds[:, :, :L1].contiguous(),
+                                  leaves["A"], leaves["Bm"][:, :L1].contiguous(),
+                                  leaves["Cm"][:, :L1].contiguous(), leaves["Dskip"],
+                                  return_last_state=True)
+    y2, h2 = sw.selective_scan_fn(xs[:, :, L1:].contiguous(), ds[:, :, L1:].contiguous(),
+                                  leaves["A"], leaves["Bm"][:, L1:].contiguous(),
+                                  leaves["Cm"][:, L1:].contiguous(), leaves["Dskip"], h0=h1,
+                                  return_last_state=True)
+    dy = _dev(ex["dy"])
+    loss = (y1 * dy[:, :, :L1]).sum() + (y2 * dy[:, :, L1:]).sum() + (h2 * _dev(ex["dh_last"])).sum()
+    loss.backward()
+    torch.cuda.synchronize()
+    o = _ref(inp, ex, opts)
+    got = {"dx": xs.grad, "ddelta": ds.grad, "dA": leaves["A"].grad, "dB": leaves["Bm"].grad,
+           "dC": leaves["Cm"].grad, "dDskip": leaves["Dskip"].grad}
+    for k, v in got.items():
+        assert_gate(fp_gate(v.cpu().numpy(), o[k], o["m_" + k]), f"chained autograd {k}")
