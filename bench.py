@@ -55,16 +55,25 @@ def algorithmic_bytes(w) -> int:
     return x_dl + bc + a_d + out
 
 
-# the sources the forward kernels are built from (the traffic record is keyed to them)
+# the sources each path's kernels are built from (traffic records are keyed to them)
 FWD_SOURCES = ("selective_common.h", "selective_scan.hip", "selective_scan16.hip", "sw_internal.h")
+AFFINE_SOURCES = ("affine_scan.hip", "sw_internal.h")
+
+# workload -> committed HBM traffic record (rocprofv3 FETCH_SIZE / WRITE_SIZE)
+TRAFFIC_RECORDS = {
+    "selective_bf16_b8_d1536_n16_l2048": "selective_row16_bf16_b8_d1536_n16_l2048_traffic.txt",
+    "affine_f32_b1_d5120_l65536": "affine_rows_f32_b1_d5120_l65536_traffic.txt",
+    "affine_f32_b8_d1536_l2048": "affine_scan_f32_b8_d1536_l2048_traffic.txt",
+}
 
 
-def kernel_source_sha256() -> str:
-    """Hash of the forward kernels' sources and headers (sorted by name)."""
+def kernel_source_sha256(path: str = "selective") -> str:
+    """Hash of the sources and headers of one path's kernels (sorted by name)."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_00601_amd", "csrc")
-    for p in sorted(os.path.join(csrc, f) for f in FWD_SOURCES):
+    names = AFFINE_SOURCES if path == "affine" else FWD_SOURCES
+    for p in sorted(os.path.join(csrc, f) for f in names):
         h.update(os.path.basename(p).encode())
         with open(p, "rb") as f:
             h.update(f.read())
@@ -74,10 +83,13 @@ def kernel_source_sha256() -> str:
 def measured_traffic(w):
     """HBM bytes per launch from the committed counter summary, if it was taken on
     the current kernel sources and this workload; else None."""
-    path = os.path.join(ROOT, "profiles", "selective_fwd_traffic.txt")
+    name = TRAFFIC_RECORDS.get(w.name)
+    if name is None:
+        return None
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
-    sha = kernel_source_sha256()
+    sha = kernel_source_sha256(w.path)
     rec = {}
     with open(path) as f:
         for line in f:
@@ -276,7 +288,10 @@ def bench_affine(w, args):
         "config": {"workload": w.name, "B": w.B, "D": w.D, "L": w.L, "input_sets_rotated": nsets,
                    "schedule": args.schedule, "form": args.form},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gbs / HBM_PEAK_GBS, "traffic": None, "kernel": kname,
+                     "frac": gbs / HBM_PEAK_GBS,
+                     "traffic": (measured_traffic(w) if args.schedule == "default" and not proj
+                                 and not args.int32 else None),
+                     "kernel": kname,
                      "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
                                        "median": float(np.median(per)) * 1e6}},
     }
@@ -388,7 +403,8 @@ def main(argv=None):
     ap.add_argument("--sets", type=int, default=0,
                     help="input sets rotated through (default: enough to exceed the MALL)")
     ap.add_argument("--print-kernel-sha", action="store_true",
-                    help="print the hash of the kernel sources (for the traffic record) and exit")
+                    help="print the hash of the kernel sources of --workload's path "
+                         "(the key of its traffic record) and exit")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, 5 times "
                          "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -401,7 +417,7 @@ def main(argv=None):
         return 2
 
     if args.print_kernel_sha:
-        print(kernel_source_sha256())
+        print(kernel_source_sha256(wl.workload(args.workload).path))
         return 0
 
     import torch
