@@ -56,8 +56,10 @@ __device__ __forceinline__ int swz(int n, int t) { return t ^ ((n >> 1) & 4); }
 struct BwSmem {
   float rv[2][3][BW_ROWS][BW_TS];  // two tile buffers; per row and step: delta, delta*x, ds
   float bc[2][2][BW_N][BW_TS];     // two tile buffers; B, C of the tile as [n][t]
-  float sp[2][BW_ROWS * BW_RS];    // per row [n][t]: lam q A, lam B      (sum over n)
-  float pw[4][64 * 4];             // per wavefront and lane: four row sums (rows4_sum)
+  // partials, two buffers (tile k uses k & 1): the sums of tile k+1 are read
+  // while tile k's are written, so one barrier per tile orders both
+  float sp[2][2][BW_ROWS * BW_RS];  // per row [n][t]: lam q A, lam B      (sum over n)
+  float pw[2][4][64 * 4];           // per wavefront and lane: four row sums (rows4_sum)
 };
 
 // Sums over the four 16-lane rows of a wavefront, by the two lane-half
@@ -335,6 +337,64 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
     load_tile(ntile - 1 - u, ring[u]);
     hring[u] = ck_load(ntile - 1 - u);
   }
+  // Sums of tile k from partial buffer pb (role a: over the states, ddelta
+  // and dx of row sr, step st; role b: over the four wavefronts' row sums,
+  // this workgroup's share of dB, dC at step bt, state bn), with the
+  // role-a values saved from that tile's staging.  The stores are the same
+  // instructions for every lane, aimed at the trash slots where a lane has
+  // nothing to store.
+  float p_dlv = 0.f, p_sg = 1.f, p_ds = 0.f, p_gp = 0.f, p_xv = 0.f, p_dyv = 0.f, p_sv = 0.f;
+  bool p_live = false;
+  auto reduce_tile = [&](int64_t k, int pb) {
+    float v0, v1, v2 = 0.f;
+    float *p0, *p1, *p2 = w.trash + tid;
+    if (role_a) {
+      float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int m = 0; m < BW_N; ++m) {
+        s1 += sm.sp[pb][0][sr * BW_RS + m * BW_TS + swz(m, st)];
+        s2 += sm.sp[pb][1][sr * BW_RS + m * BW_TS + swz(m, st)];
+      }
+      const float ddl = p_live ? (s1 + p_xv * s2) * p_sg : 0.0f;
+      v0 = ddl;
+      v1 = __builtin_fmaf(p_dlv, s2, first ? p_ds * Dsk : 0.0f);
+      const int64_t i = srow * L + (p_live ? k * BW_T + st : 0);
+      p0 = p_live ? a.ddelta + i : w.trash + tid;
+      p1 = p_live ? a.dx + i : w.trash + tid;
+      if constexpr (GATED) {
+        v2 = p_dyv * p_sv * p_gp;
+        p2 = p_live ? a.dz + i : w.trash + tid;
+      }
+      if (first) dD_acc = __builtin_fmaf(p_ds, p_xv, dD_acc);
+      db_acc += ddl;
+    } else {
+      // lane (bt / 4) * 16 + bn of each wavefront holds the dB sums of
+      // steps 4 (bt / 4) .. +3 at state bn, lane 32 more the dC sums
+      const int lb = (bt >> 2) * 16 + bn, tb = bt & 3;
+      float sb = 0.f, sc = 0.f;
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        sb += sm.pw[pb][m][lb * 4 + tb];
+        sc += sm.pw[pb][m][(32 + lb) * 4 + tb];
+      }
+      const int64_t t = k * BW_T + bt;
+      const int64_t i = ((b * G + g) * L + (t < L ? t : 0)) * BW_N + bn;
+      v0 = sb;
+      v1 = sc;
+      p0 = t < L ? w.dB_p + i : w.trash + tid;
+      p1 = t < L ? w.dC_p + i : w.trash + tid;
+    }
+    if (role_a && !first) {  // later state groups add to the sums over the states
+      v0 += *p0;
+      v1 += *p1;
+    }
+    *p0 = v0;
+    *p1 = v1;
+    if constexpr (GATED) {
+      if (first) *p2 = v2;
+    }
+  };
+
   for (int64_t k0 = ntile - 1; k0 >= 0; k0 -= BW_RING) {
 #pragma unroll
     for (int u = 0; u < BW_RING; ++u) {
@@ -368,7 +428,17 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
       const float hstart = dok ? hring[u] : 0.0f;
       load_tile(k - (BW_RING - 1), ring[(u + BW_RING - 1) % BW_RING]);
       hring[(u + BW_RING - 1) % BW_RING] = ck_load(k - (BW_RING - 1));
-      bw_barrier();
+      bw_barrier();  // tile k is staged, tile k+1's partials are complete
+
+      if (k + 1 < ntile) reduce_tile(k + 1, (int)((k + 1) & 1));
+      p_dlv = dlv;
+      p_sg = sg;
+      p_ds = ds;
+      p_gp = gp;
+      p_xv = xv;
+      p_dyv = dyv;
+      p_sv = sv;
+      p_live = live;
 
       // recompute a_t, q_t = a_t h_{t-1} and h_t of the tile; delta, delta*x
       // and B stay in registers for the backward walk
@@ -396,8 +466,8 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         }
       }
       // walk the tile backwards
-      float* const sp0 = &sm.sp[0][rr * BW_RS + n * BW_TS];
-      float* const sp1 = &sm.sp[1][rr * BW_RS + n * BW_TS];
+      float* const sp0 = &sm.sp[buf][0][rr * BW_RS + n * BW_TS];
+      float* const sp1 = &sm.sp[buf][1][rr * BW_RS + n * BW_TS];
       float pdx[BW_T], pdh[BW_T];  // lam delta x and ds h, summed over rows below
 #pragma unroll
       for (int q = BW_T - 4; q >= 0; q -= 4) {
@@ -425,64 +495,13 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
       {
         float o[4];
         rows4_sum(pdx, pdh, o);
-        *reinterpret_cast<float4*>(&sm.pw[wv][lane * 4]) = make_float4(o[0], o[1], o[2], o[3]);
-      }
-      bw_barrier();  // the partials are complete; the next tile stages the other buffer
-
-      // Role a sums over the states (ddelta, dx of row sr, step st), role b
-      // over the four wavefronts' row sums (this workgroup's share of dB, dC
-      // at step bt, state bn).  The stores are the same instructions for
-      // every lane, aimed at the trash slots where a lane has nothing to
-      // store.
-      float v0, v1, v2 = 0.f;
-      float *p0, *p1, *p2 = w.trash + tid;
-      if (role_a) {
-        float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-        for (int m = 0; m < BW_N; ++m) {
-          s1 += sm.sp[0][sr * BW_RS + m * BW_TS + swz(m, st)];
-          s2 += sm.sp[1][sr * BW_RS + m * BW_TS + swz(m, st)];
-        }
-        const float ddl = live ? (s1 + xv * s2) * sg : 0.0f;
-        v0 = ddl;
-        v1 = __builtin_fmaf(dlv, s2, first ? ds * Dsk : 0.0f);
-        const int64_t i = srow * L + (live ? k * BW_T + st : 0);
-        p0 = live ? a.ddelta + i : w.trash + tid;
-        p1 = live ? a.dx + i : w.trash + tid;
-        if constexpr (GATED) {
-          v2 = dyv * sv * gp;
-          p2 = live ? a.dz + i : w.trash + tid;
-        }
-        if (first) dD_acc = __builtin_fmaf(ds, xv, dD_acc);
-        db_acc += ddl;
-      } else {
-        // lane (bt / 4) * 16 + bn of each wavefront holds the dB sums of
-        // steps 4 (bt / 4) .. +3 at state bn, lane 32 more the dC sums
-        const int lb = (bt >> 2) * 16 + bn, tb = bt & 3;
-        float sb = 0.f, sc = 0.f;
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          sb += sm.pw[m][lb * 4 + tb];
-          sc += sm.pw[m][(32 + lb) * 4 + tb];
-        }
-        const int64_t t = k * BW_T + bt;
-        const int64_t i = ((b * G + g) * L + (t < L ? t : 0)) * BW_N + bn;
-        v0 = sb;
-        v1 = sc;
-        p0 = t < L ? w.dB_p + i : w.trash + tid;
-        p1 = t < L ? w.dC_p + i : w.trash + tid;
-      }
-      if (role_a && !first) {  // later state groups add to the sums over the states
-        v0 += *p0;
-        v1 += *p1;
-      }
-      *p0 = v0;
-      *p1 = v1;
-      if constexpr (GATED) {
-        if (first) *p2 = v2;
+        *reinterpret_cast<float4*>(&sm.pw[buf][wv][lane * 4]) =
+            make_float4(o[0], o[1], o[2], o[3]);
       }
     }
   }
+  bw_barrier();  // tile 0's partials are complete
+  reduce_tile(0, 0);
 
   if (dok && nok) {
     if (a.dh0) a.dh0[row * N + ns] = lam;
