@@ -44,6 +44,13 @@
  *    (a process-wide setting of the device's default pool).  SW_ERR_ALLOC if
  *    an allocation fails.
  *  - Threads using distinct streams may call concurrently.
+ *  - HIP graph capture: a call that uses neither the scratch nor a workspace
+ *    (the fused forward at N = 16 with L a multiple of 8 for bf16 or of 4
+ *    for fp32, 16-byte aligned arrays, and a workgroup's byte offsets below
+ *    2^31) can be captured and replayed: it launches kernels only.  A call that
+ *    uses the scratch is not replay-safe (a replay would repeat the ticket
+ *    and epoch values the host gave the captured launch), and the backward
+ *    allocates its workspace per call: do not capture those.
  */
 #ifndef SCANWEAVER_H
 #define SCANWEAVER_H
