@@ -525,6 +525,11 @@ def main(argv=None):
     kern = float(per.mean())
     hbm_gbs = abytes / kern / 1e9
     alu_achieved = SLOTS_PER_ELEM * elems / kern
+    # the library takes the 16-lane kernel for N = 16 unless SW_SS_LAYOUT=8 asks
+    # for the 8-lane one (rows whose offsets pass 2^31 also take the latter)
+    layout16 = os.environ.get("SW_SS_LAYOUT", "16") in ("", "16")
+    fwd_kernel = ("selective_blelloch_kernel" if args.schedule == "blelloch" else
+                  "selective_row16_kernel" if w.N == 16 and layout16 else "selective_fwd_kernel")
     out = {
         "metric": "selective-scan fwd B*L*D*N elems/s (+ achieved HBM GB/s vs peak), 1 GPU",
         "value": value,
@@ -554,9 +559,8 @@ def main(argv=None):
             "unit": "T fp32-lane-slot/s",
             "frac": alu_achieved / VALU_PEAK,
             "traffic": (measured_traffic(w) if args.schedule == "default" and not args.options
-                        and not args.ckpt else None),
-            "kernel": ("selective_blelloch_kernel" if args.schedule == "blelloch" else
-                       "selective_row16_kernel" if w.N == 16 else "selective_fwd_kernel"),
+                        and not args.ckpt and fwd_kernel == "selective_row16_kernel" else None),
+            "kernel": fwd_kernel,
             "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
                               "median": float(np.median(per)) * 1e6},
             "slots_per_elem": SLOTS_PER_ELEM,
