@@ -419,8 +419,7 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
         if (VEC && is_full(kt)) {
           if (ybf)
             *reinterpret_cast<uint2*>(y16_row + (t - tq)) =
-                make_uint2(bf16_rne(sv[0]) | (bf16_rne(sv[1]) << 16),
-                           bf16_rne(sv[2]) | (bf16_rne(sv[3]) << 16));
+                make_uint2(bf16x2_rne(sv[0], sv[1]), bf16x2_rne(sv[2], sv[3]));
           else
             *reinterpret_cast<float4*>(y_row + (t - tq)) = make_float4(sv[0], sv[1], sv[2], sv[3]);
         } else {

@@ -218,8 +218,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     if (dok && rh == 0 && t < L) {
       if (ybf)
         *reinterpret_cast<uint2*>(y16_row + t) =
-            make_uint2(bf16_rne(s4[0]) | (bf16_rne(s4[1]) << 16),
-                       bf16_rne(s4[2]) | (bf16_rne(s4[3]) << 16));
+            make_uint2(bf16x2_rne(s4[0], s4[1]), bf16x2_rne(s4[2], s4[3]));
       else
         *reinterpret_cast<float4*>(y_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
     }

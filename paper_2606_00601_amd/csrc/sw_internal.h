@@ -99,12 +99,15 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ float bf16_one(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// fp32 -> bf16 bits, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ uint32_t bf16_rne(float v) {
-  const uint32_t u = __float_as_uint(v);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+// fp32 -> bf16 bits, round to nearest even (NaN stays NaN), two at a time:
+// gfx950 converts a pair in one instruction (v_cvt_pk_bf16_f32); lo goes to
+// bits 0-15, hi to bits 16-31.
+typedef __bf16 sw_bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+  const sw_bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
+__device__ __forceinline__ uint32_t bf16_rne(float v) { return bf16x2_rne(v, 0.0f) & 0xffffu; }
 
 // softplus(v) = log(1 + e^v) in fp32 from the hardware exp2/log2/rcp, a few
 // ulps: e^-v is negligible past v = 16; log1p(u) = log(w) * u / (w - 1) with

@@ -393,6 +393,19 @@ def test_selective_mamba_options(sw, shape, dtype, opts):
                 f"h_last {dtype} {shape} {opts}")
 
 
+@pytest.mark.parametrize("shape", _EX_SHAPES)
+def test_selective_bf16_y_is_the_fp32_y_rounded(sw, shape):
+    """bf16 y is the fp32 y of the same call rounded once to nearest even:
+    bit-identical to torch's rounding of the fp32 output (both kernels)."""
+    B, D, N, L = shape
+    _say("case bf16 y rounding", shape)
+    opts = ("h0", "bias", "softplus", "z")
+    inp, ex = _ex_inputs(B, D, N, L, 8100 + B + D + N + L, "bf16", opts)
+    y32, _ = _run_ex(sw, inp, ex, "bf16", True, False)
+    y16, _ = _run_ex(sw, inp, ex, "bf16", True, True)
+    assert torch.equal(y16, y32.to(torch.bfloat16))
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("layout", ["16", "8"])
 def test_selective_continued_across_calls_bitexact(sw, monkeypatch, dtype, layout):
