@@ -273,7 +273,6 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
         read_ops(ops[nb % R16_NS], buf, nb);
       else if (has_next)
         read_ops(ops[nb % R16_NS], nbuf, nb - R16_NB);
-      __builtin_amdgcn_sched_barrier(0);
       if constexpr (CK) {
         // the state before step kt*T + 4*bi; rows past D write the same
         // values as row D-1 to row D-1's slots
@@ -310,7 +309,6 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
       }
       *reinterpret_cast<float4*>(p_w + 4 * bi) = make_float4(p4[0], p4[1], p4[2], p4[3]);
       if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, yx_prev, gt_prev);
-      __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
