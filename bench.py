@@ -9,9 +9,11 @@ resident in HBM.  Several input sets are rotated so that the working set is
 larger than the 256 MB MALL and each step streams its inputs from HBM.
 
 Prints one JSON line: throughput in B*L*D*N elements/s over exactly K timed
-steps, the roofline of the kernel (per-launch duration from HIP events on the
-launch stream), the HBM bandwidth it reaches, and the CPU oracle timed on the
-host cores over a bounded sample of the same workload.
+steps run back to back after W untimed ones, the roofline of the kernel (mean
+launch duration = the interval between HIP events recorded on the launch
+stream around the K steps, divided by K; the spread of single launches from an
+untimed pass afterwards), the HBM bandwidth it reaches, and the CPU oracle
+timed on the host cores over a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -203,25 +205,54 @@ def measure_copy_bandwidth(mib: int = 2048, reps: int = 10) -> dict:
             "frac_of_peak": 2 * n * 4 / sec / 1e9 / HBM_PEAK_GBS}
 
 
+SPREAD_LAUNCHES = 100
+
+
 def time_launches(step, steps, warmup):
-    """Run warmup steps, then `steps` timed ones; returns (wall seconds, per-launch seconds)."""
+    """Run `warmup` untimed steps, then exactly `steps` timed ones, back to back,
+    between one pair of HIP events on the launch stream.
+
+    Returns (wall seconds of the timed steps, GPU seconds per launch over them,
+    per-launch seconds of a further untimed pass with an event pair around each
+    launch).  The per-launch average comes from the timed region itself: event
+    pairs around every launch put a marker between kernels that idles the GPU
+    for a few microseconds each, so they are kept out of the timed region and
+    serve only the spread (std, median) of the launch durations.
+    """
     import torch
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    e0.record(stream)
     for i in range(steps):
-        ev[i][0].record(stream)
         step(i)
-        ev[i][1].record(stream)
+    e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per = np.array([a.elapsed_time(b) * 1e-3 for a, b in ev])
-    return wall, per
+    gpu_per = e0.elapsed_time(e1) * 1e-3 / max(steps, 1)
+    n = min(steps, SPREAD_LAUNCHES)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n)]
+    for i in range(n):
+        ev[i][0].record(stream)
+        step(steps + i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    spread = np.array([a.elapsed_time(b) * 1e-3 for a, b in ev])
+    return wall, gpu_per, spread
+
+
+def launch_stats(gpu_per, spread):
+    """The per_launch_us object of a bench line."""
+    return {"mean": gpu_per * 1e6, "std": float(spread.std()) * 1e6,
+            "median": float(np.median(spread)) * 1e6,
+            "mean_of_spread_pass": float(spread.mean()) * 1e6, "spread_launches": len(spread),
+            "method": "mean: HIP events around the timed steps / steps; std, median: an "
+                      "untimed pass after them with an event pair around each launch"}
 
 
 def bench_affine(w, args):
@@ -265,8 +296,7 @@ def bench_affine(w, args):
         else:
             sw.affine_scan_schedule(a, bx, out=h, schedule=args.schedule)
 
-    wall, per = time_launches(step, args.steps, args.warmup)
-    kern = float(per.mean())
+    wall, kern, per = time_launches(step, args.steps, args.warmup)
     gbs = abytes / kern / 1e9
     # the library walks each row in one workgroup once the rows alone fill the
     # GPU (>= 8 per CU) and a row is longer than one 2048-step chunk
@@ -292,8 +322,7 @@ def bench_affine(w, args):
                      "traffic": (measured_traffic(w) if args.schedule == "default" and not proj
                                  and not args.int32 else None),
                      "kernel": kname,
-                     "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
-                                       "median": float(np.median(per)) * 1e6}},
+                     "per_launch_us": launch_stats(kern, per)},
     }
     if cpu is not None:
         out["cpu_baseline"] = cpu
@@ -345,8 +374,7 @@ def bench_bwd(w, args):
         sw.selective_scan_bwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], dy_t,
                               ckpt=ck)
 
-    wall, per = time_launches(step, args.steps, args.warmup)
-    kern = float(per.mean())
+    wall, kern, per = time_launches(step, args.steps, args.warmup)
     elems = w.elems
     # algorithmic bytes: x, delta, dy read; dx, ddelta written (fp32); B, C
     # read, dB, dC written (fp32); A, Dskip read, dA, dDskip, dh0 written
@@ -365,8 +393,7 @@ def bench_bwd(w, args):
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                      "unit": "T fp32-lane-slot/s", "frac": achieved / VALU_PEAK,
                      "traffic": None, "kernel": "selective_bwd_kernel + selective_bwd_reduce_kernel",
-                     "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
-                                       "median": float(np.median(per)) * 1e6},
+                     "per_launch_us": launch_stats(kern, per),
                      "slots_per_elem": SLOTS_PER_ELEM_BWD},
         "hbm": {"algorithmic_bytes": abytes, "achieved_GBs": abytes / kern / 1e9,
                 "peak_GBs": HBM_PEAK_GBS, "frac": abytes / kern / 1e9 / HBM_PEAK_GBS},
@@ -506,26 +533,10 @@ def main(argv=None):
             sw.selective_scan_fwd_schedule(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"],
                                            s["Dskip"], schedule=args.schedule)
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-
-    stream = torch.cuda.current_stream(dev)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        ev[i][0].record(stream)
-        step(i)
-        ev[i][1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    per = np.array([a.elapsed_time(b) * 1e-3 for a, b in ev])  # seconds per launch
+    wall, kern, per = time_launches(step, args.steps, args.warmup)
 
     elems = w.elems
     value = elems * args.steps / wall
-    kern = float(per.mean())
     hbm_gbs = abytes / kern / 1e9
     alu_achieved = SLOTS_PER_ELEM * elems / kern
     # the library takes the 16-lane kernel for N = 16 unless SW_SS_LAYOUT=8 asks
@@ -564,8 +575,7 @@ def main(argv=None):
             "traffic": (measured_traffic(w) if args.schedule == "default" and not args.options
                         and not args.ckpt and fwd_kernel == "selective_row16_kernel" else None),
             "kernel": fwd_kernel,
-            "per_launch_us": {"mean": kern * 1e6, "std": float(per.std()) * 1e6,
-                              "median": float(np.median(per)) * 1e6},
+            "per_launch_us": launch_stats(kern, per),
             "slots_per_elem": SLOTS_PER_ELEM,
         },
         "hbm": {"algorithmic_bytes": abytes, "achieved_GBs": hbm_gbs, "peak_GBs": HBM_PEAK_GBS,
