@@ -138,13 +138,16 @@ def cpu_baseline(w, inp, target_s: float = 12.0, max_rows: int | None = None, th
         rows = min(R, rows * 4, max_rows or R)
         dt = run(rows)
     reps = 1
-    while dt < 0.25:  # the whole workload is short: repeat it
-        reps *= 4
+    import oracle as _o
+    used = _o.threads_used(cores, rows)
+    # the whole workload is short: repeat it until the sample is about 12 s of
+    # CPU work (wall time x threads)
+    while dt * used < 12.0 and dt < 30.0:
+        reps *= 2
         dt = sum(run(rows) for _ in range(reps))
     elems = rows * w.L * w.N * reps
-    import oracle as _o
     return {
-        "value": elems / dt, "unit": "elems/s", "cores": _o.threads_used(cores, rows),
+        "value": elems / dt, "unit": "elems/s", "cores": used,
         "kind": "oracle",
         "sample": f"{rows} of {R} (b,d) rows x L={w.L} x N={w.N} of {w.name}"
                   + (f", {reps} repeats" if reps > 1 else "") + f", fp64, {dt:.1f} s wall",
