@@ -1,0 +1,63 @@
+"""bench.py's host-side parts (no GPU): the algorithmic byte counts against
+the sizes of the five workloads, the roofline peak from the unit counts, the
+traffic records and their source hashes, and the one-GPU guard."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+
+import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_algorithmic_bytes_of_the_fused_workloads():
+    # x, delta (B,D,L) + B, C (B,L,N) in the input dtype, A (D,N) and Dskip (D)
+    # fp32, y (B,D,L) and h_last (B,D,N) fp32: the sizes of the workloads
+    expect = {
+        "selective_f32_b2_d256_n16_l512": 3_326_976,
+        "selective_bf16_b8_d1536_n16_l2048": 203_266_048,
+        "selective_f32_b1_d5120_n16_l65536": 4_035_596_288,
+        "selective_f32_b4_d2048_n16_l8192_stress": 810_164_224,
+    }
+    for name, nbytes in expect.items():
+        assert bench.algorithmic_bytes(wl.workload(name)) == nbytes, name
+
+
+def test_valu_peak_is_the_fp32_vector_rate_in_lane_slots():
+    # 157.3 TFLOP/s of fp32 vector FMA = 78.6e12 lane-slots/s (an FMA is one slot)
+    assert abs(bench.VALU_PEAK - 256 * 4 * 32 * 2.4e9) < 1.0
+    assert abs(2 * bench.VALU_PEAK / 1e12 - 157.3) < 0.1
+
+
+def test_traffic_records_match_their_sources_and_workloads():
+    for name, rec in bench.TRAFFIC_RECORDS.items():
+        w = wl.workload(name)
+        path = os.path.join(ROOT, "profiles", rec)
+        assert os.path.exists(path), rec
+        text = open(path).read()
+        assert f"kernel_source_sha256: {bench.kernel_source_sha256(w.path)}" in text, rec
+        t = bench.measured_traffic(w)
+        alg = 12 * w.elems if w.path == "affine" else bench.algorithmic_bytes(w)
+        # every algorithmic byte moves at least once, and not many twice
+        assert t is not None and alg <= t <= 1.2 * alg, (rec, t, alg)
+    # no record for a workload without one, and the hashes differ by path
+    assert bench.measured_traffic(wl.workload("selective_f32_b2_d256_n16_l512")) is None
+    assert bench.kernel_source_sha256("affine") != bench.kernel_source_sha256("selective")
+
+
+def test_launch_stats_fields():
+    st = bench.launch_stats(100e-6, np.array([101e-6, 99e-6, 100e-6]))
+    assert abs(st["mean"] - 100.0) < 1e-9
+    assert abs(st["median"] - 100.0) < 1e-9
+    assert st["spread_launches"] == 3
+
+
+def test_more_than_one_gpu_is_refused():
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr
