@@ -365,17 +365,34 @@ def bench_bwd(w, args):
 
     t = {k: to_dev(k) for k in ("x", "delta", "A", "Bm", "Cm", "Dskip")}
     del inp
+    opt = {}
+    if args.options:
+        # the Mamba-block inputs: gate z (the input dtype), delta bias with
+        # softplus, initial state
+        orng = np.random.Generator(np.random.PCG64(w.seed + 200))
+        z = orng.standard_normal(size=(w.B, w.D, w.L)).astype(np.float32)
+        opt["z"] = (torch.from_numpy(wl.bf16_round(z).view(np.int16)).to(dev).view(torch.bfloat16)
+                    if w.dtype == "bf16" else torch.from_numpy(z).to(dev))
+        opt["delta_bias"] = torch.from_numpy(
+            orng.uniform(-2.0, 0.0, size=w.D).astype(np.float32)).to(dev)
+        opt["h0"] = torch.from_numpy(
+            orng.standard_normal(size=(w.B, w.D, w.N)).astype(np.float32)).to(dev)
+        opt["delta_softplus"] = True
 
-    ck = None
+    ck = sp = None
     if args.ckpt:
-        # the forward's checkpoints, as a training step would hand them over
+        # the forward's checkpoints (and, with the gate, its output before the
+        # gate), as a training step would hand them over
         ck = sw.new_ckpt(t["x"], w.N)
-        sw.selective_scan_fwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], ckpt=ck)
+        if "z" in opt:
+            sp = torch.empty((w.B, w.D, w.L), dtype=torch.float32, device=dev)
+        sw.selective_scan_fwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], ckpt=ck,
+                              s_pre=sp, **opt)
         torch.cuda.synchronize()
 
     def step(i):
         sw.selective_scan_bwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], dy_t,
-                              ckpt=ck)
+                              ckpt=ck, s_pre=sp, **opt)
 
     wall, kern, per = time_launches(step, args.steps, args.warmup)
     elems = w.elems
@@ -383,6 +400,9 @@ def bench_bwd(w, args):
     # read, dB, dC written (fp32); A, Dskip read, dA, dDskip, dh0 written
     abytes = (3 * es + 8) * w.B * w.D * w.L + (2 * es + 8) * w.B * w.L * w.N \
         + 8 * w.D * w.N + 8 * w.D + 4 * w.B * w.D * w.N
+    if args.options:
+        # z read, dz written; delta bias read, its gradient written; h0 read
+        abytes += (es + 4) * w.B * w.D * w.L + 8 * w.D + 4 * w.B * w.D * w.N
     achieved = SLOTS_PER_ELEM_BWD * elems / kern
     out = {
         "metric": "selective-scan bwd B*L*D*N elems/s (all gradients), 1 GPU",
@@ -392,6 +412,8 @@ def bench_bwd(w, args):
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "D": w.D, "N": w.N, "L": w.L,
                    "pass": "backward", "dy": w.dtype, "gradients": "fp32",
+                   "options": ("gate z, delta bias + softplus, initial state" if args.options
+                               else "none"),
                    "forward_checkpoints": bool(args.ckpt)},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                      "unit": "T fp32-lane-slot/s", "frac": achieved / VALU_PEAK,
@@ -429,8 +451,8 @@ def main(argv=None):
                     help="training mode: the forward writes 8-step checkpoints, the backward "
                          "takes them")
     ap.add_argument("--options", action="store_true",
-                    help="forward with the Mamba-block inputs (gate, delta bias + softplus, "
-                         "initial state, y in the input dtype)")
+                    help="with the Mamba-block inputs (gate, delta bias + softplus, initial "
+                         "state; the forward's y in the input dtype), forward or backward")
     ap.add_argument("--form", choices=("bare", "proj"), default="bare",
                     help="bare-scan workloads: the plain scan or the Eq. (3)-(4) projection form")
     ap.add_argument("--sets", type=int, default=0,

@@ -237,15 +237,17 @@ int sw_selective_scan_fwd_ex(const void* x, const void* delta, const float* A, c
  * (training): ckpt (B, D, ceil(L/8), 16) fp32, required, receives the state
  * h[b,d,8k-1,n] before step 8k (h0, or zero, for k = 0) in slot
  * [b, d, k, n]; slots n >= N hold no state.  N <= 16 (SW_ERR_UNSUPPORTED
- * above).  Handing ckpt to sw_selective_scan_bwd with the same inputs spares
- * the backward its own forward sweep.  Otherwise as
- * sw_selective_scan_fwd_ex.
+ * above).  s_pre (B, D, L) fp32, or NULL, receives y before the output gate
+ * (y = s_pre * silu(z); without z, s_pre = y in fp32).  Handing ckpt (and,
+ * with z, s_pre) to sw_selective_scan_bwd with the same inputs spares the
+ * backward its own forward sweep (and its forward without the gate).
+ * Otherwise as sw_selective_scan_fwd_ex.
  */
 int sw_selective_scan_fwd_train(const void* x, const void* delta, const float* A, const void* Bm,
                                 const void* Cm, const float* Dskip, const void* z,
                                 const float* delta_bias, const float* h0, void* y, float* h_last,
-                                float* ckpt, int64_t B, int64_t D, int64_t N, int64_t L,
-                                int in_dtype, int out_dtype, int flags);
+                                float* ckpt, float* s_pre, int64_t B, int64_t D, int64_t N,
+                                int64_t L, int in_dtype, int out_dtype, int flags);
 
 /*
  * Backward of sw_selective_scan_fwd_ex: the gradients of
@@ -262,6 +264,10 @@ int sw_selective_scan_fwd_train(const void* x, const void* delta, const float* A
  *   dh_last : (B, D, N) fp32 or NULL (zero)
  *   ckpt    : the ckpt of sw_selective_scan_fwd_train on the same inputs,
  *             or NULL (the backward then rebuilds it in its workspace)
+ *   s_pre   : with z, the s_pre of sw_selective_scan_fwd_train on the same
+ *             inputs, or NULL (the backward then reruns the forward without
+ *             the gate, which also writes the checkpoints when N <= 16);
+ *             SW_ERR_INVALID_ARG without z
  * Outputs (fp32, overwritten, never accumulated into):
  *   dx, ddelta : (B, D, L), required; ddelta is with respect to the delta
  *                passed in (before bias and softplus)
@@ -282,7 +288,8 @@ int sw_selective_scan_fwd_train(const void* x, const void* delta, const float* A
 int sw_selective_scan_bwd(const void* x, const void* delta, const float* A, const void* Bm,
                           const void* Cm, const float* Dskip, const void* z,
                           const float* delta_bias, const float* h0, const void* dy,
-                          const float* dh_last, const float* ckpt, float* dx, float* ddelta,
+                          const float* dh_last, const float* ckpt, const float* s_pre,
+                          float* dx, float* ddelta,
                           float* dA, float* dB,
                           float* dC, float* dDskip, float* dz, float* ddelta_bias, float* dh0,
                           int64_t B, int64_t D, int64_t N, int64_t L, int in_dtype, int dy_dtype,

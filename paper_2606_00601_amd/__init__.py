@@ -149,7 +149,7 @@ def affine_scan_proj_i32(a, b, x=None, c=None, h0=None, *, y=None, want_h_last=T
 
 def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
                        want_h_last=True, z=None, delta_bias=None, h0=None,
-                       delta_softplus=False, y_dtype=torch.float32, ckpt=None):
+                       delta_softplus=False, y_dtype=torch.float32, ckpt=None, s_pre=None):
     """Fused selective scan forward; returns ``(y, h_last)`` (h_last None if not wanted).
 
     x, delta: (B, D, L); A: (D, N) fp32; Bm, Cm: (B, L, N); Dskip: (D,) fp32 or None.
@@ -157,13 +157,18 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
     fp32 or bf16 (``y_dtype``).  Optional inputs of a Mamba block: ``z``
     (B, D, L) gates the output by silu(z); ``delta_bias`` (D,) fp32 is added to
     delta, then ``delta_softplus`` applies softplus; ``h0`` (B, D, N) fp32 is
-    the initial state (e.g. the h_last of the previous chunk).
+    the initial state (e.g. the h_last of the previous chunk).  Training:
+    ``ckpt=new_ckpt(x, N)`` (N <= 16) receives the 8-step checkpoints and
+    ``s_pre`` (B, D, L) fp32 (with ckpt) the output before the gate, both for
+    :func:`selective_scan_bwd`.
     """
     if not isinstance(x, torch.Tensor) or x.dim() != 3:
         raise ValueError("x must be a (B, D, L) tensor")
     dt = x.dtype
     if dt not in (torch.float32, torch.bfloat16):
         raise TypeError("x must be float32 or bfloat16")
+    if s_pre is not None and ckpt is None:
+        raise ValueError("s_pre is written by the training forward: pass ckpt too")
     if y_dtype not in (torch.float32, torch.bfloat16):
         raise TypeError("y_dtype must be float32 or bfloat16")
     B, D, L = x.shape
@@ -200,13 +205,15 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
     flags = SW_DELTA_SOFTPLUS if delta_softplus else 0
     if ckpt is not None:
         _need(ckpt, "ckpt", torch.float32, (B, D, (L + 7) // 8, 16))
+    if s_pre is not None:
+        _need(s_pre, "s_pre", torch.float32, (B, D, L))
     with torch.cuda.device(x.device):
         _bind_stream(x.device)
         if ckpt is not None:
             check(lib().sw_selective_scan_fwd_train(
                 _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
-                _ptr(delta_bias), _ptr(h0), _ptr(y), _ptr(h_last), _ptr(ckpt), B, D, N, L,
-                in_dt, out_dt, flags), "sw_selective_scan_fwd_train")
+                _ptr(delta_bias), _ptr(h0), _ptr(y), _ptr(h_last), _ptr(ckpt), _ptr(s_pre),
+                B, D, N, L, in_dt, out_dt, flags), "sw_selective_scan_fwd_train")
         elif z is None and delta_bias is None and h0 is None and not flags \
                 and out_dt == SW_DTYPE_F32:
             fn = lib().sw_selective_scan_fwd if dt == torch.float32 \
@@ -264,7 +271,7 @@ def new_ckpt(x, N):
 
 
 def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, delta_bias=None,
-                       h0=None, delta_softplus=False, want_dh0=True, ckpt=None):
+                       h0=None, delta_softplus=False, want_dh0=True, ckpt=None, s_pre=None):
     """Backward of :func:`selective_scan_fwd`: gradients of sum(dy * y) +
     sum(dh_last * h_last) with respect to every input.
 
@@ -303,6 +310,8 @@ def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, 
         _need(dh_last, "dh_last", torch.float32, (B, D, N))
     if ckpt is not None:
         _need(ckpt, "ckpt", torch.float32, (B, D, (L + 7) // 8, 16))
+    if s_pre is not None:
+        _need(s_pre, "s_pre", torch.float32, (B, D, L))
     dev = x.device
     f32 = dict(dtype=torch.float32, device=dev)
     out = {"dx": torch.empty((B, D, L), **f32), "ddelta": torch.empty((B, D, L), **f32),
@@ -319,7 +328,8 @@ def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, 
         _bind_stream(dev)
         check(lib().sw_selective_scan_bwd(
             _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
-            _ptr(delta_bias), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(ckpt), _ptr(out["dx"]),
+            _ptr(delta_bias), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(ckpt), _ptr(s_pre),
+            _ptr(out["dx"]),
             _ptr(out["ddelta"]), _ptr(out["dA"]), _ptr(out["dB"]), _ptr(out["dC"]),
             _ptr(out["dDskip"]), _ptr(out["dz"]), _ptr(out["ddelta_bias"]), _ptr(out["dh0"]),
             B, D, N, L, in_dt, dy_dt, SW_DELTA_SOFTPLUS if delta_softplus else 0),
@@ -328,24 +338,27 @@ def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, 
 
 
 class _SelectiveScanFn(torch.autograd.Function):
-    """Autograd glue: the forward keeps its 8-step checkpoints (N <= 16) and the
-    backward runs sw_selective_scan_bwd; no arithmetic happens here."""
+    """Autograd glue: the forward keeps its 8-step checkpoints (N <= 16) and,
+    with a gate, its output before the gate; the backward runs
+    sw_selective_scan_bwd on them; no arithmetic happens here."""
 
     @staticmethod
     def forward(ctx, x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, delta_softplus):
         N = A.shape[1]
         ck = new_ckpt(x, N) if N <= 16 else None
+        sp = (torch.empty(x.shape, dtype=torch.float32, device=x.device)
+              if ck is not None and z is not None else None)
         y, h_last = selective_scan_fwd(x, delta, A, Bm, Cm, Dskip, z=z, delta_bias=delta_bias,
                                        h0=h0, delta_softplus=delta_softplus, ckpt=ck,
-                                       y_dtype=torch.float32)
-        ctx.save_for_backward(x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, ck)
+                                       s_pre=sp, y_dtype=torch.float32)
+        ctx.save_for_backward(x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, ck, sp)
         ctx.delta_softplus = delta_softplus
         ctx.set_materialize_grads(False)
         return y, h_last
 
     @staticmethod
     def backward(ctx, dy, dh_last):
-        x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, ck = ctx.saved_tensors
+        x, delta, A, Bm, Cm, Dskip, z, delta_bias, h0, ck, sp = ctx.saved_tensors
         if dy is None:  # only h_last reached the loss
             dy = torch.zeros(x.shape, dtype=torch.float32, device=x.device)
         dy = dy.contiguous().to(torch.float32)
@@ -353,7 +366,8 @@ class _SelectiveScanFn(torch.autograd.Function):
             dh_last = dh_last.contiguous().to(torch.float32)
         g = selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last, z=z, delta_bias=delta_bias,
                                h0=h0, delta_softplus=ctx.delta_softplus,
-                               want_dh0=h0 is not None and h0.requires_grad, ckpt=ck)
+                               want_dh0=h0 is not None and h0.requires_grad, ckpt=ck,
+                               s_pre=sp)
         cast = lambda t, like: None if t is None else t.to(like.dtype)  # noqa: E731
         return (cast(g["dx"], x), cast(g["ddelta"], delta), g["dA"], cast(g["dB"], Bm),
                 cast(g["dC"], Cm), g.get("dDskip"), cast(g.get("dz"), z) if z is not None else None,

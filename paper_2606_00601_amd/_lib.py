@@ -32,8 +32,8 @@ SIGNATURES = {
     "sw_selective_scan_fwd_schedule": (_int, [_vp] * 8 + [_i64] * 4 + [_int] * 2),
     "sw_affine_scan_schedule_i32": (_int, [_vp] * 4 + [_i64] * 3 + [_int]),
     "sw_affine_scan_proj": (_int, [_vp] * 7 + [_i64] * 3),
-    "sw_selective_scan_bwd": (_int, [_vp] * 21 + [_i64] * 4 + [_int] * 3),
-    "sw_selective_scan_fwd_train": (_int, [_vp] * 12 + [_i64] * 4 + [_int] * 3),
+    "sw_selective_scan_bwd": (_int, [_vp] * 22 + [_i64] * 4 + [_int] * 3),
+    "sw_selective_scan_fwd_train": (_int, [_vp] * 13 + [_i64] * 4 + [_int] * 3),
     "sw_affine_scan_proj_i32": (_int, [_vp] * 7 + [_i64] * 3),
     "sw_selective_scan_fwd": (_int, [_vp] * 8 + [_i64] * 4),
     "sw_selective_scan_fwd_bf16": (_int, [_vp] * 8 + [_i64] * 4),

@@ -645,7 +645,8 @@ int selective_bwd(const BwdArgs& a) {
     return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
   const size_t R = (size_t)(B * D);
   // without the forward's checkpoints the kernel rebuilds them in a workspace
-  const size_t n_ck = a.ckpt ? 0 : R * (size_t)ntile * BW_N, n_s = a.z ? R * (size_t)L : 0;
+  const size_t n_ck = a.ckpt ? 0 : R * (size_t)ntile * BW_N;
+  const size_t n_s = (a.z && !a.s_pre) ? R * (size_t)L : 0;
   const size_t n_dA = R * BW_N, n_bc = (size_t)(B * G) * (size_t)L * BW_N;
   const size_t total = n_ck + n_s + n_dA + 2 * R + 2 * n_bc + 256;
   void* base = nullptr;
@@ -655,8 +656,8 @@ int selective_bwd(const BwdArgs& a) {
   BwWork w;
   w.ck = a.ckpt ? const_cast<float*>(a.ckpt) : f;  // read-only when given
   f += n_ck;
-  float* s_pre = a.z ? f : nullptr;
-  w.s = s_pre;
+  float* s_pre = (a.z && !a.s_pre) ? f : nullptr;
+  w.s = a.s_pre ? a.s_pre : s_pre;
   f += n_s;
   w.dA_p = f;
   f += n_dA;
@@ -669,7 +670,11 @@ int selective_bwd(const BwdArgs& a) {
   w.dC_p = f;
   f += n_bc;
   w.trash = f;
-  if (a.z) {
+  // with a gate, the forward without the gate runs anyway (for the pre-gate
+  // output); for N <= 16 it also writes the tile checkpoints, so the backward
+  // kernel skips its own forward sweep (the checkpoints are bit-identical)
+  BwdArgs ab = a;
+  if (a.z && !a.s_pre) {
     // the pre-gate output: the forward pass without the gate
     SelArgs fa{};
     fa.x = a.x;
@@ -688,6 +693,10 @@ int selective_bwd(const BwdArgs& a) {
     fa.bf16_in = a.bf16_in;
     fa.softplus = a.softplus;
     fa.vec = a.vec;
+    if (!a.ckpt && a.N <= BW_N) {
+      fa.ckpt = w.ck;
+      ab.ckpt = w.ck;
+    }
     st = selective_fwd(fa);
     if (st != SW_OK) {
       workspace_free(base, s);
@@ -697,7 +706,7 @@ int selective_bwd(const BwdArgs& a) {
   // the states in groups of 16: each group's main kernel, then its reduction
   // (dA, dB, dC of its states; the sums over the states accumulate)
   for (int n0 = 0; n0 < a.N && st == SW_OK; n0 += BW_N) {
-    launch_bwd(a, w, G, ntile, grid, n0, s);
+    launch_bwd(ab, w, G, ntile, grid, n0, s);
     st = check_launch("selective_bwd_kernel");
     if (st != SW_OK) break;
     int64_t work = 2 * B * L * (BW_N / 4);

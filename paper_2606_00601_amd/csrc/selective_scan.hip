@@ -251,7 +251,8 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
     void* __restrict__ yv, float* __restrict__ h_last, int64_t D, int N, int64_t L, int64_t ndb,
     int64_t nrb, int64_t Lc, int64_t nchunks, uint32_t ntasks,
     unsigned long long* __restrict__ carry, uint32_t* __restrict__ ticket, uint32_t tbase,
-    uint32_t epoch, uint32_t flags_in, float* __restrict__ ck, int64_t nT8) {
+    uint32_t epoch, uint32_t flags_in, float* __restrict__ ck, int64_t nT8,
+    float* __restrict__ s_out) {
   static_assert(!CK || NPL <= 2, "checkpoints hold 16 states per row");
   constexpr int T = SS_T;
   const uint32_t flags = OPT ? flags_in : 0u;
@@ -296,6 +297,8 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
     const bool ybf = (flags & SEL_Y_BF16) != 0;
     float* const y_row = static_cast<float*>(yv) + (b * D + dcl) * L + tq;
     uint16_t* const y16_row = static_cast<uint16_t*>(yv) + (b * D + dcl) * L + tq;
+    // OPT: y before the output gate, for the backward of a gated call (or NULL)
+    float* const s_row = (OPT && s_out) ? s_out + (b * D + dcl) * L + tq : nullptr;
     float Al[NPL], hs[NPL];
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
@@ -412,6 +415,17 @@ __global__ __launch_bounds__(64) void selective_fwd_kernel(
         sv[1] += pr[gg].y;
         sv[2] += pr[gg].z;
         sv[3] += pr[gg].w;
+      }
+      if constexpr (OPT) {
+        if (s_row && dok) {
+          if (VEC && is_full(kt)) {
+            *reinterpret_cast<float4*>(s_row + (t - tq)) = make_float4(sv[0], sv[1], sv[2], sv[3]);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              if (t + q < te) s_row[t - tq + q] = sv[q];
+          }
+        }
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) sv[q] *= gt[q];
@@ -580,7 +594,7 @@ int make_plan(int64_t B, int64_t D, int64_t L, Plan* p) {
 
 template <typename IN, int NPL, bool VEC, bool NPADDED>
 int launch_cfg(const SelArgs& a, hipStream_t s) {
-  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16;
+  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.s_out;
   Plan p;
   int st = make_plan(a.B, a.D, a.L, &p);
   if (st != SW_OK) return st;
@@ -604,7 +618,7 @@ int launch_cfg(const SelArgs& a, hipStream_t s) {
                      static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
                      a.delta_bias, a.h0, a.y, a.h_last, a.D, (int)a.N, a.L, p.ndb, p.nrb, p.Lc,
                      p.nchunks, p.ntasks, ss.carry, ss.ticket, ss.ticket_base, ss.epoch, flags,
-                     a.ckpt, (a.L + 7) / 8);
+                     a.ckpt, (a.L + 7) / 8, a.s_out);
   st = check_launch("selective_fwd_kernel");
   if (st != SW_OK) ss.invalidate();
   return st;

@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     const IN* __restrict__ Bm, const IN* __restrict__ Cm, const float* __restrict__ Dskip,
     const IN* __restrict__ z, const float* __restrict__ dbias, const float* __restrict__ h0,
     void* __restrict__ yv, float* __restrict__ h_last, int64_t D, int64_t L, int64_t ndb,
-    uint32_t flags_in, float* __restrict__ ck, int64_t nT8) {
+    uint32_t flags_in, float* __restrict__ ck, int64_t nT8, float* __restrict__ s_out) {
   constexpr int ES = (int)sizeof(IN);
   const uint32_t flags = OPT ? flags_in : 0u;
   constexpr int V = 16 / ES;              // steps a lane holds of a super-tile
@@ -194,6 +194,8 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   float* const p_w = &sm.p[w][r * R16_PRS + n * R16_TS];
   const float* const p_r = &sm.p[w][r * R16_PRS + 8 * rh * R16_TS + 4 * rq];
   float* const y_row = static_cast<float*>(yv) + (b * D + dcl) * L;
+  // OPT: y before the output gate, for the backward of a gated call (or NULL)
+  float* const s_row = (OPT && s_out) ? s_out + (b * D + dcl) * L : nullptr;
   uint16_t* const y16_row = static_cast<uint16_t*>(yv) + (b * D + dcl) * L;
 
   auto read_partials = [&](float4 (&pr)[8]) {
@@ -210,11 +212,16 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
       s4[2] += pr[i].z;
       s4[3] += pr[i].w;
     }
-    // add the other half of the row (lane n ^ 8), then Dskip*x
+    // add the other half of the row (lane n ^ 8), then Dskip*x, then the gate
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      s4[q] = __builtin_fmaf(dsk, yx[q], s4[q] + row_ror8(s4[q])) * gt[q];
+    for (int q = 0; q < 4; ++q) s4[q] = __builtin_fmaf(dsk, yx[q], s4[q] + row_ror8(s4[q]));
     const int64_t t = kt * R16_T + 4 * rq;
+    if constexpr (OPT) {
+      if (s_row && dok && rh == 0 && t < L)
+        *reinterpret_cast<float4*>(s_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s4[q] *= gt[q];
     if (dok && rh == 0 && t < L) {
       if (ybf)
         *reinterpret_cast<uint2*>(y16_row + t) =
@@ -362,7 +369,7 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
 
 template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s) {
-  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16;
+  const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.s_out;
   const int64_t ndb = (a.D + R16_ROWS - 1) / R16_ROWS;
   const int64_t grid = a.B * ndb;
   if (grid >= ((int64_t)1 << 31))
@@ -377,7 +384,7 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
                      static_cast<const IN*>(a.delta), a.A, static_cast<const IN*>(a.Bm),
                      static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
                      a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L, ndb, flags, a.ckpt,
-                     (a.L + 7) / 8);
+                     (a.L + 7) / 8, a.s_out);
   return check_launch("selective_row16_kernel");
 }
 

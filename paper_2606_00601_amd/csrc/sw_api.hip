@@ -217,18 +217,19 @@ int selective_common(SelArgs a) {
   if ((st = check_ptr(a.y, ys, "y", true, dev)) != SW_OK) return st;
   if ((st = check_ptr(a.h_last, 4, "h_last", false, dev)) != SW_OK) return st;
   if ((st = check_ptr(a.ckpt, 4, "ckpt", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.s_out, 4, "s_pre", false, dev)) != SW_OK) return st;
   if (a.ckpt && N > 16)
     return fail(SW_ERR_UNSUPPORTED, "checkpoints need N <= 16 (got %lld)", (long long)N);
   const size_t nck = (size_t)R * (size_t)((L + 7) / 8) * 16;
   Span outs[] = {{a.y, (size_t)nx * ys, "y"}, {a.h_last, (size_t)nh * 4, "h_last"},
-                 {a.ckpt, nck * 4, "ckpt"}};
+                 {a.ckpt, nck * 4, "ckpt"}, {a.s_out, (size_t)nx * 4, "s_pre"}};
   Span ins[] = {{a.x, (size_t)nx * es, "x"},          {a.delta, (size_t)nx * es, "delta"},
                 {a.A, (size_t)(D * N) * 4, "A"},      {a.Bm, (size_t)nbc * es, "Bm"},
                 {a.Cm, (size_t)nbc * es, "Cm"},       {a.Dskip, (size_t)D * 4, "Dskip"},
                 {a.z, (size_t)nx * es, "z"},          {a.delta_bias, (size_t)D * 4, "delta_bias"},
                 {a.h0, (size_t)nh * 4, "h0"}};
-  if ((st = check_spans(outs, 3, ins, 9)) != SW_OK) return st;
-  a.vec = L % 4 == 0 && all_aligned16({a.x, a.delta, a.y, a.z});
+  if ((st = check_spans(outs, 4, ins, 9)) != SW_OK) return st;
+  a.vec = L % 4 == 0 && all_aligned16({a.x, a.delta, a.y, a.z, a.s_out});
   return a.blelloch ? selective_blelloch_fwd(a) : selective_fwd(a);
 }
 
@@ -245,6 +246,7 @@ int selective_bwd_common(BwdArgs a) {
       !mul_ok(D, N, &nan) || !mul_ok(R, 16 * ((L + 7) / 8 + 1), &tmp) || !mul_ok(tmp, 8, &tmp))
     return fail(SW_ERR_UNSUPPORTED, "sizes overflow");
   if (a.dz && !a.z) return fail(SW_ERR_INVALID_ARG, "dz requires z");
+  if (a.s_pre && !a.z) return fail(SW_ERR_INVALID_ARG, "s_pre requires z");
   if (a.ckpt && N > 16)
     return fail(SW_ERR_UNSUPPORTED, "checkpoints hold 16 states (got N=%lld)", (long long)N);
   int dev, st;
@@ -264,6 +266,7 @@ int selective_bwd_common(BwdArgs a) {
   if ((st = check_ptr(a.dy, dys, "dy", !empty, dev)) != SW_OK) return st;
   if ((st = check_ptr(a.dh_last, 4, "dh_last", false, dev)) != SW_OK) return st;
   if ((st = check_ptr(a.ckpt, 4, "ckpt", false, dev)) != SW_OK) return st;
+  if ((st = check_ptr(a.s_pre, 4, "s_pre", false, dev)) != SW_OK) return st;
   // outputs
   if ((st = check_ptr(a.dx, 4, "dx", nx > 0, dev)) != SW_OK) return st;
   if ((st = check_ptr(a.ddelta, 4, "ddelta", nx > 0, dev)) != SW_OK) return st;
@@ -285,8 +288,9 @@ int selective_bwd_common(BwdArgs a) {
                 {a.z, (size_t)nx * es, "z"},            {a.delta_bias, (size_t)D * 4, "delta_bias"},
                 {a.h0, (size_t)nh * 4, "h0"},           {a.dy, (size_t)nx * dys, "dy"},
                 {a.dh_last, (size_t)nh * 4, "dh_last"},
-                {a.ckpt, (size_t)R * (size_t)((L + 7) / 8) * 64, "ckpt"}};
-  if ((st = check_spans(outs, 9, ins, 12)) != SW_OK) return st;
+                {a.ckpt, (size_t)R * (size_t)((L + 7) / 8) * 64, "ckpt"},
+                {a.s_pre, (size_t)nx * 4, "s_pre"}};
+  if ((st = check_spans(outs, 9, ins, 13)) != SW_OK) return st;
   hipStream_t s = current_stream();
   if (empty) {
     // no step: every sum is empty, and the initial state's gradient is dh_last
@@ -526,7 +530,7 @@ SW_API int sw_selective_scan_bwd(const void* x, const void* delta, const float* 
                                  const void* Bm, const void* Cm, const float* Dskip,
                                  const void* z, const float* delta_bias, const float* h0,
                                  const void* dy, const float* dh_last, const float* ckpt,
-                                 float* dx, float* ddelta,
+                                 const float* s_pre, float* dx, float* ddelta,
                                  float* dA, float* dB, float* dC, float* dDskip, float* dz,
                                  float* ddelta_bias, float* dh0, int64_t B, int64_t D, int64_t N,
                                  int64_t L, int in_dtype, int dy_dtype, int flags) {
@@ -548,6 +552,7 @@ SW_API int sw_selective_scan_bwd(const void* x, const void* delta, const float* 
   a.h0 = h0;
   a.dh_last = dh_last;
   a.ckpt = ckpt;
+  a.s_pre = s_pre;
   a.dx = dx;
   a.ddelta = ddelta;
   a.dA = dA;
@@ -605,9 +610,9 @@ SW_API int sw_selective_scan_fwd_ex(const void* x, const void* delta, const floa
 SW_API int sw_selective_scan_fwd_train(const void* x, const void* delta, const float* A,
                                        const void* Bm, const void* Cm, const float* Dskip,
                                        const void* z, const float* delta_bias, const float* h0,
-                                       void* y, float* h_last, float* ckpt, int64_t B, int64_t D,
-                                       int64_t N, int64_t L, int in_dtype, int out_dtype,
-                                       int flags) {
+                                       void* y, float* h_last, float* ckpt, float* s_pre,
+                                       int64_t B, int64_t D, int64_t N, int64_t L, int in_dtype,
+                                       int out_dtype, int flags) {
   if (!ckpt) return sw::fail(SW_ERR_INVALID_ARG, "ckpt is NULL");
   if ((in_dtype != SW_DTYPE_F32 && in_dtype != SW_DTYPE_BF16) ||
       (out_dtype != SW_DTYPE_F32 && out_dtype != SW_DTYPE_BF16))
@@ -622,6 +627,7 @@ SW_API int sw_selective_scan_fwd_train(const void* x, const void* delta, const f
   a.y_bf16 = out_dtype == SW_DTYPE_BF16;
   a.softplus = (flags & SW_DELTA_SOFTPLUS) != 0;
   a.ckpt = ckpt;
+  a.s_out = s_pre;
   return sw::selective_common(a);
 }
 

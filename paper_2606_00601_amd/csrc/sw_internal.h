@@ -65,6 +65,7 @@ struct SelArgs {
   bool bf16_in, y_bf16, softplus, vec;
   bool blelloch = false;  // the paper's schedule (plain form only)
   float* ckpt = nullptr;  // (B*D, ceil(L/8), 16): states at 8-step boundaries (N <= 16)
+  float* s_out = nullptr;  // (B, D, L) fp32: y before the output gate (with the options)
 };
 int selective_fwd(const SelArgs& a);
 int selective_blelloch_fwd(const SelArgs& a);
@@ -78,6 +79,7 @@ struct BwdArgs {
   const void *x, *delta, *Bm, *Cm, *z, *dy;
   const float *A, *Dskip, *delta_bias, *h0, *dh_last;
   const float* ckpt;  // the forward's states at 8-step boundaries, or NULL (recomputed)
+  const float* s_pre;  // the forward's output before the gate, or NULL (recomputed)
   float *dx, *ddelta, *dA, *dB, *dC, *dDskip, *dz, *ddelta_bias, *dh0;
   int64_t B, D, N, L;
   bool bf16_in, dy_bf16, softplus, vec;  // vec: x and delta allow the forward's vector path

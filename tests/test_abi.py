@@ -114,3 +114,11 @@ def test_binding_rejects_cpu_tensors():
     a = torch.zeros((1, 2, 3))
     with pytest.raises(ValueError):
         pkg.affine_scan(a, a)
+
+
+def test_bwd_s_pre_requires_z(lib):
+    # a pre-gate output without a gate is an invalid argument, before any HIP call
+    args = [None] * 22 + [1, 1, 16, 8, 0, 0, 0]
+    args[12] = 0x1000  # s_pre
+    assert lib.sw_selective_scan_bwd(*args) == 1
+    assert "s_pre requires z" in lib.sw_last_error().decode()

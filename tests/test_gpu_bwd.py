@@ -210,10 +210,11 @@ def test_bwd_full_size_sampled(sw):
                                           ((1, 9, 5, 96), "8")])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_forward_checkpoints_and_backward_with_them(sw, monkeypatch, shape, layout, dtype):
-    """The forward's training mode stores the state before every 8th step;
-    each slot matches the oracle's final state of the sequence cut there, and
-    the backward fed with them gives the oracle's gradients, bit-identical to
-    the backward that rebuilds them itself."""
+    """The forward's training mode stores the state before every 8th step and
+    the output before the gate; each slot matches the oracle's final state of
+    the sequence cut there, the pre-gate output is the ungated forward's y bit
+    for bit, and the backward fed with them gives the oracle's gradients,
+    bit-identical to the backward that rebuilds them itself."""
     monkeypatch.setenv("SW_SS_LAYOUT", layout)
     B, D, N, L = shape
     opts = ("z", "bias", "softplus", "h0", "dhl")
@@ -228,9 +229,14 @@ def test_forward_checkpoints_and_backward_with_them(sw, monkeypatch, shape, layo
         z = _dev(ex["z"])
     kw = dict(z=z, delta_bias=_dev(ex["delta_bias"]), h0=_dev(ex["h0"]), delta_softplus=True)
     ck = sw.new_ckpt(x, N)
+    sp = torch.empty((B, D, L), dtype=torch.float32, device="cuda")
     y, hl = sw.selective_scan_fwd(x, dl, _dev(inp["A"]), Bm, Cm, _dev(inp["Dskip"]), ckpt=ck,
-                                  **kw)
+                                  s_pre=sp, **kw)
+    ungated = {k: v for k, v in kw.items() if k != "z"}
+    y_ungated, _ = sw.selective_scan_fwd(x, dl, _dev(inp["A"]), Bm, Cm, _dev(inp["Dskip"]),
+                                         **ungated)
     torch.cuda.synchronize()
+    assert torch.equal(sp, y_ungated)
     ckn = ck.cpu().numpy()
     nt8 = (L + 7) // 8
     for k in sorted({0, 1, nt8 // 2, nt8 - 1}):
@@ -250,12 +256,16 @@ def test_forward_checkpoints_and_backward_with_them(sw, monkeypatch, shape, layo
     args = (x, dl, _dev(inp["A"]), Bm, Cm, _dev(inp["Dskip"]), dy, dhl)
     g1 = sw.selective_scan_bwd(*args, ckpt=ck, **kw)
     g0 = sw.selective_scan_bwd(*args, **kw)
+    g2 = sw.selective_scan_bwd(*args, ckpt=ck, s_pre=sp, **kw)
+    g3 = sw.selective_scan_bwd(*args, s_pre=sp, **kw)
     torch.cuda.synchronize()
     o = _ref(inp, ex, opts)
     _check_all(g1, o, f"bwd with ckpt {dtype} {shape}",
                ["dx", "ddelta", "dA", "dB", "dC", "dDskip", "dz", "ddelta_bias", "dh0"])
     for k in g0:
         assert torch.equal(g0[k], g1[k]), k
+        assert torch.equal(g0[k], g2[k]), k
+        assert torch.equal(g0[k], g3[k]), k
 
 
 def test_forward_checkpoints_reject_large_N(sw):
