@@ -69,7 +69,8 @@ typedef enum sw_status {
   SW_ERR_ALLOC = 4        /* scratch allocation failed */
 } sw_status;
 
-/* Version of this ABI, major*10000 + minor*100 + patch. */
+/* Version of this ABI, major*10000 + minor*100 + patch (200: the training
+ * forward and the backward exchange the pre-gate output, s_pre). */
 int sw_version(void);
 
 /*

@@ -459,7 +459,7 @@ int zero_words(uint32_t* p, size_t words, hipStream_t s) {
 
 // ------------------------------------------------------------------ C ABI
 
-SW_API int sw_version(void) { return 100; }
+SW_API int sw_version(void) { return 200; }
 
 SW_API int sw_affine_scan(const float* a, const float* bx, const float* h0, float* h_out,
                           int64_t B, int64_t D, int64_t L) {

@@ -122,3 +122,8 @@ def test_bwd_s_pre_requires_z(lib):
     args[12] = 0x1000  # s_pre
     assert lib.sw_selective_scan_bwd(*args) == 1
     assert "s_pre requires z" in lib.sw_last_error().decode()
+
+
+def test_abi_version(lib):
+    # 0.2.0: sw_selective_scan_fwd_train and sw_selective_scan_bwd take s_pre
+    assert lib.sw_version() == 200
