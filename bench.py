@@ -249,13 +249,78 @@ def time_launches(step, steps, warmup):
     return wall, gpu_per, spread
 
 
-def launch_stats(gpu_per, spread):
+GRAPH_SPREAD_REPLAYS = 20
+
+
+def time_graph(step, steps, warmup):
+    """time_launches with the launches replayed from a HIP graph.
+
+    After `warmup` eager steps, `steps` launches are captured into one graph
+    (torch's capture; the library enqueues on the capturing stream), which is
+    replayed once untimed, then once between one pair of HIP events (exactly
+    `steps` timed launches, without the host's per-call enqueue cost), then
+    GRAPH_SPREAD_REPLAYS more times with an event pair around each replay for
+    the spread (per-launch means of the replays).  Only calls that launch
+    kernels and use no scratch or workspace can be captured; the library
+    refuses the others while capturing.
+    """
+    import torch
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(3):
+            step(i)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            step(i)
+    g.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_per = e0.elapsed_time(e1) * 1e-3 / max(steps, 1)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(GRAPH_SPREAD_REPLAYS)]
+    for a, b in ev:
+        a.record(stream)
+        g.replay()
+        b.record(stream)
+    torch.cuda.synchronize()
+    spread = np.array([a.elapsed_time(b) * 1e-3 / max(steps, 1) for a, b in ev])
+    return wall, gpu_per, spread
+
+
+def run_timed(step, args):
+    if getattr(args, "graph", False):
+        return time_graph(step, args.steps, args.warmup)
+    return time_launches(step, args.steps, args.warmup)
+
+
+def launch_stats(gpu_per, spread, graph=False):
     """The per_launch_us object of a bench line."""
-    return {"mean": gpu_per * 1e6, "std": float(spread.std()) * 1e6,
-            "median": float(np.median(spread)) * 1e6,
-            "mean_of_spread_pass": float(spread.mean()) * 1e6, "spread_launches": len(spread),
-            "method": "mean: HIP events around the timed steps / steps; std, median: an "
-                      "untimed pass after them with an event pair around each launch"}
+    out = {"mean": gpu_per * 1e6, "std": float(spread.std()) * 1e6,
+           "median": float(np.median(spread)) * 1e6,
+           "mean_of_spread_pass": float(spread.mean()) * 1e6, "spread_launches": len(spread),
+           "method": "mean: HIP events around the timed steps / steps; std, median: an "
+                     "untimed pass after them with an event pair around each launch"}
+    if graph:
+        del out["spread_launches"]  # the spread is over replays, not single launches
+        out["spread_replays"] = len(spread)
+        out["method"] = ("launches replayed from one HIP graph of `steps` launches; mean: HIP "
+                         "events around one replay / steps; std, median: over the per-launch "
+                         "means of further replays, an event pair around each")
+    return out
 
 
 def bench_affine(w, args):
@@ -299,7 +364,7 @@ def bench_affine(w, args):
         else:
             sw.affine_scan_schedule(a, bx, out=h, schedule=args.schedule)
 
-    wall, kern, per = time_launches(step, args.steps, args.warmup)
+    wall, kern, per = run_timed(step, args)
     gbs = abytes / kern / 1e9
     # the library walks each row in one workgroup once the rows alone fill the
     # GPU (>= 8 per CU) and a row is longer than one 2048-step chunk
@@ -319,13 +384,14 @@ def bench_affine(w, args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int32" if args.int32 else "f32", "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "D": w.D, "L": w.L, "input_sets_rotated": nsets,
-                   "schedule": args.schedule, "form": args.form},
+                   "schedule": args.schedule, "form": args.form,
+                   "launch": "hip-graph" if args.graph else "eager"},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS,
                      "traffic": (measured_traffic(w) if args.schedule == "default" and not proj
                                  and not args.int32 else None),
                      "kernel": kname,
-                     "per_launch_us": launch_stats(kern, per)},
+                     "per_launch_us": launch_stats(kern, per, args.graph)},
     }
     if cpu is not None:
         out["cpu_baseline"] = cpu
@@ -394,7 +460,7 @@ def bench_bwd(w, args):
         sw.selective_scan_bwd(t["x"], t["delta"], t["A"], t["Bm"], t["Cm"], t["Dskip"], dy_t,
                               ckpt=ck, s_pre=sp, **opt)
 
-    wall, kern, per = time_launches(step, args.steps, args.warmup)
+    wall, kern, per = run_timed(step, args)
     elems = w.elems
     # algorithmic bytes: x, delta, dy read; dx, ddelta written (fp32); B, C
     # read, dB, dC written (fp32); A, Dskip read, dA, dDskip, dh0 written
@@ -418,7 +484,7 @@ def bench_bwd(w, args):
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                      "unit": "T fp32-lane-slot/s", "frac": achieved / VALU_PEAK,
                      "traffic": None, "kernel": "selective_bwd_kernel + selective_bwd_reduce_kernel",
-                     "per_launch_us": launch_stats(kern, per),
+                     "per_launch_us": launch_stats(kern, per, args.graph),
                      "slots_per_elem": SLOTS_PER_ELEM_BWD},
         "hbm": {"algorithmic_bytes": abytes, "achieved_GBs": abytes / kern / 1e9,
                 "peak_GBs": HBM_PEAK_GBS, "frac": abytes / kern / 1e9 / HBM_PEAK_GBS},
@@ -460,6 +526,10 @@ def main(argv=None):
     ap.add_argument("--print-kernel-sha", action="store_true",
                     help="print the hash of the kernel sources of --workload's path "
                          "(the key of its traffic record) and exit")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the timed launches from one HIP graph (forward and bare "
+                         "scan; removes the host's per-call enqueue cost, which bounds the "
+                         "launch-sized workloads)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, 5 times "
                          "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -494,6 +564,10 @@ def main(argv=None):
 
     import paper_2606_00601_amd as sw
     w = wl.workload(args.workload)
+    if args.graph and args.which == "bwd":
+        print("--graph: the backward allocates a workspace per call and cannot be captured",
+              file=sys.stderr)
+        return 2
     if w.path == "affine":
         return bench_affine(w, args)
     if args.which == "bwd":
@@ -558,7 +632,7 @@ def main(argv=None):
             sw.selective_scan_fwd_schedule(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"],
                                            s["Dskip"], schedule=args.schedule)
 
-    wall, kern, per = time_launches(step, args.steps, args.warmup)
+    wall, kern, per = run_timed(step, args)
 
     elems = w.elems
     value = elems * args.steps / wall
@@ -590,6 +664,7 @@ def main(argv=None):
             "options": ("gate z, delta bias + softplus, initial state" if args.options
                         else "none"),
             "forward_checkpoints": bool(args.ckpt),
+            "launch": "hip-graph" if args.graph else "eager",
         },
         "roofline": {
             "bound": "alu",
@@ -600,7 +675,7 @@ def main(argv=None):
             "traffic": (measured_traffic(w) if args.schedule == "default" and not args.options
                         and not args.ckpt and fwd_kernel == "selective_row16_kernel" else None),
             "kernel": fwd_kernel,
-            "per_launch_us": launch_stats(kern, per),
+            "per_launch_us": launch_stats(kern, per, args.graph),
             "slots_per_elem": SLOTS_PER_ELEM,
         },
         "hbm": {"algorithmic_bytes": abytes, "achieved_GBs": hbm_gbs, "peak_GBs": HBM_PEAK_GBS,

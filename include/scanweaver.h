@@ -45,12 +45,16 @@
  *    an allocation fails.
  *  - Threads using distinct streams may call concurrently.
  *  - HIP graph capture: a call that uses neither the scratch nor a workspace
- *    (the fused forward at N = 16 with L a multiple of 8 for bf16 or of 4
- *    for fp32, 16-byte aligned arrays, and a workgroup's byte offsets below
- *    2^31) can be captured and replayed: it launches kernels only.  A call that
- *    uses the scratch is not replay-safe (a replay would repeat the ticket
- *    and epoch values the host gave the captured launch), and the backward
- *    allocates its workspace per call: do not capture those.
+ *    can be captured and replayed: it launches kernels only.  Such calls are
+ *    the fused forward at N = 16 with L a multiple of 8 for bf16 or of 4 for
+ *    fp32, 16-byte aligned arrays and a workgroup's byte offsets below 2^31;
+ *    the bare scan and its projection form when a row fits one chunk
+ *    (L <= 2048) or the rows alone fill the GPU (B*D >= 8 per compute unit);
+ *    and the Blelloch schedule entry points.  A call that uses the scratch
+ *    is not replay-safe (a replay would repeat the ticket range and epoch the
+ *    host gave the captured launch), and the backward allocates a workspace
+ *    per call: while the stream is capturing, those calls return
+ *    SW_ERR_UNSUPPORTED before enqueuing anything.
  */
 #ifndef SCANWEAVER_H
 #define SCANWEAVER_H

@@ -375,6 +375,25 @@ void keep_pool_memory(int dev) {
   pool_ready[dev] = true;
 }
 
+// A call that needs the per-stream scratch or a workspace cannot be captured
+// into a HIP graph: a replay would repeat the ticket range and epoch the host
+// handed out (the tickets are spent, so the replayed kernel writes nothing),
+// and a workspace allocated per call would become a graph allocation.  Refuse
+// it while `s` is capturing instead of recording a graph that replays wrongly.
+int refuse_capture(hipStream_t s, const char* what) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(s, &cs);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(SW_ERR_HIP, "hipStreamIsCapturing: %s", hipGetErrorString(e));
+  }
+  if (cs != hipStreamCaptureStatusNone)
+    return fail(SW_ERR_UNSUPPORTED,
+                "this call uses %s and cannot be captured into a HIP graph (stream capture "
+                "is active)", what);
+  return SW_OK;
+}
+
 }  // namespace
 
 ScratchSession::ScratchSession() {}
@@ -390,6 +409,8 @@ ScratchSession::~ScratchSession() {
 }
 
 int ScratchSession::reserve(size_t carry_words, uint32_t tickets, hipStream_t s) {
+  int st = refuse_capture(s, "the per-stream scratch (tickets and carries)");
+  if (st != SW_OK) return st;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(SW_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
@@ -412,7 +433,7 @@ int ScratchSession::reserve(size_t carry_words, uint32_t tickets, hipStream_t s)
       ws.base = nullptr;
       return fail(SW_ERR_ALLOC, "hipMallocAsync(%zu bytes): %s", bytes, hipGetErrorString(e));
     }
-    int st = zero_words(reinterpret_cast<uint32_t*>(ws.base), bytes / 4, s);
+    st = zero_words(reinterpret_cast<uint32_t*>(ws.base), bytes / 4, s);
     if (st != SW_OK) return st;
     ws.bytes = bytes;
   }
@@ -426,6 +447,9 @@ int ScratchSession::reserve(size_t carry_words, uint32_t tickets, hipStream_t s)
 }
 
 int workspace_alloc(void** p, size_t bytes, hipStream_t s) {
+  *p = nullptr;
+  int st = refuse_capture(s, "a workspace allocated per call");
+  if (st != SW_OK) return st;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(SW_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));

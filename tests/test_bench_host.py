@@ -63,3 +63,17 @@ def test_more_than_one_gpu_is_refused():
                          capture_output=True, text=True, timeout=120)
     assert res.returncode == 2
     assert "one GPU" in res.stderr
+
+
+def test_launch_stats_of_graph_replays():
+    st = bench.launch_stats(5e-6, np.array([5.1e-6, 4.9e-6]), graph=True)
+    assert st["spread_replays"] == 2 and "spread_launches" not in st
+    assert "graph" in st["method"]
+
+
+def test_graph_backward_is_refused():
+    # the backward allocates a workspace per call: no graph capture
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--graph", "--pass",
+                          "bwd", "--no-cpu"], capture_output=True, text=True, timeout=300)
+    assert res.returncode == 2
+    assert "cannot be captured" in res.stderr

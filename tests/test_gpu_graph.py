@@ -3,9 +3,10 @@ and replayed: every replay, with eager calls and synchronizations between the
 replays, gives the eager result bit for bit.
 
 The N = 16 forward takes no scratch memory and allocates nothing, so it can be
-captured; the entry points that use the per-stream scratch (the bare scan's
-look-back, the chained chunks of the N != 16 kernel) or allocate (the
-backward) are not graph-replay safe and are not captured here.
+captured; the calls that use the per-stream scratch (the bare scan's
+look-back, the persistent kernel of N != 16) or allocate (the backward) are
+not graph-replay safe, and the library refuses them while the stream is
+capturing (checked here).
 """
 import sys
 
@@ -78,3 +79,73 @@ def test_forward_graph_replays_match_eager(sw, options):
         y2, h2 = sw.selective_scan_fwd(x, dl, A, Bm, Cm, Dk, **kw)
         torch.cuda.synchronize()
         assert torch.equal(y2, y_ref) and torch.equal(h2, h_ref)
+
+
+def test_capture_refuses_calls_that_need_scratch_or_workspace(sw):
+    """While the stream is capturing, the calls that use the per-stream scratch
+    (the bare scan's look-back over chunks of a few long rows, the persistent
+    kernel of N != 16) or allocate a workspace (the backward) raise instead of
+    recording a graph whose replay would write nothing; a legal call captured
+    beside them replays correctly, and the refused calls still work eagerly."""
+    _say("case capture refusals")
+    rng = np.random.Generator(np.random.PCG64(779))
+    dev = "cuda"
+    # bare scan (int32 ring: exact, so any carry order gives the same bits),
+    # 4 rows of 8192 steps: 4 chunks per row, chained by look-back
+    ai = torch.from_numpy(rng.integers(-2**31, 2**31, (1, 4, 8192), dtype=np.int64)
+                          .astype(np.int32)).to(dev)
+    bi = torch.from_numpy(rng.integers(-2**31, 2**31, (1, 4, 8192), dtype=np.int64)
+                          .astype(np.int32)).to(dev)
+    # fused forward with N = 8 (persistent kernel with a ticket counter)
+    B, D, L = 1, 16, 64
+    f32 = lambda *s: torch.from_numpy(rng.standard_normal(s).astype(np.float32)).to(dev)
+    x, dl = f32(B, D, L), torch.from_numpy(
+        rng.uniform(0.01, 0.1, (B, D, L)).astype(np.float32)).to(dev)
+    A8 = -torch.from_numpy(rng.uniform(0.5, 2.0, (D, 8)).astype(np.float32)).to(dev)
+    B8, C8 = f32(B, L, 8), f32(B, L, 8)
+    # legal: N = 16 forward; the backward of the same (refused: workspace)
+    A16 = -torch.from_numpy(rng.uniform(0.5, 2.0, (D, 16)).astype(np.float32)).to(dev)
+    B16, C16, Dk, dy = f32(B, L, 16), f32(B, L, 16), f32(D), f32(B, D, L)
+
+    refused = {
+        "bare scan with look-back": lambda: sw.affine_scan_i32(ai, bi),
+        "forward N=8": lambda: sw.selective_scan_fwd(x, dl, A8, B8, C8, Dk),
+        "backward": lambda: sw.selective_scan_bwd(x, dl, A16, B16, C16, Dk, dy),
+    }
+    y_ref, h_ref = sw.selective_scan_fwd(x, dl, A16, B16, C16, Dk)
+    eager = {k: f() for k, f in refused.items()}
+    torch.cuda.synchronize()
+    y = torch.empty_like(y_ref)
+    hl = torch.empty_like(h_ref)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        sw.selective_scan_fwd(x, dl, A16, B16, C16, Dk, y=y, h_last=hl)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sw.selective_scan_fwd(x, dl, A16, B16, C16, Dk, y=y, h_last=hl)
+        for name, fn in refused.items():
+            with pytest.raises(sw.ScanWeaverError, match="captured") as ei:
+                fn()
+            assert ei.value.status == 2, name  # SW_ERR_UNSUPPORTED
+    for i in range(3):
+        y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_ref) and torch.equal(hl, h_ref), f"replay {i}"
+    # the refused calls, eagerly again, give what they gave before the capture
+    def parts(v):
+        if isinstance(v, dict):
+            return [v[k] for k in sorted(v)]
+        return [t for t in (v if isinstance(v, (tuple, list)) else (v,)) if t is not None]
+
+    for name, fn in refused.items():
+        got = parts(fn())
+        torch.cuda.synchronize()
+        ref = parts(eager[name])
+        assert len(got) == len(ref) and len(got) > 0, name
+        for gi, ri in zip(got, ref):
+            assert torch.equal(gi, ri), name
