@@ -183,6 +183,13 @@ int sw_affine_scan_proj_i32(const int32_t* a, const int32_t* b, const int32_t* x
  *   y        : (B, D, L) fp32 output   h_last : (B, D, N) fp32 output or NULL
  * 1 <= N <= 64, else SW_ERR_UNSUPPORTED.  State and accumulation are fp32.
  * With L == 0 and B*D > 0, h_last (if given) is set to zero.
+ * Calls whose rows fill at most half of the GPU's SIMDs (N = 16, e.g. one
+ * sequence of a small model) split each row into segments composed with
+ * Eq. (7): their results agree with a whole-row walk within fp32 rounding,
+ * not bit for bit.  The environment variable SW_SS_SEGMENTS, read per call,
+ * forces the segment count (1: whole rows).  y's memory holds the segments'
+ * carries between the call's kernels, so y must not be read until the call
+ * completes on its stream (as for any output).
  */
 int sw_selective_scan_fwd(const float* x, const float* delta, const float* A, const float* Bm,
                           const float* Cm, const float* Dskip, float* y, float* h_last,
@@ -239,7 +246,9 @@ int sw_selective_scan_fwd_ex(const void* x, const void* delta, const float* A, c
 
 /*
  * sw_selective_scan_fwd_ex that also keeps what the backward pass needs
- * (training): ckpt (B, D, ceil(L/8), 16) fp32, required, receives the state
+ * (training; always walks whole rows, so y is bit-identical to that of
+ * sw_selective_scan_fwd_ex run with SW_SS_SEGMENTS=1): ckpt (B, D,
+ * ceil(L/8), 16) fp32, required, receives the state
  * h[b,d,8k-1,n] before step 8k (h0, or zero, for k = 0) in slot
  * [b, d, k, n]; slots n >= N hold no state.  N <= 16 (SW_ERR_UNSUPPORTED
  * above).  s_pre (B, D, L) fp32, or NULL, receives y before the output gate

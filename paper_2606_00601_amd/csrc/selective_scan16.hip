@@ -32,6 +32,19 @@
 // super-tile of delta/x, two tiles of B/C; lanes past the end read zeros or
 // are masked.  There is no carry between workgroups: each workgroup walks
 // its rows over the whole sequence.
+//
+// Narrow shapes (too few rows to give every SIMD a wavefront) split each row
+// into segments instead, composed with Eq. (7) in three launches that need no
+// memory beyond y: (1) each segment but the last walks from a zero state
+// (the first from h0) and records its end state U and the product P of its
+// a_t; (2) a fold turns these into each segment's initial state,
+// h_in(s+1) = P_s h_in(s) + U_s; (3) every segment walks from its initial
+// state and stores y.  The records of segment s live in y's first 32 words
+// of segment s+1 (P in 16, U in 16; the fold leaves h_in in the first 16),
+// which launch (3) reads before it overwrites them with y.
+#include <stdlib.h>
+
+#include <atomic>
 #include <type_traits>
 
 #include "selective_common.h"
@@ -91,17 +104,35 @@ struct R16Ops {
   float4 b, c;
 };
 
+// Segment modes of the kernel (see the top of the file).
+enum : int { R16_WHOLE = 0, R16_SEG_ENDS = 1, R16_SEG_FWD = 2 };
+
+// The record words of the segment starting at step t of a row, in y's memory
+// (fp32 or bf16 elements; t is a multiple of 64, so the words are aligned).
+__device__ __forceinline__ float* seg_words(void* yv, bool ybf, int64_t row, int64_t L,
+                                            int64_t t) {
+  return ybf ? reinterpret_cast<float*>(static_cast<uint16_t*>(yv) + row * L + t)
+             : static_cast<float*>(yv) + row * L + t;
+}
+
 // OPT: the optional Mamba-block inputs (flags, z, delta bias) are read;
 // without it the kernel is the plain form (an initial state is always taken).
 // CK: the state at every 8-step boundary goes to ck, laid out as
 // (B*D, nT8, 16), for the backward pass.
-template <typename IN, bool OPT, bool CK>
+// SEG: R16_WHOLE walks whole rows; R16_SEG_ENDS and R16_SEG_FWD are launches
+// (1) and (3) of the segmented form, whose workgroups are (row block,
+// segment) pairs, blockIdx.x = row block * segments of the launch + segment;
+// a row has nseg segments of Lseg steps, the last one taking the rest.
+template <typename IN, bool OPT, bool CK, int SEG>
 __global__ __launch_bounds__(256) void selective_row16_kernel(
     const IN* __restrict__ x, const IN* __restrict__ delta, const float* __restrict__ A,
     const IN* __restrict__ Bm, const IN* __restrict__ Cm, const float* __restrict__ Dskip,
     const IN* __restrict__ z, const float* __restrict__ dbias, const float* __restrict__ h0,
     void* __restrict__ yv, float* __restrict__ h_last, int64_t D, int64_t L, int64_t ndb,
-    uint32_t flags_in, float* __restrict__ ck, int64_t nT8, float* __restrict__ s_out) {
+    uint32_t flags_in, float* __restrict__ ck, int64_t nT8, float* __restrict__ s_out,
+    int64_t nseg, int64_t Lseg) {
+  static_assert(!(CK && SEG != R16_WHOLE), "checkpoints are written by whole-row walks only");
+  constexpr bool ENDS = SEG == R16_SEG_ENDS;  // no y: the segment's P and end state
   constexpr int ES = (int)sizeof(IN);
   const uint32_t flags = OPT ? flags_in : 0u;
   constexpr int V = 16 / ES;              // steps a lane holds of a super-tile
@@ -113,31 +144,45 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   const int tid = threadIdx.x;
   const int w = tid / 64, lane = tid % 64;
   const int r = lane / R16_N, n = lane % R16_N;
-  const int64_t b = blockIdx.x / ndb;
-  const int64_t d0 = (blockIdx.x - b * ndb) * R16_ROWS;
+  // segment of this workgroup (launch (1) covers segments 0 .. nseg-2)
+  const int64_t nsl = ENDS ? nseg - 1 : nseg;
+  const int64_t sg = SEG != R16_WHOLE ? (int64_t)blockIdx.x % nsl : 0;
+  const int64_t rblk = SEG != R16_WHOLE ? (int64_t)blockIdx.x / nsl : (int64_t)blockIdx.x;
+  const int64_t ts = SEG != R16_WHOLE ? sg * Lseg : 0;  // first step of the segment
+  const int64_t Ls = SEG != R16_WHOLE ? (sg == nseg - 1 ? L - ts : Lseg) : L;  // its steps
+  const int64_t b = rblk / ndb;
+  const int64_t d0 = (rblk - b * ndb) * R16_ROWS;
   const int64_t d = d0 + R16_RPW * w + r;
   const bool dok = d < D;
   const int64_t dcl = dok ? d : D - 1;  // rows past D compute a copy of row D-1, never stored
   const int64_t rows = imin(R16_ROWS, D - d0);
   const int64_t row0 = b * D + d0;
 
-  const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(x + row0 * L, (uint32_t)(rows * L * ES));
-  const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(delta + row0 * L, (uint32_t)(rows * L * ES));
-  const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(Bm + b * L * R16_N, (uint32_t)(L * R16_N * ES));
-  const __amdgpu_buffer_rsrc_t rc = buffer_rsrc(Cm + b * L * R16_N, (uint32_t)(L * R16_N * ES));
+  // resources start at the segment's first step (row strides stay L)
+  const uint32_t rows_bytes = (uint32_t)((rows * L - ts) * ES);
+  const uint32_t bc_bytes = (uint32_t)((L - ts) * R16_N * ES);
+  const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(x + row0 * L + ts, rows_bytes);
+  const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(delta + row0 * L + ts, rows_bytes);
+  const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(Bm + (b * L + ts) * R16_N, bc_bytes);
+  const __amdgpu_buffer_rsrc_t rc = buffer_rsrc(Cm + (b * L + ts) * R16_N, bc_bytes);
   // the gate's input; without a gate (OPT set) the same loads read x (cached),
   // so that every path of one instantiation issues the same loads
   const __amdgpu_buffer_rsrc_t rz =
-      buffer_rsrc(((flags & SEL_GATED) ? z : x) + row0 * L, (uint32_t)(rows * L * ES));
+      buffer_rsrc(((flags & SEL_GATED) ? z : x) + row0 * L + ts, rows_bytes);
   const int32_t lrow = (int32_t)((dcl - d0) * L * ES);  // byte offset of this lane's row
 
   const float Al = A[dcl * R16_N + n] * R16_LOG2E;
   const float dsk = Dskip ? Dskip[dcl] : 0.0f;
   const float dbv = (OPT && dbias) ? dbias[dcl] : 0.0f;
   const bool ybf = (flags & SEL_Y_BF16) != 0;
-  float h = h0 ? h0[(b * D + dcl) * R16_N + n] : 0.0f;
+  float h = (h0 && sg == 0) ? h0[(b * D + dcl) * R16_N + n] : 0.0f;
+  if constexpr (SEG == R16_SEG_FWD) {
+    // the initial state the fold left in this segment's first words of y
+    if (sg > 0) h = seg_words(yv, ybf, b * D + dcl, L, ts)[n];
+  }
+  float pa = 1.0f;  // ENDS: product of the segment's a_t
 
-  const int64_t nsup = (L + ST - 1) / ST;
+  const int64_t nsup = (Ls + ST - 1) / ST;
   const int64_t ntile = nsup * TPS;  // tiles past L are identity steps, never stored
 
   // ---- B/C staging: thread tid widens steps tt = tid/8 of a tile, states
@@ -175,7 +220,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
         dv += dbv;
         if (flags & SEL_SOFTPLUS) dv = softplus_f32(dv);
       }
-      if (t0 + k >= L) dv = xv = 0.0f;  // identity step: a = 1, u = 0
+      if (t0 + k >= Ls) dv = xv = 0.0f;  // identity step: a = 1, u = 0
       dl[k] = dv;
       dx[k] = dv * xv;
     }
@@ -187,16 +232,17 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   const int rq = n % 8, rh = n / 8;
   RawVec<IN, 4> yxr, yzr;  // raw x and z of those four steps, for the tile awaiting its reduce
   auto fetch_yx = [&](int64_t kt) {
+    if constexpr (ENDS) return;
     const int32_t off = lrow + (int32_t)((kt * R16_T + 4 * rq) * ES);
     yxr.load_buf(rx, off);
     if constexpr (OPT) yzr.load_buf(rz, off);
   };
   float* const p_w = &sm.p[w][r * R16_PRS + n * R16_TS];
   const float* const p_r = &sm.p[w][r * R16_PRS + 8 * rh * R16_TS + 4 * rq];
-  float* const y_row = static_cast<float*>(yv) + (b * D + dcl) * L;
+  float* const y_row = static_cast<float*>(yv) + (b * D + dcl) * L + ts;
   // OPT: y before the output gate, for the backward of a gated call (or NULL)
-  float* const s_row = (OPT && s_out) ? s_out + (b * D + dcl) * L : nullptr;
-  uint16_t* const y16_row = static_cast<uint16_t*>(yv) + (b * D + dcl) * L;
+  float* const s_row = (OPT && s_out) ? s_out + (b * D + dcl) * L + ts : nullptr;
+  uint16_t* const y16_row = static_cast<uint16_t*>(yv) + (b * D + dcl) * L + ts;
 
   auto read_partials = [&](float4 (&pr)[8]) {
 #pragma unroll
@@ -217,12 +263,12 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     for (int q = 0; q < 4; ++q) s4[q] = __builtin_fmaf(dsk, yx[q], s4[q] + row_ror8(s4[q]));
     const int64_t t = kt * R16_T + 4 * rq;
     if constexpr (OPT) {
-      if (s_row && dok && rh == 0 && t < L)
+      if (s_row && dok && rh == 0 && t < Ls)
         *reinterpret_cast<float4*>(s_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) s4[q] *= gt[q];
-    if (dok && rh == 0 && t < L) {
+    if (dok && rh == 0 && t < Ls) {
       if (ybf)
         *reinterpret_cast<uint2*>(y16_row + t) =
             make_uint2(bf16x2_rne(s4[0], s4[1]), bf16x2_rne(s4[2], s4[3]));
@@ -233,7 +279,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
 
   auto read_ops = [&](R16Ops& o, int buf, int bi) {
     o.b = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n * R16_TS + 4 * bi]);
-    o.c = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n * R16_TS + 4 * bi]);
+    if constexpr (!ENDS) o.c = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n * R16_TS + 4 * bi]);
   };
 
   // ---- prologue: delta/x of super-tile 0, B/C of tiles 0..2, y-x of tile 0
@@ -272,7 +318,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     // this wavefront's own partials: after the barrier, so that the barrier
     // only drains the staging writes
     float4 pr[8];
-    if (kt > 0) read_partials(pr);
+    if (!ENDS && kt > 0) read_partials(pr);
 #pragma unroll
     for (int bi = 0; bi < R16_NB; ++bi) {
       const int nb = bi + R16_LA;
@@ -312,10 +358,17 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
         }
         const float a = __builtin_amdgcn_exp2f(dlv * Al);
         h = __builtin_fmaf(a, h, dxv * bq[q]);
-        p4[q] = cq[q] * h;
+        if constexpr (ENDS) {
+          pa *= a;
+          p4[q] = 0.0f;
+        } else {
+          p4[q] = cq[q] * h;
+        }
       }
-      *reinterpret_cast<float4*>(p_w + 4 * bi) = make_float4(p4[0], p4[1], p4[2], p4[3]);
-      if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, yx_prev, gt_prev);
+      if constexpr (!ENDS) {
+        *reinterpret_cast<float4*>(p_w + 4 * bi) = make_float4(p4[0], p4[1], p4[2], p4[3]);
+        if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, yx_prev, gt_prev);
+      }
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -345,12 +398,39 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
       }
     }
   }
-  {
+  if constexpr (ENDS) {
+    // the records of this segment, in the first words of the next one
+    if (dok) {
+      float* wd = seg_words(yv, ybf, b * D + d, L, ts + Ls);
+      wd[n] = pa;
+      wd[R16_N + n] = h;
+    }
+  } else {
     float4 pr[8];
     read_partials(pr);
     finish_reduce(ntile - 1, pr, yx_prev, gt_prev);
+    if (h_last && dok && (SEG == R16_WHOLE || sg == nseg - 1)) h_last[(b * D + d) * R16_N + n] = h;
   }
-  if (h_last && dok) h_last[(b * D + d) * R16_N + n] = h;
+}
+
+// Launch (2) of the segmented form: one lane per (row, state) walks the
+// segments' records in order and leaves each segment's initial state in its
+// first words: h_in(1) = U_0 (segment 0 started from h0), then
+// h_in(s+1) = P_s h_in(s) + U_s.
+__global__ __launch_bounds__(256) void row16_fold_kernel(void* __restrict__ yv, bool ybf,
+                                                         int64_t R, int64_t L, int64_t nseg,
+                                                         int64_t Lseg) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= R * R16_N) return;
+  const int64_t row = i / R16_N;
+  const int n = (int)(i % R16_N);
+  float h = 0.0f;
+  for (int64_t sgi = 1; sgi < nseg; ++sgi) {
+    float* wd = seg_words(yv, ybf, row, L, sgi * Lseg);
+    const float P = wd[n], U = wd[R16_N + n];
+    h = sgi == 1 ? U : __builtin_fmaf(P, h, U);
+    wd[n] = h;
+  }
 }
 
 }  // namespace
@@ -367,6 +447,75 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
          (L + pad) * R16_N * (int64_t)es < ((int64_t)1 << 31) && D > 0;
 }
 
+// Segments per row for the segmented form: enough to give up to one
+// wavefront per SIMD when the rows alone occupy at most half of them (a lone
+// wavefront's walk sets the time there, and the first launch costs about 0.6
+// of a walk over the segments before the last),
+// each segment at least one super-tile and at most 16 of them (the fold walks
+// them in order).  SW_SS_SEGMENTS forces a count (1: whole rows).  Returns
+// the count and sets *Lseg (a multiple of the super-tile; the last segment
+// takes the rest of the row, at least Lseg steps).
+int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, int64_t* Lseg) {
+  *Lseg = L;
+  int64_t want = 1;
+  const char* env = getenv("SW_SS_SEGMENTS");
+  if (env && *env) {
+    want = atoll(env);
+  } else {
+    // compute units per device, looked up once per device
+    static std::atomic<int> cu_cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 1;
+    }
+    int cus = (dev >= 0 && dev < 64) ? cu_cache[dev].load(std::memory_order_relaxed) : 0;
+    if (cus <= 0) {
+      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+          cus <= 0) {
+        (void)hipGetLastError();
+        return 1;
+      }
+      if (dev >= 0 && dev < 64) cu_cache[dev].store(cus, std::memory_order_relaxed);
+    }
+    const int64_t waves = nwg * R16_WAVES, simds = 4 * (int64_t)cus;
+    if (waves * 2 <= simds) want = simds / waves;
+  }
+  if (want > 16) want = 16;
+  if (want > L / st) want = L / st;
+  if (want < 2) return 1;
+  const int64_t per = (L + want - 1) / want;
+  *Lseg = (per + st - 1) / st * st;
+  const int64_t nseg = L / *Lseg;
+  if (nseg < 2) {
+    *Lseg = L;
+    return 1;
+  }
+  return nseg;
+}
+
+template <typename IN, bool OPT>
+void launch_row16_segments(const SelArgs& a, int64_t ndb, uint32_t flags, int64_t nseg,
+                           int64_t Lseg, hipStream_t s) {
+  const int64_t R = a.B * a.D;
+  const int64_t rblocks = a.B * ndb;
+  hipLaunchKernelGGL((selective_row16_kernel<IN, OPT, false, R16_SEG_ENDS>),
+                     dim3((unsigned)(rblocks * (nseg - 1))), dim3(256), 0, s,
+                     static_cast<const IN*>(a.x), static_cast<const IN*>(a.delta), a.A,
+                     static_cast<const IN*>(a.Bm), static_cast<const IN*>(a.Cm), a.Dskip,
+                     static_cast<const IN*>(a.z), a.delta_bias, a.h0, a.y, nullptr, a.D, a.L,
+                     ndb, flags, nullptr, (int64_t)0, nullptr, nseg, Lseg);
+  const int64_t lanes = R * R16_N;
+  hipLaunchKernelGGL(row16_fold_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s,
+                     a.y, a.y_bf16, R, a.L, nseg, Lseg);
+  hipLaunchKernelGGL((selective_row16_kernel<IN, OPT, false, R16_SEG_FWD>),
+                     dim3((unsigned)(rblocks * nseg)), dim3(256), 0, s,
+                     static_cast<const IN*>(a.x), static_cast<const IN*>(a.delta), a.A,
+                     static_cast<const IN*>(a.Bm), static_cast<const IN*>(a.Cm), a.Dskip,
+                     static_cast<const IN*>(a.z), a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L,
+                     ndb, flags, nullptr, (int64_t)0, a.s_out, nseg, Lseg);
+}
+
 template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s) {
   const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.s_out;
@@ -376,15 +525,27 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
     return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
   const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.y_bf16 ? SEL_Y_BF16 : 0u) |
                          (a.z ? SEL_GATED : 0u);
-  auto kern = opt ? (a.ckpt ? selective_row16_kernel<IN, true, true>
-                            : selective_row16_kernel<IN, true, false>)
-                  : (a.ckpt ? selective_row16_kernel<IN, false, true>
-                            : selective_row16_kernel<IN, false, false>);
+  // narrow shapes: the segmented form (not with checkpoints, which are
+  // written by whole-row walks)
+  int64_t Lseg = a.L;
+  const int64_t nseg =
+      a.ckpt ? 1 : row16_segments(grid, a.L, 16 * (16 / (int64_t)sizeof(IN)), &Lseg);
+  if (nseg > 1 && grid * nseg < ((int64_t)1 << 31)) {
+    if (opt)
+      launch_row16_segments<IN, true>(a, ndb, flags, nseg, Lseg, s);
+    else
+      launch_row16_segments<IN, false>(a, ndb, flags, nseg, Lseg, s);
+    return check_launch("selective_row16_kernel (segments)");
+  }
+  auto kern = opt ? (a.ckpt ? selective_row16_kernel<IN, true, true, R16_WHOLE>
+                            : selective_row16_kernel<IN, true, false, R16_WHOLE>)
+                  : (a.ckpt ? selective_row16_kernel<IN, false, true, R16_WHOLE>
+                            : selective_row16_kernel<IN, false, false, R16_WHOLE>);
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, static_cast<const IN*>(a.x),
                      static_cast<const IN*>(a.delta), a.A, static_cast<const IN*>(a.Bm),
                      static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
                      a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L, ndb, flags, a.ckpt,
-                     (a.L + 7) / 8, a.s_out);
+                     (a.L + 7) / 8, a.s_out, (int64_t)1, a.L);
   return check_launch("selective_row16_kernel");
 }
 

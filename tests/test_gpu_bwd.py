@@ -216,6 +216,9 @@ def test_forward_checkpoints_and_backward_with_them(sw, monkeypatch, shape, layo
     for bit, and the backward fed with them gives the oracle's gradients,
     bit-identical to the backward that rebuilds them itself."""
     monkeypatch.setenv("SW_SS_LAYOUT", layout)
+    # the training forward walks whole rows; so does the ungated forward it is
+    # compared with bit for bit (narrow calls would otherwise be segmented)
+    monkeypatch.setenv("SW_SS_SEGMENTS", "1")
     B, D, N, L = shape
     opts = ("z", "bias", "softplus", "h0", "dhl")
     _say("case ckpt", dtype, shape, layout)

@@ -413,6 +413,9 @@ def test_selective_continued_across_calls_bitexact(sw, monkeypatch, dtype, layou
     call's h_last, runs the same per-step arithmetic as one call: y and the
     final state are bit-identical."""
     monkeypatch.setenv("SW_SS_LAYOUT", layout)
+    # whole-row walks (this narrow shape would otherwise take the segmented
+    # form, whose rounding depends on where the segments fall)
+    monkeypatch.setenv("SW_SS_SEGMENTS", "1")
     _say("case selective continued", dtype, layout)
     B, D, N, L = 2, 24, 16, 4096
     inp = wl.selective_inputs(B, D, N, L, 7777, dtype)
@@ -431,6 +434,35 @@ def test_selective_continued_across_calls_bitexact(sw, monkeypatch, dtype, layou
     torch.cuda.synchronize()
     assert torch.equal(torch.cat(parts, dim=2), y_one)
     assert torch.equal(h, h_one)
+
+
+# Narrow calls split rows into segments (three launches composed with Eq. (7),
+# carries kept in y's memory).  (B, D, L) and the forced count ("auto": the
+# library's choice); D not a multiple of 16 leaves rows past D in the last
+# workgroup; counts that do not divide L give a longer last segment; L below
+# two super-tiles stays whole.
+_SEG_CASES = [((1, 37, 1000), "3"), ((2, 16, 512), "16"), ((1, 5, 4096), "auto"),
+              ((1, 48, 2048), "auto"), ((1, 20, 64), "16"), ((3, 7, 776), "5")]
+
+
+@pytest.mark.parametrize("case", _SEG_CASES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("opts", [(), ("h0", "bias", "softplus", "z", "ybf16")])
+def test_selective_segments(sw, monkeypatch, case, dtype, opts):
+    (B, D, L), segs = case
+    if segs != "auto":
+        monkeypatch.setenv("SW_SS_SEGMENTS", segs)
+    _say("case selective segments", dtype, (B, D, L), segs, opts)
+    inp, ex = _ex_inputs(B, D, 16, L, 9100 + B + D + L, dtype, opts)
+    softplus, y_bf16 = "softplus" in opts, "ybf16" in opts
+    y, hl = _run_ex(sw, inp, ex, dtype, softplus, y_bf16)
+    o = _ex_oracle(inp, ex, softplus)
+    _y_gate(y, o, y_bf16, f"segments y {dtype} {(B, D, L)} {segs} {opts}")
+    assert_gate(fp_gate(hl.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]),
+                f"segments h_last {dtype} {(B, D, L)} {segs} {opts}")
+    # the same call again gives the same bits (fixed segments, no atomics)
+    y2, hl2 = _run_ex(sw, inp, ex, dtype, softplus, y_bf16)
+    assert torch.equal(y, y2) and torch.equal(hl, hl2)
 
 
 def test_selective_L0_returns_h0(sw):
