@@ -30,7 +30,8 @@ from __future__ import annotations
 
 import torch
 
-from ._lib import ScanWeaverError, check, last_error, lib, status_string  # noqa: F401
+from ._lib import (SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32,  # noqa: F401
+                   ScanWeaverError, check, last_error, lib, status_string)
 
 __all__ = ["affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
            "affine_scan_proj", "affine_scan_proj_i32",
@@ -51,18 +52,49 @@ def _ptr(t):
 def _need(t, name, dtype, shape=None):
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
-    if t.device.type != "cuda":
+    if not t.is_cuda:
         raise ValueError(f"{name} must be on a GPU (got {t.device})")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
-    if shape is not None and tuple(t.shape) != tuple(shape):
+    if shape is not None and t.shape != tuple(shape):
         raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
 
 
-def _bind_stream(device):
-    lib().sw_set_stream(torch.cuda.current_stream(device).cuda_stream)
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
+def _stream_handle(idx):
+    """torch's current HIP stream on GPU idx, as a raw handle."""
+    if _raw_stream is not None:
+        return _raw_stream(idx)
+    return torch.cuda.current_stream(idx).cuda_stream
+
+
+class _on:
+    """``with _on(device):`` makes the tensor's GPU current (switching only when
+    another one is) and hands torch's current stream on it to the library, for
+    the library calls inside the block."""
+
+    __slots__ = ("idx", "prev")
+
+    def __init__(self, device):
+        self.idx = device.index if device.index is not None else torch.cuda.current_device()
+        self.prev = -1
+
+    def __enter__(self):
+        cur = torch.cuda.current_device()
+        if cur != self.idx:
+            torch.cuda.set_device(self.idx)
+            self.prev = cur
+        lib().sw_set_stream(_stream_handle(self.idx))
+        return self
+
+    def __exit__(self, *exc):
+        if self.prev >= 0:
+            torch.cuda.set_device(self.prev)
+        return False
 
 
 def _affine(fn, where, dtype, a, bx, h0, out):
@@ -77,8 +109,7 @@ def _affine(fn, where, dtype, a, bx, h0, out):
         out = torch.empty_like(a)
     else:
         _need(out, "out", dtype, a.shape)
-    with torch.cuda.device(a.device):
-        _bind_stream(a.device)
+    with _on(a.device):
         check(fn(_ptr(a), _ptr(bx), _ptr(h0), _ptr(out), B, D, L), where)
     return out
 
@@ -127,8 +158,7 @@ def _affine_proj(fn, where, dtype, a, b, x, c, h0, y, want_h_last):
     else:
         _need(y, "y", dtype, a.shape)
     h_last = torch.empty((B, D), dtype=dtype, device=a.device) if want_h_last else None
-    with torch.cuda.device(a.device):
-        _bind_stream(a.device)
+    with _on(a.device):
         check(fn(_ptr(a), _ptr(b), _ptr(x), _ptr(c), _ptr(h0), _ptr(y), _ptr(h_last), B, D, L),
               where)
     return y, h_last
@@ -199,7 +229,6 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
             _need(h_last, "h_last", torch.float32, (B, D, N))
     else:
         h_last = None
-    from ._lib import SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32
     in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
     out_dt = SW_DTYPE_F32 if y_dtype == torch.float32 else SW_DTYPE_BF16
     flags = SW_DELTA_SOFTPLUS if delta_softplus else 0
@@ -207,8 +236,7 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
         _need(ckpt, "ckpt", torch.float32, (B, D, (L + 7) // 8, 16))
     if s_pre is not None:
         _need(s_pre, "s_pre", torch.float32, (B, D, L))
-    with torch.cuda.device(x.device):
-        _bind_stream(x.device)
+    with _on(x.device):
         if ckpt is not None:
             check(lib().sw_selective_scan_fwd_train(
                 _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
@@ -252,10 +280,8 @@ def selective_scan_fwd_schedule(x, delta, A, Bm, Cm, Dskip=None, *, schedule="de
         _need(Dskip, "Dskip", torch.float32, (D,))
     y = torch.empty((B, D, L), dtype=torch.float32, device=x.device)
     h_last = torch.empty((B, D, N), dtype=torch.float32, device=x.device) if want_h_last else None
-    from ._lib import SW_DTYPE_BF16, SW_DTYPE_F32
     in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
-    with torch.cuda.device(x.device):
-        _bind_stream(x.device)
+    with _on(x.device):
         check(lib().sw_selective_scan_fwd_schedule(
             _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(y),
             _ptr(h_last), B, D, N, L, in_dt, _SCHEDULES[schedule]),
@@ -321,11 +347,9 @@ def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, 
     out["ddelta_bias"] = torch.empty((D,), **f32) if delta_bias is not None else None
     out["dz"] = torch.empty((B, D, L), **f32) if z is not None else None
     out["dh0"] = torch.empty((B, D, N), **f32) if want_dh0 else None
-    from ._lib import SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32
     in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
     dy_dt = SW_DTYPE_F32 if dy.dtype == torch.float32 else SW_DTYPE_BF16
-    with torch.cuda.device(dev):
-        _bind_stream(dev)
+    with _on(dev):
         check(lib().sw_selective_scan_bwd(
             _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
             _ptr(delta_bias), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(ckpt), _ptr(s_pre),
