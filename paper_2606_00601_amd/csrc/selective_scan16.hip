@@ -106,6 +106,7 @@ struct R16Ops {
 
 // Segment modes of the kernel (see the top of the file).
 enum : int { R16_WHOLE = 0, R16_SEG_ENDS = 1, R16_SEG_FWD = 2 };
+constexpr int R16_MAX_SEG = 16;  // segments per row at most
 
 // The record words of the segment starting at step t of a row, in y's memory
 // (fp32 or bf16 elements; t is a multiple of 64, so the words are aligned).
@@ -424,12 +425,23 @@ __global__ __launch_bounds__(256) void row16_fold_kernel(void* __restrict__ yv, 
   if (i >= R * R16_N) return;
   const int64_t row = i / R16_N;
   const int n = (int)(i % R16_N);
+  // all records first (independent loads in flight together), then the fold
+  float P[R16_MAX_SEG], U[R16_MAX_SEG];
+#pragma unroll
+  for (int sgi = 1; sgi < R16_MAX_SEG; ++sgi) {
+    if (sgi < nseg) {
+      const float* wd = seg_words(yv, ybf, row, L, sgi * Lseg);
+      P[sgi] = wd[n];
+      U[sgi] = wd[R16_N + n];
+    }
+  }
   float h = 0.0f;
-  for (int64_t sgi = 1; sgi < nseg; ++sgi) {
-    float* wd = seg_words(yv, ybf, row, L, sgi * Lseg);
-    const float P = wd[n], U = wd[R16_N + n];
-    h = sgi == 1 ? U : __builtin_fmaf(P, h, U);
-    wd[n] = h;
+#pragma unroll
+  for (int sgi = 1; sgi < R16_MAX_SEG; ++sgi) {
+    if (sgi < nseg) {
+      h = sgi == 1 ? U[sgi] : __builtin_fmaf(P[sgi], h, U[sgi]);
+      seg_words(yv, ybf, row, L, sgi * Lseg)[n] = h;
+    }
   }
 }
 
@@ -481,13 +493,13 @@ int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, int64_t* Lseg) {
     const int64_t waves = nwg * R16_WAVES, simds = 4 * (int64_t)cus;
     if (waves * 2 <= simds) want = simds / waves;
   }
-  if (want > 16) want = 16;
+  if (want > R16_MAX_SEG) want = R16_MAX_SEG;
   if (want > L / st) want = L / st;
   if (want < 2) return 1;
   const int64_t per = (L + want - 1) / want;
   *Lseg = (per + st - 1) / st * st;
-  const int64_t nseg = L / *Lseg;
-  if (nseg < 2) {
+  const int64_t nseg = L / *Lseg;  // <= want: Lseg >= L / want
+  if (nseg < 2 || nseg > R16_MAX_SEG) {
     *Lseg = L;
     return 1;
   }

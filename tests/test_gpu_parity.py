@@ -465,6 +465,25 @@ def test_selective_segments(sw, monkeypatch, case, dtype, opts):
     assert torch.equal(y, y2) and torch.equal(hl, hl2)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_selective_segments_no_dskip_no_hlast(sw, monkeypatch, dtype):
+    """The segmented form with Dskip and h_last left out (h_last NULL: the last
+    segment stores no state), against the oracle and the whole-row walk."""
+    B, D, N, L = 1, 24, 16, 2048
+    _say("case selective segments no dskip / h_last", dtype, (B, D, N, L))
+    inp = wl.selective_inputs(B, D, N, L, 9321, dtype)
+    monkeypatch.setenv("SW_SS_SEGMENTS", "6")
+    y, hl = _run_selective(sw, inp, dtype, with_dskip=False, want_h_last=False)
+    assert hl is None
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"], None,
+                              bounds=True)
+    assert_gate(fp_gate(y.cpu().numpy(), o["y"], o["y_mag"], o["y_sens"]),
+                f"segments no dskip {dtype}")
+    monkeypatch.setenv("SW_SS_SEGMENTS", "1")
+    y1, _ = _run_selective(sw, inp, dtype, with_dskip=False, want_h_last=False)
+    assert rownorm_rel(y.cpu().numpy(), y1.cpu().numpy()) <= 1e-5
+
+
 def test_selective_L0_returns_h0(sw):
     x = torch.empty((2, 3, 0), device="cuda")
     A = torch.randn((3, 16), device="cuda")
