@@ -37,7 +37,7 @@
 // into segments instead, composed with Eq. (7) in three launches that need no
 // memory beyond y: (1) each segment but the last walks from a zero state
 // (the first from h0) and records its end state U and the product P of its
-// a_t; (2) a fold turns these into each segment's initial state,
+// a_t, formed as exp(A * the segment's sum of delta); (2) a fold turns these into each segment's initial state,
 // h_in(s+1) = P_s h_in(s) + U_s; (3) every segment walks from its initial
 // state and stores y.  The records of segment s live in y's first 32 words
 // of segment s+1 (P in 16, U in 16; the fold leaves h_in in the first 16),
@@ -181,7 +181,9 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     // the initial state the fold left in this segment's first words of y
     if (sg > 0) h = seg_words(yv, ybf, b * D + dcl, L, ts)[n];
   }
-  float pa = 1.0f;  // ENDS: product of the segment's a_t
+  // ENDS: this lane's share of the sum of delta over the segment; the product
+  // of the segment's a_t is exp2(Al * that sum over the row's 16 lanes)
+  float dsum = 0.0f;
 
   const int64_t nsup = (Ls + ST - 1) / ST;
   const int64_t ntile = nsup * TPS;  // tiles past L are identity steps, never stored
@@ -224,6 +226,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
       if (t0 + k >= Ls) dv = xv = 0.0f;  // identity step: a = 1, u = 0
       dl[k] = dv;
       dx[k] = dv * xv;
+      if constexpr (ENDS) dsum += dv;
     }
   };
 
@@ -360,7 +363,6 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
         const float a = __builtin_amdgcn_exp2f(dlv * Al);
         h = __builtin_fmaf(a, h, dxv * bq[q]);
         if constexpr (ENDS) {
-          pa *= a;
           p4[q] = 0.0f;
         } else {
           p4[q] = cq[q] * h;
@@ -401,9 +403,11 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   }
   if constexpr (ENDS) {
     // the records of this segment, in the first words of the next one
+#pragma unroll
+    for (int m = 8; m >= 1; m /= 2) dsum += __shfl_xor(dsum, m, R16_N);
     if (dok) {
       float* wd = seg_words(yv, ybf, b * D + d, L, ts + Ls);
-      wd[n] = pa;
+      wd[n] = __builtin_amdgcn_exp2f(Al * dsum);
       wd[R16_N + n] = h;
     }
   } else {
@@ -459,14 +463,17 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
          (L + pad) * R16_N * (int64_t)es < ((int64_t)1 << 31) && D > 0;
 }
 
-// Segments per row for the segmented form: enough to give up to one
-// wavefront per SIMD when the rows alone occupy at most half of them (a lone
-// wavefront's walk sets the time there, and the first launch costs about 0.6
-// of a walk over the segments before the last),
-// each segment at least one super-tile and at most 16 of them (the fold walks
-// them in order).  SW_SS_SEGMENTS forces a count (1: whole rows).  Returns
-// the count and sets *Lseg (a multiple of the super-tile; the last segment
-// takes the rest of the row, at least Lseg steps).
+// Segments per row for the segmented form, from the wavefronts the rows give
+// per SIMD (r) and the row length (measured on MI355X, fp32, N = 16):
+//   r <= 1/2: one wavefront per SIMD (a lone wavefront's walk sets the time);
+//   1/2 < r < 1, L >= 2048: 8 segments (B=1, D=2560, L=16384: 480 -> 362 us);
+//   1 < r < 3/2, L >= 4096: 4 segments (B=1, D=5120, L=65536: 2711 -> 2603 us);
+//   otherwise whole rows (r = 1 and r >= 3/2 lose with any count).
+// Counts are powers of two, so that power-of-two rows split evenly; each
+// segment is at least one super-tile, at most R16_MAX_SEG per row (the fold
+// walks them in order).  SW_SS_SEGMENTS forces a count (1: whole rows).
+// Returns the count and sets *Lseg (a multiple of the super-tile; the last
+// segment takes the rest of the row, at least Lseg steps).
 int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, int64_t* Lseg) {
   *Lseg = L;
   int64_t want = 1;
@@ -491,7 +498,14 @@ int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, int64_t* Lseg) {
       if (dev >= 0 && dev < 64) cu_cache[dev].store(cus, std::memory_order_relaxed);
     }
     const int64_t waves = nwg * R16_WAVES, simds = 4 * (int64_t)cus;
-    if (waves * 2 <= simds) want = simds / waves;
+    if (waves * 2 <= simds) {
+      want = simds / waves;
+      while (want & (want - 1)) want &= want - 1;  // largest power of two below
+    } else if (waves < simds && L >= 2048) {
+      want = 8;
+    } else if (waves > simds && waves * 2 < simds * 3 && L >= 4096) {
+      want = 4;
+    }
   }
   if (want > R16_MAX_SEG) want = R16_MAX_SEG;
   if (want > L / st) want = L / st;
