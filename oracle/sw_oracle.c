@@ -288,6 +288,10 @@ int swo_affine_prefix_u32(const uint32_t* a, const uint32_t* bx, const uint32_t*
   return 0;
 }
 
+/* softplus(v) = log(1 + e^v).  For v > 0 it is written v + log(1 + e^-v),
+ * the same value, so that e^v is never formed where it would overflow. */
+static double softplus_f64(double v) { return v > 0.0 ? v + log1p(exp(-v)) : log1p(exp(v)); }
+
 /* ------------------------------------------------------------------------ */
 /* Fused selective scan, fp64.  Rows are (batch, channel) pairs; row r reads
  * x[r,:], delta[r,:], A[r,:] (its channel's row of A), Dskip[r], and the
@@ -308,7 +312,9 @@ int swo_affine_prefix_u32(const uint32_t* a, const uint32_t* bx, const uint32_t*
  * The optional inputs of a Mamba block (the production kernel the paper
  * compares against fuses them; Sec. 1, Sec. 6.3), all NULL / 0 by default:
  *   delta_bias[d]:  delta' = delta + delta_bias[d];
- *   softplus:       delta' = log(1 + exp(delta'))  (log1p of exp in fp64);
+ *   softplus:       delta' = log(1 + exp(delta')), evaluated in fp64 as
+ *                   log1p(exp(v)) for v <= 0 and v + log1p(exp(-v)) above
+ *                   (the same function; exp(v) would overflow for v > 709);
  *   h0[r, n]:       initial state h[-1] instead of zero (mag_0 = |h0|);
  *   z[r, t]:        y_t <- y_t * silu(z_t), silu(z) = z / (1 + exp(-z)); the
  *                   magnitude and sensitivity of y scale by |silu(z_t)|. */
@@ -346,7 +352,7 @@ static void sel_rows(int64_t r0, int64_t r1, const void* vctx) {
       for (int64_t t = 0; t < L; t++) {
         double dv = (double)dl[t];
         if (c->delta_bias) dv += (double)c->delta_bias[r];
-        if (c->softplus) dv = log1p(exp(dv));
+        if (c->softplus) dv = softplus_f64(dv);
         double a = exp(dv * An);
         if (c->a_mode == 1) a = (double)(float)a;
         const double u = dv * (double)x[t] * (double)Bm[t * N + n];
@@ -481,7 +487,7 @@ static void bwd_rows(int64_t r0, int64_t r1, int ti, const void* vctx) {
     for (int64_t t = 0; t < L; t++) {
       const double raw = (double)c->delta[r * L + t] + (c->delta_bias ? (double)c->delta_bias[r] : 0.0);
       if (c->softplus) {
-        dl[t] = log1p(exp(raw));
+        dl[t] = softplus_f64(raw);
         sg[t] = 1.0 / (1.0 + exp(-raw));
       } else {
         dl[t] = raw;
