@@ -3,17 +3,21 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
 
 One step is one call of the fused selective scan (every step of the hot path:
-bf16 widening, exp discretisation, the recurrence, the C contraction, the
-D skip and the h_last write) over one batch of synthetic input that is already
-resident in HBM.  Several input sets are rotated so that the working set is
+exp discretisation, the recurrence, the C contraction, the D skip and the
+h_last write; bf16 widening on the bf16 workload) over one batch of synthetic
+input that is already resident in HBM.  The default workload is the largest
+single-GPU one, B=1, D=5120, N=16, L=65536 in fp32 (4.04 GB of algorithmic
+traffic per step).  Several input sets are rotated so that the working set is
 larger than the 256 MB MALL and each step streams its inputs from HBM.
 
 Prints one JSON line: throughput in B*L*D*N elements/s over exactly K timed
-steps run back to back after W untimed ones, the roofline of the kernel (mean
-launch duration = the interval between HIP events recorded on the launch
-stream around the K steps, divided by K; the spread of single launches from an
-untimed pass afterwards), the HBM bandwidth it reaches, and the CPU oracle
-timed on the host cores over a bounded sample of the same workload.
+steps run back to back after W untimed ones (preceded by a clock warm-up of
+at least --clock-warmup-ms of launches, stated in the line), the HBM roofline
+of the call (algorithmic bytes / mean call duration, the interval between HIP
+events recorded on the launch stream around the K steps divided by K, against
+8 TB/s; the spread of single calls from an untimed pass afterwards), its fp32
+arithmetic against the fp32 vector peak, and the CPU oracle timed on the host
+cores over a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -31,19 +35,17 @@ if ROOT not in sys.path:
 
 import workloads as wl  # noqa: E402
 
-DEFAULT_WORKLOAD = "selective_bf16_b8_d1536_n16_l2048"
+DEFAULT_WORKLOAD = "selective_f32_b1_d5120_n16_l65536"
 
 # MI355X figures used for the roofline
 HBM_PEAK_GBS = 8000.0            # HBM3E, 8 TB/s
 N_CU, SIMD_PER_CU, CLOCK_HZ = 256, 4, 2.4e9
-# fp32 vector peak 157.3 TFLOP/s = 256 CUs x 4 SIMDs x 32 lanes x 2.4 GHz fp32
-# operations (an FMA counted as one operation of two flops): 78.6e12 lane-slots/s
-FP32_LANES_PER_SIMD = 32
-VALU_PEAK = N_CU * SIMD_PER_CU * FP32_LANES_PER_SIMD * CLOCK_HZ  # 7.86e13
-# slots the method needs per (b,d,t,n) element: delta*A' mul, (delta*x)*B mul,
-# state FMA, C FMA (4 fp32 operations) and one exp2, a transcendental issued
-# at a quarter of the fp32 rate (4 slots)
-SLOTS_PER_ELEM = 8.0
+# fp32 vector peak, as published: 157.3 TFLOP/s
+FP32_PEAK_TFLOPS = 157.3
+# fp32 flops the method does per (b,d,t,n) element: delta*A' (1), (delta*x)*B
+# (1), the state FMA (2), the C FMA (2); the exp2 is not a flop and is not counted
+FLOP_PER_ELEM = 6.0
+FLOP_PER_ELEM_BWD = 14.0
 MALL_BYTES = 256 << 20
 
 
@@ -211,6 +213,24 @@ def measure_copy_bandwidth(mib: int = 2048, reps: int = 10) -> dict:
 SPREAD_LAUNCHES = 100
 
 
+def clock_warmup(step, ms: float) -> int:
+    """Launch steps until at least `ms` of wall time has passed (synchronising
+    every few launches): the GPU raises its clock only after some tens of
+    milliseconds of sustained work, and the first launches of a cold GPU run
+    up to ~30% slower.  Returns the number of launches."""
+    import torch
+    if ms <= 0:
+        return 0
+    t0 = time.perf_counter()
+    n = 0
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        for _ in range(4):
+            step(n)
+            n += 1
+        torch.cuda.synchronize()
+    return n
+
+
 def time_launches(step, steps, warmup):
     """Run `warmup` untimed steps, then exactly `steps` timed ones, back to back,
     between one pair of HIP events on the launch stream.
@@ -302,9 +322,17 @@ def time_graph(step, steps, warmup):
 
 
 def run_timed(step, args):
+    args.clock_warmup_launches = clock_warmup(step, getattr(args, "clock_warmup_ms", 0))
     if getattr(args, "graph", False):
         return time_graph(step, args.steps, args.warmup)
     return time_launches(step, args.steps, args.warmup)
+
+
+def warmup_record(args) -> dict:
+    """How the GPU was warmed up before the timed steps (part of every line)."""
+    return {"clock_warmup_ms": getattr(args, "clock_warmup_ms", 0),
+            "clock_warmup_launches": getattr(args, "clock_warmup_launches", 0),
+            "warmup_steps": args.warmup}
 
 
 def launch_stats(gpu_per, spread, graph=False):
@@ -385,7 +413,8 @@ def bench_affine(w, args):
         "dtype": "int32" if args.int32 else "f32", "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "D": w.D, "L": w.L, "input_sets_rotated": nsets,
                    "schedule": args.schedule, "form": args.form,
-                   "launch": "hip-graph" if args.graph else "eager"},
+                   "launch": "hip-graph" if args.graph else "eager",
+                   "warmup": warmup_record(args)},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS,
                      "traffic": (measured_traffic(w) if args.schedule == "default" and not proj
@@ -399,11 +428,11 @@ def bench_affine(w, args):
     return 0
 
 
-# slots the backward needs per (b,d,t,n) element: exp2 (4 slots) plus twelve
-# fp32 operations -- delta*A', (delta*x)*B, a*h_{t-1}, the state add, the
+# fp32 flops the backward needs per (b,d,t,n) element (the exp2 not counted):
+# twelve operations -- delta*A', (delta*x)*B, a*h_{t-1}, the state add, the
 # adjoint FMA, lam*q, the dA FMA, (lam q)*A, lam*B, lam*(delta x), ds*h and
-# a*lam (the forward sweep that rebuilds the tile checkpoints is overhead)
-SLOTS_PER_ELEM_BWD = 16.0
+# a*lam -- two of them FMAs (the forward sweep that rebuilds the tile
+# checkpoints is overhead)
 
 
 def bench_bwd(w, args):
@@ -469,25 +498,26 @@ def bench_bwd(w, args):
     if args.options:
         # z read, dz written; delta bias read, its gradient written; h0 read
         abytes += (es + 4) * w.B * w.D * w.L + 8 * w.D + 4 * w.B * w.D * w.N
-    achieved = SLOTS_PER_ELEM_BWD * elems / kern
+    flops = FLOP_PER_ELEM_BWD * elems / kern
+    gbs = abytes / kern / 1e9
     out = {
         "metric": "selective-scan bwd B*L*D*N elems/s (all gradients), 1 GPU",
         "value": elems * args.steps / wall, "unit": "elems/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "D": w.D, "N": w.N, "L": w.L,
                    "pass": "backward", "dy": w.dtype, "gradients": "fp32",
                    "options": ("gate z, delta bias + softplus, initial state" if args.options
                                else "none"),
-                   "forward_checkpoints": bool(args.ckpt)},
-        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
-                     "unit": "T fp32-lane-slot/s", "frac": achieved / VALU_PEAK,
-                     "traffic": None, "kernel": "selective_bwd_kernel + selective_bwd_reduce_kernel",
+                   "forward_checkpoints": bool(args.ckpt), "warmup": warmup_record(args)},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "selective_bwd_kernel + selective_bwd_reduce_kernel",
                      "per_launch_us": launch_stats(kern, per, args.graph),
-                     "slots_per_elem": SLOTS_PER_ELEM_BWD},
-        "hbm": {"algorithmic_bytes": abytes, "achieved_GBs": abytes / kern / 1e9,
-                "peak_GBs": HBM_PEAK_GBS, "frac": abytes / kern / 1e9 / HBM_PEAK_GBS},
+                     "algorithmic_bytes": abytes},
+        "alu": {"achieved": flops / 1e12, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": flops / 1e12 / FP32_PEAK_TFLOPS, "flop_per_elem": FLOP_PER_ELEM_BWD},
     }
     print(json.dumps(out), flush=True)
     return 0
@@ -496,11 +526,12 @@ def bench_bwd(w, args):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    # the GPU reaches its steady clock only after ~200 launches of the fused
-    # forward (about 30 ms of work; the first hundred run ~30% slower), so the
-    # default warm-up covers that before the timed steps
-    ap.add_argument("--warmup", type=int, default=300)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    # the GPU reaches its steady clock only after some tens of milliseconds of
+    # sustained launches (the first ~30 ms run up to ~30% slower): launches run
+    # for at least this long before the W warm-up steps, whatever W is
+    ap.add_argument("--clock-warmup-ms", type=float, default=250.0)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-threads", type=int, default=0,
@@ -637,7 +668,7 @@ def main(argv=None):
     elems = w.elems
     value = elems * args.steps / wall
     hbm_gbs = abytes / kern / 1e9
-    alu_achieved = SLOTS_PER_ELEM * elems / kern
+    flops = FLOP_PER_ELEM * elems / kern
     # the library takes the 16-lane kernel for N = 16 unless SW_SS_LAYOUT=8 asks
     # for the 8-lane one (rows whose offsets pass 2^31 also take the latter)
     layout16 = os.environ.get("SW_SS_LAYOUT", "16") in ("", "16")
@@ -654,7 +685,7 @@ def main(argv=None):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {
             "workload": w.name, "B": w.B, "D": w.D, "N": w.N, "L": w.L,
@@ -665,21 +696,22 @@ def main(argv=None):
                         else "none"),
             "forward_checkpoints": bool(args.ckpt),
             "launch": "hip-graph" if args.graph else "eager",
+            "warmup": warmup_record(args),
         },
         "roofline": {
-            "bound": "alu",
-            "achieved": alu_achieved / 1e12,
-            "peak": VALU_PEAK / 1e12,
-            "unit": "T fp32-lane-slot/s",
-            "frac": alu_achieved / VALU_PEAK,
+            "bound": "hbm",
+            "achieved": hbm_gbs,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": hbm_gbs / HBM_PEAK_GBS,
             "traffic": (measured_traffic(w) if args.schedule == "default" and not args.options
                         and not args.ckpt and fwd_kernel == "selective_row16_kernel" else None),
             "kernel": fwd_kernel,
             "per_launch_us": launch_stats(kern, per, args.graph),
-            "slots_per_elem": SLOTS_PER_ELEM,
+            "algorithmic_bytes": abytes,
         },
-        "hbm": {"algorithmic_bytes": abytes, "achieved_GBs": hbm_gbs, "peak_GBs": HBM_PEAK_GBS,
-                "frac": hbm_gbs / HBM_PEAK_GBS},
+        "alu": {"achieved": flops / 1e12, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": flops / 1e12 / FP32_PEAK_TFLOPS, "flop_per_elem": FLOP_PER_ELEM},
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(w, inp, threads=args.cpu_threads)

@@ -35,13 +35,26 @@
 //
 // Narrow shapes (too few rows to give every SIMD a wavefront) split each row
 // into segments instead, composed with Eq. (7) in three launches that need no
-// memory beyond y: (1) each segment but the last walks from a zero state
-// (the first from h0) and records its end state U and the product P of its
-// a_t, formed as exp(A * the segment's sum of delta); (2) a fold turns these into each segment's initial state,
-// h_in(s+1) = P_s h_in(s) + U_s; (3) every segment walks from its initial
-// state and stores y.  The records of segment s live in y's first 32 words
-// of segment s+1 (P in 16, U in 16; the fold leaves h_in in the first 16),
-// which launch (3) reads before it overwrites them with y.
+// memory beyond y, in one of two forms.
+// Records form: (1) each segment but the last walks from a zero state (the
+// first from h0) and records its end state U and the product P of its a_t,
+// formed as exp(A * the segment's sum of delta); (2) a fold turns these into
+// each segment's initial state, h_in(s+1) = P_s h_in(s) + U_s; (3) every
+// segment walks from its initial state and stores y.  The records of segment
+// s live in y's first 32 words of segment s+1 (P in 16, U in 16; the fold
+// leaves h_in in the first 16), which launch (3) reads before it overwrites
+// them with y.
+// Correction form (long segments, fp32 y): (1) every segment walks from a
+// zero state (the first from h0), stores y except in its first super-tile,
+// and records P and U as above (the last segment its P beside the records
+// of its own first words, its U in h_last); (2) the fold composes them and
+// corrects h_last; (3) each later segment walks again from its initial
+// state, rewriting y, until the part of every state carried in from the
+// segment's start has faded against the segment's own terms.  By Eq. (5)
+// the state is that carried part, P_t h_in, plus the walk from zero, so y
+// beyond that point already holds the result to within 2^-26 of its
+// magnitude; with the decay of Mamba-like parameters the third launch walks
+// a small part of each segment, and the first runs every segment at once.
 #include <stdlib.h>
 
 #include <atomic>
@@ -71,6 +84,7 @@ static_assert(R16_NB == 8 && R16_NB % R16_NS == 0 && R16_LA < R16_NS,
 struct R16Smem {
   float bc[R16_NBUF][2][R16_N * R16_TS];     // [buf][B, C][n * TS + t]
   float p[R16_WAVES][R16_RPW * R16_PRS];     // per wavefront: [row][n * TS + t]
+  int vote[R16_WAVES];                       // correction walk: wavefronts not yet done
 };
 
 // Value of `v` in lane M of this lane's 16-lane row.
@@ -105,8 +119,19 @@ struct R16Ops {
 };
 
 // Segment modes of the kernel (see the top of the file).
-enum : int { R16_WHOLE = 0, R16_SEG_ENDS = 1, R16_SEG_FWD = 2 };
+//   R16_SEG_ENDS, R16_SEG_FWD: launches (1) and (3) of the records form;
+//   R16_SEG_ALL, R16_SEG_CORR: launches (1) and (3) of the correction form.
+enum : int { R16_WHOLE = 0, R16_SEG_ENDS = 1, R16_SEG_FWD = 2, R16_SEG_ALL = 3, R16_SEG_CORR = 4 };
 constexpr int R16_MAX_SEG = 16;  // segments per row at most
+// The correction walk of a segment stops once, for every state of its
+// workgroup, the part of the state carried in from the segment's start,
+// P_t h_in (P_t the product of the a since the start), is at most this
+// fraction of the magnitude m_t of the segment's own terms (the sum of their
+// absolute values, tracked by the walk).  Both P_t |h_in| and every later
+// carried part shrink or grow by the same factors |a| as m_t's terms, so
+// from then on the part left out is at most R16_CORR_EPS times the
+// magnitude of the state, and of y (an fp32 walk rounds at 2^-24 of it).
+constexpr float R16_CORR_EPS = 1.4901161193847656e-08f;  // 2^-26
 
 // The record words of the segment starting at step t of a row, in y's memory
 // (fp32 or bf16 elements; t is a multiple of 64, so the words are aligned).
@@ -134,6 +159,9 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     int64_t nseg, int64_t Lseg) {
   static_assert(!(CK && SEG != R16_WHOLE), "checkpoints are written by whole-row walks only");
   constexpr bool ENDS = SEG == R16_SEG_ENDS;  // no y: the segment's P and end state
+  constexpr bool ALL = SEG == R16_SEG_ALL;    // y from a zero state, and the segment's records
+  constexpr bool CORR = SEG == R16_SEG_CORR;  // the walk from the composed initial state
+  constexpr bool DSUM = ENDS || ALL || CORR;  // sum of delta over the segment
   constexpr int ES = (int)sizeof(IN);
   const uint32_t flags = OPT ? flags_in : 0u;
   constexpr int V = 16 / ES;              // steps a lane holds of a super-tile
@@ -145,9 +173,10 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   const int tid = threadIdx.x;
   const int w = tid / 64, lane = tid % 64;
   const int r = lane / R16_N, n = lane % R16_N;
-  // segment of this workgroup (launch (1) covers segments 0 .. nseg-2)
-  const int64_t nsl = ENDS ? nseg - 1 : nseg;
-  const int64_t sg = SEG != R16_WHOLE ? (int64_t)blockIdx.x % nsl : 0;
+  // segment of this workgroup (launch (1) of the records form covers
+  // segments 0 .. nseg-2, launch (3) of the correction form 1 .. nseg-1)
+  const int64_t nsl = (ENDS || CORR) ? nseg - 1 : nseg;
+  const int64_t sg = SEG != R16_WHOLE ? (int64_t)blockIdx.x % nsl + (CORR ? 1 : 0) : 0;
   const int64_t rblk = SEG != R16_WHOLE ? (int64_t)blockIdx.x / nsl : (int64_t)blockIdx.x;
   const int64_t ts = SEG != R16_WHOLE ? sg * Lseg : 0;  // first step of the segment
   const int64_t Ls = SEG != R16_WHOLE ? (sg == nseg - 1 ? L - ts : Lseg) : L;  // its steps
@@ -177,10 +206,13 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   const float dbv = (OPT && dbias) ? dbias[dcl] : 0.0f;
   const bool ybf = (flags & SEL_Y_BF16) != 0;
   float h = (h0 && sg == 0) ? h0[(b * D + dcl) * R16_N + n] : 0.0f;
-  if constexpr (SEG == R16_SEG_FWD) {
+  if constexpr (SEG == R16_SEG_FWD || CORR) {
     // the initial state the fold left in this segment's first words of y
     if (sg > 0) h = seg_words(yv, ybf, b * D + dcl, L, ts)[n];
   }
+  // CORR: the initial state, and the magnitude of the segment's own terms
+  const float hin = h;
+  float mag = 0.0f;
   // ENDS: this lane's share of the sum of delta over the segment; the product
   // of the segment's a_t is exp2(Al * that sum over the row's 16 lanes)
   float dsum = 0.0f;
@@ -226,7 +258,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
       if (t0 + k >= Ls) dv = xv = 0.0f;  // identity step: a = 1, u = 0
       dl[k] = dv;
       dx[k] = dv * xv;
-      if constexpr (ENDS) dsum += dv;
+      if constexpr (DSUM) dsum += dv;
     }
   };
 
@@ -266,13 +298,16 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
 #pragma unroll
     for (int q = 0; q < 4; ++q) s4[q] = __builtin_fmaf(dsk, yx[q], s4[q] + row_ror8(s4[q]));
     const int64_t t = kt * R16_T + 4 * rq;
+    // ALL: the first super-tile of every segment but the first holds the
+    // records until the correction walk writes its y
+    const bool skip = ALL && sg > 0 && t < ST;
     if constexpr (OPT) {
       if (s_row && dok && rh == 0 && t < Ls)
         *reinterpret_cast<float4*>(s_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) s4[q] *= gt[q];
-    if (dok && rh == 0 && t < Ls) {
+    if (dok && rh == 0 && t < Ls && !skip) {
       if (ybf)
         *reinterpret_cast<uint2*>(y16_row + t) =
             make_uint2(bf16x2_rne(s4[0], s4[1]), bf16x2_rne(s4[2], s4[3]));
@@ -361,7 +396,9 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
             dlv = dxv = 0.0f;
         }
         const float a = __builtin_amdgcn_exp2f(dlv * Al);
-        h = __builtin_fmaf(a, h, dxv * bq[q]);
+        const float u = dxv * bq[q];
+        h = __builtin_fmaf(a, h, u);
+        if constexpr (CORR) mag = __builtin_fmaf(a, mag, __builtin_fabsf(u));
         if constexpr (ENDS) {
           p4[q] = 0.0f;
         } else {
@@ -382,6 +419,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     wave_order();  // this wavefront's partials are written before its next reads
   };
 
+  int64_t kt_end = ntile;  // tiles walked
   for (int64_t sup = 0; sup < nsup; ++sup) {
 #pragma unroll
     for (int tt = 0; tt < TPS; ++tt) {
@@ -400,6 +438,24 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
         default: break;
       }
     }
+    if constexpr (CORR) {
+      // the carried part of each state, P h_in with P = exp2(A log2e * the
+      // row's sum of delta so far), against the walk's own magnitude; the
+      // workgroup stops together (its wavefronts share the B/C staging)
+      float srow = dsum;
+#pragma unroll
+      for (int mm = 8; mm >= 1; mm /= 2) srow += __shfl_xor(srow, mm, R16_N);
+      const float carried = __builtin_amdgcn_exp2f(Al * srow) * hin;
+      const bool done = !dok || __builtin_fabsf(carried) <= R16_CORR_EPS * mag;
+      const uint64_t open = __builtin_amdgcn_ballot_w64(!done);
+      if (lane == 0) sm.vote[w] = open != 0;
+      wg_barrier();
+      const bool stop = (sm.vote[0] | sm.vote[1] | sm.vote[2] | sm.vote[3]) == 0;
+      if (stop) {
+        kt_end = (sup + 1) * TPS;
+        break;
+      }
+    }
   }
   if constexpr (ENDS) {
     // the records of this segment, in the first words of the next one
@@ -413,8 +469,28 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   } else {
     float4 pr[8];
     read_partials(pr);
-    finish_reduce(ntile - 1, pr, yx_prev, gt_prev);
-    if (h_last && dok && (SEG == R16_WHOLE || sg == nseg - 1)) h_last[(b * D + d) * R16_N + n] = h;
+    finish_reduce(kt_end - 1, pr, yx_prev, gt_prev);
+    if constexpr (ALL) {
+      // the records of this segment: its P and end state in the first words
+      // of the next segment; the last segment's P beside the records there,
+      // its end state in h_last (the fold composes both)
+#pragma unroll
+      for (int mm = 8; mm >= 1; mm /= 2) dsum += __shfl_xor(dsum, mm, R16_N);
+      if (dok) {
+        const float P = __builtin_amdgcn_exp2f(Al * dsum);
+        if (sg < nseg - 1) {
+          float* wd = seg_words(yv, false, b * D + d, L, ts + Ls);
+          wd[n] = P;
+          wd[R16_N + n] = h;
+        } else {
+          seg_words(yv, false, b * D + d, L, ts)[2 * R16_N + n] = P;
+        }
+      }
+    }
+    if constexpr (!CORR) {
+      if (h_last && dok && (SEG == R16_WHOLE || sg == nseg - 1))
+        h_last[(b * D + d) * R16_N + n] = h;
+    }
   }
 }
 
@@ -449,6 +525,41 @@ __global__ __launch_bounds__(256) void row16_fold_kernel(void* __restrict__ yv, 
   }
 }
 
+// Launch (2) of the correction form: one lane per (row, state) composes the
+// segments' records in order, h_in(1) = U_0 (segment 0 started from h0),
+// h_in(s+1) = P_s h_in(s) + U_s, leaves h_in(s) in the first words of segment
+// s, and corrects the final state: h_last = P_last h_in(last) + U_last.
+__global__ __launch_bounds__(256) void row16_fold_corr_kernel(float* __restrict__ y,
+                                                              float* __restrict__ h_last,
+                                                              int64_t R, int64_t L, int64_t nseg,
+                                                              int64_t Lseg) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= R * R16_N) return;
+  const int64_t row = i / R16_N;
+  const int n = (int)(i % R16_N);
+  float P[R16_MAX_SEG], U[R16_MAX_SEG];
+#pragma unroll
+  for (int sgi = 1; sgi < R16_MAX_SEG; ++sgi) {
+    if (sgi < nseg) {
+      const float* wd = seg_words(y, false, row, L, sgi * Lseg);
+      P[sgi] = wd[n];  // of segment sgi - 1
+      U[sgi] = wd[R16_N + n];
+    }
+  }
+  float h = 0.0f;
+#pragma unroll
+  for (int sgi = 1; sgi < R16_MAX_SEG; ++sgi) {
+    if (sgi < nseg) {
+      h = sgi == 1 ? U[sgi] : __builtin_fmaf(P[sgi], h, U[sgi]);
+      seg_words(y, false, row, L, sgi * Lseg)[n] = h;
+    }
+  }
+  if (h_last) {
+    const float Pl = seg_words(y, false, row, L, (nseg - 1) * Lseg)[2 * R16_N + n];
+    h_last[row * R16_N + n] = __builtin_fmaf(Pl, h, h_last[row * R16_N + n]);
+  }
+}
+
 }  // namespace
 
 // True when the N = 16 layout can take the call: vector-aligned rows, and
@@ -473,9 +584,15 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
 // segment is at least one super-tile, at most R16_MAX_SEG per row (the fold
 // walks them in order).  SW_SS_SEGMENTS forces a count (1: whole rows).
 // Returns the count and sets *Lseg (a multiple of the super-tile; the last
-// segment takes the rest of the row, at least Lseg steps).
-int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, int64_t* Lseg) {
+// segment takes the rest of the row, at least Lseg steps) and *corr: true
+// for the correction form (segments of at least R16_CORR_MIN_LSEG steps,
+// when the call allows it: fp32 y, no checkpoints), false for the records
+// form.  SW_SS_SEGFORM=1 or 2 forces the records or the correction form.
+constexpr int64_t R16_CORR_MIN_LSEG = 4096;
+int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, bool corr_ok, int64_t* Lseg,
+                       bool* corr) {
   *Lseg = L;
+  *corr = false;
   int64_t want = 1;
   const char* env = getenv("SW_SS_SEGMENTS");
   if (env && *env) {
@@ -517,6 +634,9 @@ int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, int64_t* Lseg) {
     *Lseg = L;
     return 1;
   }
+  *corr = corr_ok && *Lseg >= R16_CORR_MIN_LSEG;
+  const char* fenv = getenv("SW_SS_SEGFORM");
+  if (fenv && *fenv) *corr = corr_ok && atoi(fenv) == 2;
   return nseg;
 }
 
@@ -542,6 +662,34 @@ void launch_row16_segments(const SelArgs& a, int64_t ndb, uint32_t flags, int64_
                      ndb, flags, nullptr, (int64_t)0, a.s_out, nseg, Lseg);
 }
 
+// The correction form: (1) every segment walks from a zero state (the first
+// from h0), stores y (all but its first super-tile) and records its P and
+// end state; (2) the fold composes the records into each segment's initial
+// state and corrects h_last; (3) every segment but the first walks again from
+// its initial state, rewriting y, until the part carried in from the start
+// is negligible against the segment's own terms (R16_CORR_EPS).
+template <typename IN, bool OPT>
+void launch_row16_corr(const SelArgs& a, int64_t ndb, uint32_t flags, int64_t nseg,
+                       int64_t Lseg, hipStream_t s) {
+  const int64_t R = a.B * a.D;
+  const int64_t rblocks = a.B * ndb;
+  hipLaunchKernelGGL((selective_row16_kernel<IN, OPT, false, R16_SEG_ALL>),
+                     dim3((unsigned)(rblocks * nseg)), dim3(256), 0, s,
+                     static_cast<const IN*>(a.x), static_cast<const IN*>(a.delta), a.A,
+                     static_cast<const IN*>(a.Bm), static_cast<const IN*>(a.Cm), a.Dskip,
+                     static_cast<const IN*>(a.z), a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L,
+                     ndb, flags, nullptr, (int64_t)0, a.s_out, nseg, Lseg);
+  const int64_t lanes = R * R16_N;
+  hipLaunchKernelGGL(row16_fold_corr_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256),
+                     0, s, static_cast<float*>(a.y), a.h_last, R, a.L, nseg, Lseg);
+  hipLaunchKernelGGL((selective_row16_kernel<IN, OPT, false, R16_SEG_CORR>),
+                     dim3((unsigned)(rblocks * (nseg - 1))), dim3(256), 0, s,
+                     static_cast<const IN*>(a.x), static_cast<const IN*>(a.delta), a.A,
+                     static_cast<const IN*>(a.Bm), static_cast<const IN*>(a.Cm), a.Dskip,
+                     static_cast<const IN*>(a.z), a.delta_bias, a.h0, a.y, nullptr, a.D, a.L,
+                     ndb, flags, nullptr, (int64_t)0, a.s_out, nseg, Lseg);
+}
+
 template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s) {
   const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.s_out;
@@ -554,8 +702,17 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
   // narrow shapes: the segmented form (not with checkpoints, which are
   // written by whole-row walks)
   int64_t Lseg = a.L;
-  const int64_t nseg =
-      a.ckpt ? 1 : row16_segments(grid, a.L, 16 * (16 / (int64_t)sizeof(IN)), &Lseg);
+  bool corr = false;
+  const int64_t nseg = a.ckpt ? 1
+                              : row16_segments(grid, a.L, 16 * (16 / (int64_t)sizeof(IN)),
+                                               !a.y_bf16, &Lseg, &corr);
+  if (nseg > 1 && grid * nseg < ((int64_t)1 << 31) && corr) {
+    if (opt)
+      launch_row16_corr<IN, true>(a, ndb, flags, nseg, Lseg, s);
+    else
+      launch_row16_corr<IN, false>(a, ndb, flags, nseg, Lseg, s);
+    return check_launch("selective_row16_kernel (segments, correction form)");
+  }
   if (nseg > 1 && grid * nseg < ((int64_t)1 << 31)) {
     if (opt)
       launch_row16_segments<IN, true>(a, ndb, flags, nseg, Lseg, s);

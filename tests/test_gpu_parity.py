@@ -484,6 +484,68 @@ def test_selective_segments_no_dskip_no_hlast(sw, monkeypatch, dtype):
     assert rownorm_rel(y.cpu().numpy(), y1.cpu().numpy()) <= 1e-5
 
 
+# The correction form of the segmented walk (fp32 y): every segment walks from
+# a zero state in one launch, a fold composes the carries, and a third launch
+# walks each later segment again from its composed state until the carried
+# part is negligible.  Short segments never reach that point (the walk covers
+# the whole segment); the long ones stop early.  (B, D, L), forced count.
+_CORR_CASES = [((1, 37, 1000), "3"), ((2, 16, 512), "4"), ((3, 7, 776), "5"),
+               ((1, 20, 16384), "2"), ((1, 24, 8192), "auto")]
+
+
+@pytest.mark.parametrize("case", _CORR_CASES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("opts", [(), ("h0", "bias", "softplus", "z")])
+def test_selective_segments_correction(sw, monkeypatch, case, dtype, opts):
+    (B, D, L), segs = case
+    monkeypatch.setenv("SW_SS_SEGFORM", "2")
+    if segs != "auto":
+        monkeypatch.setenv("SW_SS_SEGMENTS", segs)
+    _say("case selective segments correction", dtype, (B, D, L), segs, opts)
+    inp, ex = _ex_inputs(B, D, 16, L, 9400 + B + D + L, dtype, opts)
+    softplus = "softplus" in opts
+    y, hl = _run_ex(sw, inp, ex, dtype, softplus, False)
+    o = _ex_oracle(inp, ex, softplus)
+    _y_gate(y, o, False, f"correction y {dtype} {(B, D, L)} {segs} {opts}")
+    assert_gate(fp_gate(hl.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]),
+                f"correction h_last {dtype} {(B, D, L)} {segs} {opts}")
+    assert rownorm_rel(y.cpu().numpy(), o["y"]) <= 1e-5
+    # the same call again gives the same bits (fixed segments, no atomics)
+    y2, hl2 = _run_ex(sw, inp, ex, dtype, softplus, False)
+    assert torch.equal(y, y2) and torch.equal(hl, hl2)
+
+
+@pytest.mark.parametrize("kind", ["no_decay", "growth", "zero_carry", "stress"])
+def test_selective_segments_correction_regimes(sw, monkeypatch, kind):
+    """The correction walk where the carried part never fades (A = 0: the
+    walk covers every segment whole), where it grows (A > 0), where there is
+    none (x = 0 before the last segment: every composed state is zero and the
+    walk stops after its first super-tile) and where it fades at very
+    different rates per state (the stress recipe's delta and A)."""
+    B, D, N, L = 1, 20, 16, 8192
+    monkeypatch.setenv("SW_SS_SEGFORM", "2")
+    monkeypatch.setenv("SW_SS_SEGMENTS", "4")
+    _say("case selective segments correction regime", kind)
+    inp = wl.selective_inputs(B, D, N, L, 9500, "f32", stress=(kind == "stress"))
+    if kind == "no_decay":
+        inp["A"] = np.zeros_like(inp["A"])
+    elif kind == "growth":
+        inp["A"] = np.abs(inp["A"]) * np.float32(1e-4)
+    elif kind == "zero_carry":
+        inp["x"] = inp["x"].copy()
+        inp["x"][:, :, : 3 * L // 4] = 0.0
+    y, hl = _run_selective(sw, inp, "f32")
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                              inp["Dskip"], bounds=True)
+    assert_gate(fp_gate(y.cpu().numpy(), o["y"], o["y_mag"], o["y_sens"]), f"correction {kind} y")
+    assert_gate(fp_gate(hl.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]),
+                f"correction {kind} h_last")
+    # against the whole-row walk of the same call
+    monkeypatch.setenv("SW_SS_SEGMENTS", "1")
+    y1, hl1 = _run_selective(sw, inp, "f32")
+    assert rownorm_rel(y.cpu().numpy(), y1.cpu().numpy()) <= 1e-5
+
+
 def test_selective_L0_returns_h0(sw):
     x = torch.empty((2, 3, 0), device="cuda")
     A = torch.randn((3, 16), device="cuda")
