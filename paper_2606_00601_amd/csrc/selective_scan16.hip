@@ -562,6 +562,18 @@ __global__ __launch_bounds__(256) void row16_fold_corr_kernel(float* __restrict_
 
 }  // namespace
 
+// The fold of the correction form, shared with the 64-row layout
+// (selective_scan_rows64.hip), which keeps its records in the same places.
+void launch_fold_corr(float* y, float* h_last, int64_t R, int64_t L, int64_t nseg, int64_t Lseg,
+                      hipStream_t s) {
+  const int64_t lanes = R * R16_N;
+  hipLaunchKernelGGL(row16_fold_corr_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0,
+                     s, y, h_last, R, L, nseg, Lseg);
+}
+
+template <typename IN>
+bool try_quad(const SelArgs& a, hipStream_t s, int* status);
+
 // True when the N = 16 layout can take the call: vector-aligned rows, and
 // every byte offset of a workgroup (including loads run ahead past the end)
 // below 2^31.
@@ -679,9 +691,7 @@ void launch_row16_corr(const SelArgs& a, int64_t ndb, uint32_t flags, int64_t ns
                      static_cast<const IN*>(a.Bm), static_cast<const IN*>(a.Cm), a.Dskip,
                      static_cast<const IN*>(a.z), a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L,
                      ndb, flags, nullptr, (int64_t)0, a.s_out, nseg, Lseg);
-  const int64_t lanes = R * R16_N;
-  hipLaunchKernelGGL(row16_fold_corr_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256),
-                     0, s, static_cast<float*>(a.y), a.h_last, R, a.L, nseg, Lseg);
+  launch_fold_corr(static_cast<float*>(a.y), a.h_last, R, a.L, nseg, Lseg, s);
   hipLaunchKernelGGL((selective_row16_kernel<IN, OPT, false, R16_SEG_CORR>),
                      dim3((unsigned)(rblocks * (nseg - 1))), dim3(256), 0, s,
                      static_cast<const IN*>(a.x), static_cast<const IN*>(a.delta), a.A,
@@ -692,6 +702,9 @@ void launch_row16_corr(const SelArgs& a, int64_t ndb, uint32_t flags, int64_t ns
 
 template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s) {
+  // few rows, long sequences: four lanes per row, four states per lane
+  int st = SW_OK;
+  if (try_quad<IN>(a, s, &st)) return st;
   const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.s_out;
   const int64_t ndb = (a.D + R16_ROWS - 1) / R16_ROWS;
   const int64_t grid = a.B * ndb;

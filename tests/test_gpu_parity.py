@@ -546,6 +546,70 @@ def test_selective_segments_correction_regimes(sw, monkeypatch, kind):
     assert rownorm_rel(y.cpu().numpy(), y1.cpu().numpy()) <= 1e-5
 
 
+# The quad layout (four lanes per row, four states per lane, 16 rows per
+# wavefront) taken by few-row, long calls; forced here on small shapes
+# (SW_SS_QUAD=1) with the segment count given: D not a multiple of 64 leaves
+# wavefronts with rows past D and wavefronts with none, L a multiple of 16 but
+# not of 64 gives a last segment longer than the others, one segment is the
+# whole-row walk.  (B, D, L), segments.
+_QUAD_CASES = [((1, 37, 1040), "2"), ((2, 100, 2048), "3"), ((1, 64, 4096), "4"),
+                 ((1, 5, 16), "1"), ((3, 130, 512), "1"), ((1, 70, 8192), "7")]
+
+
+@pytest.mark.parametrize("case", _QUAD_CASES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("opts", [(), ("h0", "bias", "softplus", "z")])
+def test_selective_quad(sw, monkeypatch, case, dtype, opts):
+    (B, D, L), segs = case
+    monkeypatch.setenv("SW_SS_QUAD", "1")
+    monkeypatch.setenv("SW_SS_SEGMENTS", segs)
+    _say("case selective quad", dtype, (B, D, L), segs, opts)
+    inp, ex = _ex_inputs(B, D, 16, L, 9600 + B + D + L, dtype, opts)
+    softplus = "softplus" in opts
+    y, hl = _run_ex(sw, inp, ex, dtype, softplus, False)
+    o = _ex_oracle(inp, ex, softplus)
+    _y_gate(y, o, False, f"quad y {dtype} {(B, D, L)} {segs} {opts}")
+    assert_gate(fp_gate(hl.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]),
+                f"quad h_last {dtype} {(B, D, L)} {segs} {opts}")
+    assert rownorm_rel(y.cpu().numpy(), o["y"]) <= 1e-5
+    y2, hl2 = _run_ex(sw, inp, ex, dtype, softplus, False)
+    assert torch.equal(y, y2) and torch.equal(hl, hl2)
+
+
+@pytest.mark.parametrize("kind", ["no_decay", "growth", "zero_carry", "stress", "no_dskip"])
+def test_selective_quad_regimes(sw, monkeypatch, kind):
+    """The quad layout's correction walk where the carried part never fades,
+    grows, is zero, or fades at very different rates (as for the 16-lane
+    layout); and without Dskip and h_last."""
+    B, D, N, L = 1, 90, 16, 8192
+    monkeypatch.setenv("SW_SS_QUAD", "1")
+    monkeypatch.setenv("SW_SS_SEGMENTS", "4")
+    _say("case selective quad regime", kind)
+    inp = wl.selective_inputs(B, D, N, L, 9700, "f32", stress=(kind == "stress"))
+    if kind == "no_decay":
+        inp["A"] = np.zeros_like(inp["A"])
+    elif kind == "growth":
+        inp["A"] = np.abs(inp["A"]) * np.float32(1e-4)
+    elif kind == "zero_carry":
+        inp["x"] = inp["x"].copy()
+        inp["x"][:, :, : 3 * L // 4] = 0.0
+    with_d = kind != "no_dskip"
+    y, hl = _run_selective(sw, inp, "f32", with_dskip=with_d, want_h_last=with_d)
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                              inp["Dskip"] if with_d else None, bounds=True)
+    assert_gate(fp_gate(y.cpu().numpy(), o["y"], o["y_mag"], o["y_sens"]), f"quad {kind} y")
+    if with_d:
+        assert_gate(fp_gate(hl.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]),
+                    f"quad {kind} h_last")
+    else:
+        assert hl is None
+    # against the whole-row walk of the 16-lane layout
+    monkeypatch.setenv("SW_SS_QUAD", "0")
+    monkeypatch.setenv("SW_SS_SEGMENTS", "1")
+    y1, _ = _run_selective(sw, inp, "f32", with_dskip=with_d, want_h_last=with_d)
+    assert rownorm_rel(y.cpu().numpy(), y1.cpu().numpy()) <= 1e-5
+
+
 def test_selective_L0_returns_h0(sw):
     x = torch.empty((2, 3, 0), device="cuda")
     A = torch.randn((3, 16), device="cuda")
