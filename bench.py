@@ -60,11 +60,15 @@ def algorithmic_bytes(w) -> int:
 
 
 # the sources each path's kernels are built from (traffic records are keyed to them)
-FWD_SOURCES = ("selective_common.h", "selective_scan.hip", "selective_scan16.hip", "sw_internal.h")
+FWD_SOURCES = ("selective_common.h", "selective_scan.hip", "selective_scan16.hip",
+               "selective_scan_quad.hip", "sw_internal.h")
 AFFINE_SOURCES = ("affine_scan.hip", "sw_internal.h")
 
 # workload -> committed HBM traffic record (rocprofv3 FETCH_SIZE / WRITE_SIZE)
 TRAFFIC_RECORDS = {
+    "selective_f32_b1_d5120_n16_l65536": "selective_quad_f32_b1_d5120_n16_l65536_traffic.txt",
+    "selective_f32_b4_d2048_n16_l8192_stress":
+        "selective_row16_f32_b4_d2048_n16_l8192_stress_traffic.txt",
     "selective_bf16_b8_d1536_n16_l2048": "selective_row16_bf16_b8_d1536_n16_l2048_traffic.txt",
     "affine_f32_b1_d5120_l65536": "affine_rows_f32_b1_d5120_l65536_traffic.txt",
     "affine_f32_b8_d1536_l2048": "affine_scan_f32_b8_d1536_l2048_traffic.txt",
@@ -84,9 +88,10 @@ def kernel_source_sha256(path: str = "selective") -> str:
     return h.hexdigest()
 
 
-def measured_traffic(w):
-    """HBM bytes per launch from the committed counter summary, if it was taken on
-    the current kernel sources and this workload; else None."""
+def measured_traffic(w, launch=None):
+    """HBM bytes per call from the committed counter summary, if it was taken on
+    the current kernel sources, this workload and (for the fused forward) the
+    same launches; else None."""
     name = TRAFFIC_RECORDS.get(w.name)
     if name is None:
         return None
@@ -101,6 +106,8 @@ def measured_traffic(w):
                 k, v = line.split(":", 1)
                 rec[k.strip()] = v.strip()
     if rec.get("kernel_source_sha256") != sha or rec.get("workload") != w.name:
+        return None
+    if launch is not None and rec.get("launch") != launch:
         return None
     try:
         return int(float(rec["hbm_bytes_per_launch"]))
@@ -663,17 +670,15 @@ def main(argv=None):
             sw.selective_scan_fwd_schedule(s["x"], s["delta"], s["A"], s["Bm"], s["Cm"],
                                            s["Dskip"], schedule=args.schedule)
 
+    step(0)
+    launch = sw.last_launch()  # the kernels the library picked for this call
     wall, kern, per = run_timed(step, args)
 
     elems = w.elems
     value = elems * args.steps / wall
     hbm_gbs = abytes / kern / 1e9
     flops = FLOP_PER_ELEM * elems / kern
-    # the library takes the 16-lane kernel for N = 16 unless SW_SS_LAYOUT=8 asks
-    # for the 8-lane one (rows whose offsets pass 2^31 also take the latter)
-    layout16 = os.environ.get("SW_SS_LAYOUT", "16") in ("", "16")
-    fwd_kernel = ("selective_blelloch_kernel" if args.schedule == "blelloch" else
-                  "selective_row16_kernel" if w.N == 16 and layout16 else "selective_fwd_kernel")
+    fwd_kernel = launch
     out = {
         "metric": "selective-scan fwd B*L*D*N elems/s (+ achieved HBM GB/s vs peak), 1 GPU",
         "value": value,
@@ -704,8 +709,8 @@ def main(argv=None):
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": hbm_gbs / HBM_PEAK_GBS,
-            "traffic": (measured_traffic(w) if args.schedule == "default" and not args.options
-                        and not args.ckpt and fwd_kernel == "selective_row16_kernel" else None),
+            "traffic": (measured_traffic(w, launch) if args.schedule == "default"
+                        and not args.options and not args.ckpt else None),
             "kernel": fwd_kernel,
             "per_launch_us": launch_stats(kern, per, args.graph),
             "algorithmic_bytes": abytes,

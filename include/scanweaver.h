@@ -331,6 +331,13 @@ const char* sw_status_string(int status);
 /* Message for the calling thread's last non-OK return ("" if none). */
 const char* sw_last_error(void);
 
+/* Which kernels the calling thread's last successful fused forward call
+ * (sw_selective_scan_fwd*, "" before any) enqueued: the layout, and for a
+ * call split into segments their count, length and form -- e.g.
+ * "selective_quad_kernel: 12 segments of 5440 steps, correction form (3
+ * launches)".  For tuning and benchmarks; the text is not a stable format. */
+const char* sw_last_launch(void);
+
 #ifdef __cplusplus
 }
 #endif

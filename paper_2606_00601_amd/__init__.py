@@ -33,7 +33,7 @@ import torch
 from ._lib import (SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32,  # noqa: F401
                    ScanWeaverError, check, last_error, lib, status_string)
 
-__all__ = ["affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
+__all__ = ["last_launch", "affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
            "affine_scan_proj", "affine_scan_proj_i32",
            "selective_scan_fwd", "selective_scan_fwd_schedule", "selective_scan_bwd", "new_ckpt",
            "selective_scan_fn",
@@ -43,6 +43,12 @@ __all__ = ["affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_sca
 
 def version() -> int:
     return int(lib().sw_version())
+
+
+def last_launch() -> str:
+    """Which kernels this thread's last fused forward call enqueued (layout,
+    segment count and form); for tuning and benchmarks, not a stable format."""
+    return lib().sw_last_launch().decode()
 
 
 def _ptr(t):

@@ -42,6 +42,7 @@ SIGNATURES = {
     "sw_get_stream": (_vp, []),
     "sw_status_string": (ctypes.c_char_p, [_int]),
     "sw_last_error": (ctypes.c_char_p, []),
+    "sw_last_launch": (ctypes.c_char_p, []),
 }
 
 _lock = threading.Lock()

@@ -160,6 +160,7 @@ int selective_blelloch_fwd(const SelArgs& a) {
                        0, s, static_cast<const float*>(a.x), static_cast<const float*>(a.delta),
                        a.A, static_cast<const float*>(a.Bm), static_cast<const float*>(a.Cm),
                        a.Dskip, static_cast<float*>(a.y), a.h_last, R, a.D, (int)a.N, a.L);
+  note_launch("selective_blelloch_kernel: the Blelloch tree, whole rows");
   return check_launch("selective_blelloch_kernel");
 }
 

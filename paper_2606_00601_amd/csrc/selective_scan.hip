@@ -621,6 +621,8 @@ int launch_cfg(const SelArgs& a, hipStream_t s) {
                      a.ckpt, (a.L + 7) / 8, a.s_out);
   st = check_launch("selective_fwd_kernel");
   if (st != SW_OK) ss.invalidate();
+  note_launch("selective_fwd_kernel: %d states per lane, %lld chunks per row", NPL,
+              (long long)p.nchunks);
   return st;
 }
 

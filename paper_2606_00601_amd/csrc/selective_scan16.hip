@@ -724,6 +724,8 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
       launch_row16_corr<IN, true>(a, ndb, flags, nseg, Lseg, s);
     else
       launch_row16_corr<IN, false>(a, ndb, flags, nseg, Lseg, s);
+    note_launch("selective_row16_kernel: %lld segments of %lld steps, correction form (3 launches)",
+                (long long)nseg, (long long)Lseg);
     return check_launch("selective_row16_kernel (segments, correction form)");
   }
   if (nseg > 1 && grid * nseg < ((int64_t)1 << 31)) {
@@ -731,6 +733,8 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
       launch_row16_segments<IN, true>(a, ndb, flags, nseg, Lseg, s);
     else
       launch_row16_segments<IN, false>(a, ndb, flags, nseg, Lseg, s);
+    note_launch("selective_row16_kernel: %lld segments of %lld steps, records form (3 launches)",
+                (long long)nseg, (long long)Lseg);
     return check_launch("selective_row16_kernel (segments)");
   }
   auto kern = opt ? (a.ckpt ? selective_row16_kernel<IN, true, true, R16_WHOLE>
@@ -742,6 +746,7 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
                      static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(a.z),
                      a.delta_bias, a.h0, a.y, a.h_last, a.D, a.L, ndb, flags, a.ckpt,
                      (a.L + 7) / 8, a.s_out, (int64_t)1, a.L);
+  note_launch("selective_row16_kernel: whole rows");
   return check_launch("selective_row16_kernel");
 }
 

@@ -457,6 +457,11 @@ bool try_quad(const SelArgs& a, hipStream_t s, int* status) {
   else
     launch_quad_t<IN, false>(a, flags, nseg, Lseg, s);
   *status = check_launch("selective_quad_kernel");
+  if (nseg > 1)
+    note_launch("selective_quad_kernel: %lld segments of %lld steps, correction form (3 launches)",
+                (long long)nseg, (long long)Lseg);
+  else
+    note_launch("selective_quad_kernel: whole rows");
   return true;
 }
 

@@ -30,6 +30,7 @@ int affine_scan_io_u32(const uint32_t* a, const uint32_t* b, const uint32_t* x, 
 namespace {
 thread_local hipStream_t tls_stream = nullptr;
 thread_local char tls_msg[512] = "";
+thread_local char tls_launch[256] = "";
 bool pool_ready[64] = {};  // guarded by scratch_mu
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
@@ -341,6 +342,13 @@ int fail(int status, const char* fmt, ...) {
   vsnprintf(tls_msg, sizeof(tls_msg), fmt, ap);
   va_end(ap);
   return status;
+}
+
+void note_launch(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(tls_launch, sizeof(tls_launch), fmt, ap);
+  va_end(ap);
 }
 
 hipStream_t current_stream() { return tls_stream; }
@@ -674,3 +682,5 @@ SW_API const char* sw_status_string(int status) {
 }
 
 SW_API const char* sw_last_error(void) { return sw::tls_msg; }
+
+SW_API const char* sw_last_launch(void) { return sw::tls_launch; }

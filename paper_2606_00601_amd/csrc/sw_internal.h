@@ -19,6 +19,9 @@ namespace sw {
 int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 hipStream_t current_stream();
 int check_launch(const char* what);  // hipGetLastError -> SW_ERR_HIP with a message
+// Records, for sw_last_launch(), which kernels the calling thread's last
+// fused forward enqueued.
+void note_launch(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 
 // Zero `words` 32-bit words with a plain kernel (no memset node).
 int zero_words(uint32_t* p, size_t words, hipStream_t s);
