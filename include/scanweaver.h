@@ -99,6 +99,32 @@ int sw_affine_scan(const float* a, const float* bx, const float* h0, float* h_ou
 int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t* h0, int32_t* h_out,
                        int64_t B, int64_t D, int64_t L);
 
+/*
+ * sw_affine_scan for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, layout, results (within fp32 rounding of the same
+ * schedule) and errors as sw_affine_scan, but no hipMalloc, hipFree or
+ * allocating library routine is called: the look-back tickets and chunk
+ * carries live in a static array in the library's device code (256 bytes +
+ * 24 bytes per chunk, 1.5 MiB for SW_NOALLOC_MAX_CHUNKS chunks), one copy per
+ * GPU, held until the process ends; its address is looked up on the first
+ * call on each device.  Each call clears the part it uses with a fill kernel
+ * on the call's stream before the scan.
+ *   - Calls whose chunk-parallel look-back kernel would need more than
+ *     SW_NOALLOC_MAX_CHUNKS chunks return SW_ERR_UNSUPPORTED before enqueuing
+ *     anything.  That kernel runs when L > 2048 and B*D < 8 * (compute
+ *     units); its chunk count is B * D * ceil(L / 2048).  Other calls (one
+ *     chunk per row, or enough rows to give each its own workgroup) use no
+ *     scratch and have no limit beyond sw_affine_scan's.
+ *   - Every call on one GPU shares that GPU's array: two calls that may run
+ *     at the same time on one GPU (on different streams, or from different
+ *     host threads without ordering) race and give wrong results.  Order
+ *     them on one stream.
+ */
+#define SW_NOALLOC_MAX_CHUNKS 65536
+int sw_affine_scan_noalloc(const float* a, const float* bx, const float* h0, float* h_out,
+                           int64_t B, int64_t D, int64_t L);
+
 /* Scan schedules of sw_affine_scan_schedule. */
 enum {
   SW_SCHED_DEFAULT = 0,  /* the library's: lane-sequential composition, DPP wavefront scan,

@@ -33,7 +33,7 @@ import torch
 from ._lib import (SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32,  # noqa: F401
                    ScanWeaverError, check, last_error, lib, status_string)
 
-__all__ = ["last_launch", "affine_scan", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
+__all__ = ["last_launch", "affine_scan", "affine_scan_noalloc", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
            "affine_scan_proj", "affine_scan_proj_i32",
            "selective_scan_fwd", "selective_scan_fwd_schedule", "selective_scan_bwd", "new_ckpt",
            "selective_scan_fn",
@@ -123,6 +123,15 @@ def _affine(fn, where, dtype, a, bx, h0, out):
 def affine_scan(a, bx, h0=None, out=None):
     """Inclusive states of h_t = a_t h_{t-1} + bx_t (fp32, shape (B, D, L))."""
     return _affine(lib().sw_affine_scan, "sw_affine_scan", torch.float32, a, bx, h0, out)
+
+
+def affine_scan_noalloc(a, bx, h0=None, out=None):
+    """:func:`affine_scan` through the entry point that allocates no device
+    memory (its look-back scratch is a fixed array in the library; calls with
+    more than ``SW_NOALLOC_MAX_CHUNKS`` look-back chunks are refused).  With
+    ``out`` given, the call itself allocates nothing."""
+    return _affine(lib().sw_affine_scan_noalloc, "sw_affine_scan_noalloc", torch.float32, a, bx,
+                   h0, out)
 
 
 def affine_scan_i32(a, bx, h0=None, out=None):

@@ -28,6 +28,7 @@ SIGNATURES = {
     "sw_version": (_int, []),
     "sw_affine_scan": (_int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64]),
     "sw_affine_scan_i32": (_int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64]),
+    "sw_affine_scan_noalloc": (_int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64]),
     "sw_affine_scan_schedule": (_int, [_vp] * 4 + [_i64] * 3 + [_int]),
     "sw_selective_scan_fwd_schedule": (_int, [_vp] * 8 + [_i64] * 4 + [_int] * 2),
     "sw_affine_scan_schedule_i32": (_int, [_vp] * 4 + [_i64] * 3 + [_int]),

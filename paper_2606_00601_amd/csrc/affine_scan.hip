@@ -24,7 +24,16 @@
 // hold a ticket, which guarantees forward progress.  When the rows alone fill
 // the GPU, affine_rows_kernel below walks each row in one workgroup instead
 // and no carry leaves the chip.
+#include <mutex>
+
 #include "sw_internal.h"
+
+// Scratch of the entry point that allocates nothing (sw_affine_scan_noalloc):
+// the ticket counter in the first 256 bytes, then three carry words per chunk
+// for at most SW_NOALLOC_MAX_CHUNKS chunks.  Each GPU holds its own copy,
+// found by hipGetSymbolAddress once per device; host code uses only that
+// address, never the array's name.
+static __device__ __align__(256) unsigned long long scratch[32 + 3 * (int64_t)SW_NOALLOC_MAX_CHUNKS];
 
 namespace sw {
 namespace {
@@ -388,8 +397,34 @@ __global__ __launch_bounds__(AS_THREADS) void affine_rows_kernel(const AffIO<T> 
   }
 }
 
+std::mutex scratch_addr_mu;
+unsigned long long* scratch_addr[64] = {};  // per device, guarded by scratch_addr_mu
+
+// The device address of `scratch` on device `dev` (the current device).
+int static_scratch(int dev, unsigned long long** out) {
+  *out = nullptr;
+  if (dev < 0 || dev >= 64)
+    return fail(SW_ERR_UNSUPPORTED, "device %d: the static scratch table holds 64 devices", dev);
+  std::lock_guard<std::mutex> g(scratch_addr_mu);
+  if (!scratch_addr[dev]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(SW_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                  hipGetErrorString(e));
+    }
+    scratch_addr[dev] = static_cast<unsigned long long*>(p);
+  }
+  *out = scratch_addr[dev];
+  return SW_OK;
+}
+
+// `fixed`: take the look-back scratch from the static array instead of the
+// per-stream allocation, clearing the ticket and this call's carry words with
+// a fill kernel first (so every call starts from epoch 1 and ticket 0).
 template <typename T, bool IO>
-int launch_affine(const AffIO<T>& io, int64_t R, int64_t L, bool vec) {
+int launch_affine(const AffIO<T>& io, int64_t R, int64_t L, bool vec, bool fixed = false) {
   hipStream_t s = current_stream();
   constexpr int64_t CH = (int64_t)AS_THREADS * AS_K;
   int dev = 0, cus = 0;
@@ -408,6 +443,28 @@ int launch_affine(const AffIO<T>& io, int64_t R, int64_t L, bool vec) {
   const int64_t nchunks = (L + CH - 1) / CH;
   const int64_t total = R * nchunks;
   const int64_t grid = total < 65536 ? total : 65536;
+  auto kern = vec ? affine_scan_kernel<T, AS_K, true, IO> : affine_scan_kernel<T, AS_K, false, IO>;
+  if (fixed) {
+    unsigned long long* base = nullptr;
+    if (nchunks > 1) {
+      if (total > (int64_t)SW_NOALLOC_MAX_CHUNKS)
+        return fail(SW_ERR_UNSUPPORTED,
+                    "%lld look-back chunks of %lld steps exceed the %d the static scratch holds",
+                    (long long)total, (long long)CH, (int)SW_NOALLOC_MAX_CHUNKS);
+      int cur = 0;
+      hipError_t e = hipGetDevice(&cur);
+      if (e != hipSuccess) return fail(SW_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+      int st = static_scratch(cur, &base);
+      if (st != SW_OK) return st;
+      // 64 words of ticket area, then 2 words per 64-bit carry word
+      st = zero_words(reinterpret_cast<uint32_t*>(base), (size_t)(64 + 6 * total), s);
+      if (st != SW_OK) return st;
+    }
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(AS_THREADS), 0, s, io, R, L, nchunks,
+                       total, base ? base + 32 : nullptr, reinterpret_cast<uint32_t*>(base), 0u,
+                       1u);
+    return check_launch("affine_scan_kernel");
+  }
   ScratchSession ss;
   if (nchunks > 1) {
     if (total >= ((int64_t)1 << 31))
@@ -416,7 +473,6 @@ int launch_affine(const AffIO<T>& io, int64_t R, int64_t L, bool vec) {
     int st = ss.reserve((size_t)total * 3, (uint32_t)(total + grid), s);
     if (st != SW_OK) return st;
   }
-  auto kern = vec ? affine_scan_kernel<T, AS_K, true, IO> : affine_scan_kernel<T, AS_K, false, IO>;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(AS_THREADS), 0, s, io, R, L, nchunks, total,
                      ss.carry, ss.ticket, ss.ticket_base, ss.epoch);
   int st = check_launch("affine_scan_kernel");
@@ -430,6 +486,12 @@ int affine_scan_f32(const float* a, const float* bx, const float* h0, float* h, 
                     int64_t L, bool vec) {
   return launch_affine<float, false>(AffIO<float>{a, bx, nullptr, nullptr, h0, h, nullptr}, R, L,
                                      vec);
+}
+
+int affine_scan_f32_noalloc(const float* a, const float* bx, const float* h0, float* h,
+                            int64_t R, int64_t L, bool vec) {
+  return launch_affine<float, false>(AffIO<float>{a, bx, nullptr, nullptr, h0, h, nullptr}, R, L,
+                                     vec, true);
 }
 
 int affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,

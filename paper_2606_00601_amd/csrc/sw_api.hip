@@ -17,6 +17,8 @@ int affine_scan_f32(const float* a, const float* bx, const float* h0, float* h, 
                     int64_t L, bool vec);
 int affine_scan_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
                     int64_t R, int64_t L, bool vec);
+int affine_scan_f32_noalloc(const float* a, const float* bx, const float* h0, float* h,
+                            int64_t R, int64_t L, bool vec);
 int affine_blelloch_f32(const float* a, const float* bx, const float* h0, float* h, int64_t R,
                         int64_t L, bool vec);
 int affine_blelloch_u32(const uint32_t* a, const uint32_t* bx, const uint32_t* h0, uint32_t* h,
@@ -505,6 +507,11 @@ SW_API int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t
                                      reinterpret_cast<const uint32_t*>(h0),
                                      reinterpret_cast<uint32_t*>(h_out), B, D, L,
                                      sw::affine_scan_u32);
+}
+
+SW_API int sw_affine_scan_noalloc(const float* a, const float* bx, const float* h0,
+                                  float* h_out, int64_t B, int64_t D, int64_t L) {
+  return sw::affine_common<float>(a, bx, h0, h_out, B, D, L, sw::affine_scan_f32_noalloc);
 }
 
 SW_API int sw_affine_scan_schedule(const float* a, const float* bx, const float* h0,

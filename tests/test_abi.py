@@ -54,6 +54,7 @@ def test_validation_without_gpu(lib):
     assert lib.sw_affine_scan(None, None, None, None, -1, 2, 3) == 1
     assert "negative" in lib.sw_last_error().decode()
     assert lib.sw_affine_scan_i32(None, None, None, None, 1, -2, 3) == 1
+    assert lib.sw_affine_scan_noalloc(None, None, None, None, 1, 2, -3) == 1
     assert lib.sw_selective_scan_fwd(*([None] * 8), 1, 1, -1, 4) == 1
     # N outside [1, 64]: unsupported
     assert lib.sw_selective_scan_fwd(*([None] * 8), 1, 1, 65, 4) == 2
