@@ -3,7 +3,9 @@
 Thin Python binding over libscanweaver.so (C ABI in include/scanweaver.h).
 Each function only checks and marshals its torch tensors (device, dtype,
 contiguity), hands the current HIP stream to the library and raises on a
-non-OK status; every step of the computation runs in the HIP kernels.
+non-OK status; every step of the computation runs in the HIP kernels.  The
+calls go through a small CPython extension (csrc/swcall.c) that mirrors the
+C ABI one function per entry point; ``lib()`` is the same ABI through ctypes.
 
 * ``affine_scan(a, bx, h0=None)``: h_t = a_t h_{t-1} + bx_t over the last
   axis of (B, D, L) fp32 tensors (ScanWeaver Sec. 3.1, Eq. (3)).
@@ -31,7 +33,7 @@ from __future__ import annotations
 import torch
 
 from ._lib import (SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32,  # noqa: F401
-                   ScanWeaverError, check, last_error, lib, status_string)
+                   ScanWeaverError, check, fast, last_error, lib, status_string)
 
 __all__ = ["last_launch", "affine_scan", "affine_scan_noalloc", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
            "affine_scan_proj", "affine_scan_proj_i32",
@@ -60,15 +62,24 @@ def _need(t, name, dtype, shape=None):
         raise TypeError(f"{name} must be a torch.Tensor")
     if not t.is_cuda:
         raise ValueError(f"{name} must be on a GPU (got {t.device})")
-    if t.dtype != dtype:
+    if t.dtype is not dtype:  # dtypes are singletons
         raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
-    if shape is not None and t.shape != tuple(shape):
+    if shape is not None and t.shape != shape:  # torch.Size compares as a tuple
         raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
 
 
 _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_get_device = getattr(torch._C, "_cuda_getDevice", None)
+
+
+def _current_device():
+    # the binding only runs once a GPU tensor exists, so torch's GPU state is
+    # initialised and its raw query is enough
+    if _get_device is not None:
+        return _get_device()
+    return torch.cuda.current_device()
 
 
 def _stream_handle(idx):
@@ -86,15 +97,16 @@ class _on:
     __slots__ = ("idx", "prev")
 
     def __init__(self, device):
-        self.idx = device.index if device.index is not None else torch.cuda.current_device()
+        idx = device.index
+        self.idx = idx if idx is not None else _current_device()
         self.prev = -1
 
     def __enter__(self):
-        cur = torch.cuda.current_device()
+        cur = _current_device()
         if cur != self.idx:
             torch.cuda.set_device(self.idx)
             self.prev = cur
-        lib().sw_set_stream(_stream_handle(self.idx))
+        fast().sw_set_stream(_stream_handle(self.idx))
         return self
 
     def __exit__(self, *exc):
@@ -122,7 +134,7 @@ def _affine(fn, where, dtype, a, bx, h0, out):
 
 def affine_scan(a, bx, h0=None, out=None):
     """Inclusive states of h_t = a_t h_{t-1} + bx_t (fp32, shape (B, D, L))."""
-    return _affine(lib().sw_affine_scan, "sw_affine_scan", torch.float32, a, bx, h0, out)
+    return _affine(fast().sw_affine_scan, "sw_affine_scan", torch.float32, a, bx, h0, out)
 
 
 def affine_scan_noalloc(a, bx, h0=None, out=None):
@@ -130,13 +142,13 @@ def affine_scan_noalloc(a, bx, h0=None, out=None):
     memory (its look-back scratch is a fixed array in the library; calls with
     more than ``SW_NOALLOC_MAX_CHUNKS`` look-back chunks are refused).  With
     ``out`` given, the call itself allocates nothing."""
-    return _affine(lib().sw_affine_scan_noalloc, "sw_affine_scan_noalloc", torch.float32, a, bx,
+    return _affine(fast().sw_affine_scan_noalloc, "sw_affine_scan_noalloc", torch.float32, a, bx,
                    h0, out)
 
 
 def affine_scan_i32(a, bx, h0=None, out=None):
     """The recurrence in Z/2^32 on int32 tensors (bit-exact for any schedule)."""
-    return _affine(lib().sw_affine_scan_i32, "sw_affine_scan_i32", torch.int32, a, bx, h0, out)
+    return _affine(fast().sw_affine_scan_i32, "sw_affine_scan_i32", torch.int32, a, bx, h0, out)
 
 
 _SCHEDULES = {"default": 0, "blelloch": 1}
@@ -146,14 +158,14 @@ def affine_scan_schedule(a, bx, h0=None, out=None, *, schedule="default"):
     """:func:`affine_scan` with an explicit scan schedule ("default" or
     "blelloch", the paper's upsweep / downsweep tree)."""
     sched = _SCHEDULES[schedule]
-    fn = lambda *args: lib().sw_affine_scan_schedule(*args, sched)  # noqa: E731
+    fn = lambda *args: fast().sw_affine_scan_schedule(*args, sched)  # noqa: E731
     return _affine(fn, "sw_affine_scan_schedule", torch.float32, a, bx, h0, out)
 
 
 def affine_scan_schedule_i32(a, bx, h0=None, out=None, *, schedule="default"):
     """:func:`affine_scan_i32` with an explicit scan schedule."""
     sched = _SCHEDULES[schedule]
-    fn = lambda *args: lib().sw_affine_scan_schedule_i32(*args, sched)  # noqa: E731
+    fn = lambda *args: fast().sw_affine_scan_schedule_i32(*args, sched)  # noqa: E731
     return _affine(fn, "sw_affine_scan_schedule_i32", torch.int32, a, bx, h0, out)
 
 
@@ -182,13 +194,13 @@ def _affine_proj(fn, where, dtype, a, b, x, c, h0, y, want_h_last):
 def affine_scan_proj(a, b, x=None, c=None, h0=None, *, y=None, want_h_last=True):
     """Eq. (3)-(4) elementwise: h_t = a_t h_{t-1} + b_t x_t, y_t = c_t h_t (fp32,
     shape (B, D, L); x, c None mean ones).  Returns ``(y, h_last)``."""
-    return _affine_proj(lib().sw_affine_scan_proj, "sw_affine_scan_proj", torch.float32, a, b,
+    return _affine_proj(fast().sw_affine_scan_proj, "sw_affine_scan_proj", torch.float32, a, b,
                         x, c, h0, y, want_h_last)
 
 
 def affine_scan_proj_i32(a, b, x=None, c=None, h0=None, *, y=None, want_h_last=True):
     """The projection form in Z/2^32 on int32 tensors (bit-exact)."""
-    return _affine_proj(lib().sw_affine_scan_proj_i32, "sw_affine_scan_proj_i32", torch.int32,
+    return _affine_proj(fast().sw_affine_scan_proj_i32, "sw_affine_scan_proj_i32", torch.int32,
                         a, b, x, c, h0, y, want_h_last)
 
 
@@ -253,20 +265,20 @@ def selective_scan_fwd(x, delta, A, Bm, Cm, Dskip=None, *, y=None, h_last=None,
         _need(s_pre, "s_pre", torch.float32, (B, D, L))
     with _on(x.device):
         if ckpt is not None:
-            check(lib().sw_selective_scan_fwd_train(
+            check(fast().sw_selective_scan_fwd_train(
                 _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
                 _ptr(delta_bias), _ptr(h0), _ptr(y), _ptr(h_last), _ptr(ckpt), _ptr(s_pre),
                 B, D, N, L, in_dt, out_dt, flags), "sw_selective_scan_fwd_train")
         elif z is None and delta_bias is None and h0 is None and not flags \
                 and out_dt == SW_DTYPE_F32:
-            fn = lib().sw_selective_scan_fwd if dt == torch.float32 \
-                else lib().sw_selective_scan_fwd_bf16
+            fn = fast().sw_selective_scan_fwd if dt == torch.float32 \
+                else fast().sw_selective_scan_fwd_bf16
             where = "sw_selective_scan_fwd" if dt == torch.float32 \
                 else "sw_selective_scan_fwd_bf16"
             check(fn(_ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(y),
                      _ptr(h_last), B, D, N, L), where)
         else:
-            check(lib().sw_selective_scan_fwd_ex(
+            check(fast().sw_selective_scan_fwd_ex(
                 _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
                 _ptr(delta_bias), _ptr(h0), _ptr(y), _ptr(h_last), B, D, N, L, in_dt, out_dt,
                 flags), "sw_selective_scan_fwd_ex")
@@ -297,7 +309,7 @@ def selective_scan_fwd_schedule(x, delta, A, Bm, Cm, Dskip=None, *, schedule="de
     h_last = torch.empty((B, D, N), dtype=torch.float32, device=x.device) if want_h_last else None
     in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
     with _on(x.device):
-        check(lib().sw_selective_scan_fwd_schedule(
+        check(fast().sw_selective_scan_fwd_schedule(
             _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(y),
             _ptr(h_last), B, D, N, L, in_dt, _SCHEDULES[schedule]),
             "sw_selective_scan_fwd_schedule")
@@ -365,7 +377,7 @@ def selective_scan_bwd(x, delta, A, Bm, Cm, Dskip, dy, dh_last=None, *, z=None, 
     in_dt = SW_DTYPE_F32 if dt == torch.float32 else SW_DTYPE_BF16
     dy_dt = SW_DTYPE_F32 if dy.dtype == torch.float32 else SW_DTYPE_BF16
     with _on(dev):
-        check(lib().sw_selective_scan_bwd(
+        check(fast().sw_selective_scan_bwd(
             _ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(Dskip), _ptr(z),
             _ptr(delta_bias), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(ckpt), _ptr(s_pre),
             _ptr(out["dx"]),

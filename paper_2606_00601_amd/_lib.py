@@ -77,6 +77,28 @@ def lib() -> ctypes.CDLL:
         return _lib
 
 
+_fast = None
+
+
+def fast():
+    """The extension module the binding calls the library through: one
+    function per entry point with the same name and arguments as ``lib()``'s
+    (addresses as ints or None), at a fraction of ctypes' per-call cost.
+    It links the same libscanweaver.so, so the per-thread stream and error
+    message are shared with ``lib()``.  Raises if it has not been built."""
+    global _fast
+    if _fast is not None:
+        return _fast
+    lib()
+    try:
+        from . import _swcall
+    except ImportError as e:
+        raise RuntimeError(f"the call extension is missing ({e}): build it with "
+                           "`python -m paper_2606_00601_amd.build`") from e
+    _fast = _swcall
+    return _fast
+
+
 def status_string(status: int) -> str:
     return lib().sw_status_string(int(status)).decode()
 

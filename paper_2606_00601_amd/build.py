@@ -64,7 +64,29 @@ def build(verbose: bool = False, jobs: int = 0) -> str:
         tmp = LIB + ".tmp%d" % os.getpid()
         _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
     os.replace(tmp, LIB)
+    build_swcall(verbose)
     return LIB
+
+
+def swcall_path() -> str:
+    import sysconfig
+    return os.path.join(PKG, "_swcall" + sysconfig.get_config_var("EXT_SUFFIX"))
+
+
+def build_swcall(verbose: bool = False) -> str:
+    """The CPython extension the binding calls the library through
+    (csrc/swcall.c, host code only, linked against libscanweaver.so in place)."""
+    import sysconfig
+    out = swcall_path()
+    tmp = out + ".tmp%d" % os.getpid()
+    cc = os.environ.get("CC", "gcc")
+    cmd = [cc, "-std=c99", "-O2", "-Wall", "-Wextra", "-fPIC", "-shared",
+           "-I" + sysconfig.get_paths()["include"], "-I" + INCLUDE,
+           os.path.join(CSRC, "swcall.c"), "-L" + PKG, "-lscanweaver", "-Wl,-rpath,$ORIGIN",
+           "-o", tmp]
+    _run(cmd, verbose)
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -427,12 +427,9 @@ template <typename T, bool IO>
 int launch_affine(const AffIO<T>& io, int64_t R, int64_t L, bool vec, bool fixed = false) {
   hipStream_t s = current_stream();
   constexpr int64_t CH = (int64_t)AS_THREADS * AS_K;
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
-    (void)hipGetLastError();
-    cus = 256;
-  }
+  int cus = 0;
+  int st0 = device_cus(&cus);
+  if (st0 != SW_OK) return st0;
   if (L > CH && R >= 8 * (int64_t)cus) {
     // enough rows to fill the machine: one workgroup per row, carries stay on chip
     const int64_t grid = R < ((int64_t)1 << 30) ? R : ((int64_t)1 << 30);

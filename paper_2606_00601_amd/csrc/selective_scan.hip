@@ -561,12 +561,9 @@ int env_int(const char* name, int dflt) {
 
 // Persistent grid size and chunking for a launch.
 int make_plan(int64_t B, int64_t D, int64_t L, Plan* p) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
   int cus = 0;
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e != hipSuccess || cus <= 0)
-    return fail(SW_ERR_HIP, "device query failed: %s", hipGetErrorString(e));
+  int st = device_cus(&cus);
+  if (st != SW_OK) return st;
   // Resident wavefronts per CU and tasks per wavefront (tuning knobs, read
   // per call).  One task per wavefront measured best at Mamba shapes: extra
   // chunks only add waits on the previous chunk's carry.

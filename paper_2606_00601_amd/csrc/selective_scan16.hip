@@ -57,7 +57,6 @@
 // a small part of each segment, and the first runs every segment at once.
 #include <stdlib.h>
 
-#include <atomic>
 #include <type_traits>
 
 #include "selective_common.h"
@@ -610,22 +609,8 @@ int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, bool corr_ok, int64_t
   if (env && *env) {
     want = atoll(env);
   } else {
-    // compute units per device, looked up once per device
-    static std::atomic<int> cu_cache[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) {
-      (void)hipGetLastError();
-      return 1;
-    }
-    int cus = (dev >= 0 && dev < 64) ? cu_cache[dev].load(std::memory_order_relaxed) : 0;
-    if (cus <= 0) {
-      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-          cus <= 0) {
-        (void)hipGetLastError();
-        return 1;
-      }
-      if (dev >= 0 && dev < 64) cu_cache[dev].store(cus, std::memory_order_relaxed);
-    }
+    int cus = 0;
+    if (device_cus(&cus) != SW_OK) return 1;  // whole rows need no device facts
     const int64_t waves = nwg * R16_WAVES, simds = 4 * (int64_t)cus;
     if (waves * 2 <= simds) {
       want = simds / waves;

@@ -31,7 +31,6 @@
 // 2^-26 of the state's own magnitude (checked every 64 steps, per wavefront).
 #include <stdlib.h>
 
-#include <atomic>
 
 #include "selective_common.h"
 
@@ -376,21 +375,8 @@ int64_t quad_segments(int64_t B, int64_t D, int64_t L, int64_t* Lseg) {
   const char* env = getenv("SW_SS_QUAD");
   const int force = (env && *env) ? atoi(env) : -1;
   if (force == 0) return 0;
-  static std::atomic<int> cu_cache[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) {
-    (void)hipGetLastError();
-    return 0;
-  }
-  int cus = (dev >= 0 && dev < 64) ? cu_cache[dev].load(std::memory_order_relaxed) : 0;
-  if (cus <= 0) {
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cus <= 0) {
-      (void)hipGetLastError();
-      return 0;
-    }
-    if (dev >= 0 && dev < 64) cu_cache[dev].store(cus, std::memory_order_relaxed);
-  }
+  int cus = 0;
+  if (device_cus(&cus) != SW_OK) return 0;  // the other layouts need no device facts
   const int64_t blocks = B * ((D + Q_WAVES * Q_RPW - 1) / (Q_WAVES * Q_RPW));
   int64_t want;
   const char* senv = getenv("SW_SS_SEGMENTS");

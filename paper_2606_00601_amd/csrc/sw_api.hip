@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <map>
 #include <mutex>
 #include <utility>
@@ -479,6 +480,28 @@ int workspace_alloc(void** p, size_t bytes, hipStream_t s) {
 
 void workspace_free(void* p, hipStream_t s) {
   if (p) (void)hipFreeAsync(p, s);
+}
+
+int device_cus(int* cus) {
+  static std::atomic<int> cache[64];
+  *cus = 0;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(SW_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  }
+  int n = (dev >= 0 && dev < 64) ? cache[dev].load(std::memory_order_relaxed) : 0;
+  if (n <= 0) {
+    e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess || n <= 0) {
+      (void)hipGetLastError();
+      return fail(SW_ERR_HIP, "compute unit count of device %d: %s", dev, hipGetErrorString(e));
+    }
+    if (dev >= 0 && dev < 64) cache[dev].store(n, std::memory_order_relaxed);
+  }
+  *cus = n;
+  return SW_OK;
 }
 
 int zero_words(uint32_t* p, size_t words, hipStream_t s) {

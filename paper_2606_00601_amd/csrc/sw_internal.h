@@ -23,6 +23,10 @@ int check_launch(const char* what);  // hipGetLastError -> SW_ERR_HIP with a mes
 // fused forward enqueued.
 void note_launch(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 
+// Compute units of the current device (looked up once per device), written
+// to *cus; returns SW_OK or SW_ERR_HIP with the message set.
+int device_cus(int* cus);
+
 // Zero `words` 32-bit words with a plain kernel (no memset node).
 int zero_words(uint32_t* p, size_t words, hipStream_t s);
 

@@ -44,6 +44,45 @@ def test_library_exports_nothing_else():
     assert syms == set(_declared())
 
 
+def test_call_extension_mirrors_the_header():
+    import paper_2606_00601_amd as pkg
+    f = pkg.fast()
+    for n in _declared():
+        assert callable(getattr(f, n)), n
+    from paper_2606_00601_amd import build
+    assert os.path.exists(build.swcall_path())
+
+
+def test_call_extension_answers_like_ctypes(lib):
+    import paper_2606_00601_amd as pkg
+    f = pkg.fast()
+    cases = [("sw_affine_scan", (None, None, None, None, -1, 2, 3)),
+             ("sw_affine_scan_noalloc", (None, None, None, None, 1, 2, -3)),
+             ("sw_selective_scan_fwd", (*([None] * 8), 1, 1, 65, 4)),
+             ("sw_selective_scan_fwd_ex", (*([None] * 11), 1, 1, 16, 4, 7, 0, 0)),
+             ("sw_selective_scan_bwd", (*([None] * 22), 1, 1, 16, 4, 0, 0, 8)),
+             ("sw_affine_scan_schedule", (None, None, None, None, 1, 1, 1, 9))]
+    for name, args in cases:
+        want = getattr(lib, name)(*args)
+        want_msg = lib.sw_last_error()
+        got = getattr(f, name)(*args)
+        assert got == want and got != 0, name
+        assert f.sw_last_error() == want_msg, name
+    assert f.sw_version() == lib.sw_version()
+    assert f.sw_status_string(2) == lib.sw_status_string(2)
+    # one library underneath: the stream set through one view is the other's
+    f.sw_set_stream(0x1234)
+    assert lib.sw_get_stream() == 0x1234 and f.sw_get_stream() == 0x1234
+    lib.sw_set_stream(None)
+    assert f.sw_get_stream() is None
+    with pytest.raises(TypeError):
+        f.sw_affine_scan(None, None, None, None, 1, 1)  # one argument short
+    with pytest.raises(TypeError):
+        f.sw_affine_scan(1.5, None, None, None, 1, 1, 1)  # not an address
+    with pytest.raises(OverflowError):
+        f.sw_affine_scan_schedule(None, None, None, None, 1, 1, 1, 2 ** 40)
+
+
 def test_binding_signatures_match_header():
     from paper_2606_00601_amd._lib import SIGNATURES
     assert set(SIGNATURES) == set(_declared())
