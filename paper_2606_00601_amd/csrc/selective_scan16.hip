@@ -77,6 +77,13 @@ constexpr int R16_PRS = R16_N * R16_TS + 32;  // partials: row stride (rows 32 b
 constexpr int R16_LA = 2;                   // read-ahead, in 4-step blocks
 constexpr int R16_NS = 4;                   // rotating operand sets
 constexpr float R16_LOG2E = 1.4426950408889634f;
+// A byte offset past the end of every buffer resource of the kernel (their
+// sizes stay below 2^31 - 16): a load there returns zeros and moves no
+// memory.  The super-tile of delta and x run ahead of the walk takes it for
+// steps past the segment, so that no row reads the start of the next one
+// (6% of those bytes at L = 2048 in bf16).  The tiles of B, C and of x for
+// the D skip run ahead too, but only a tile, and mostly hit L2.
+constexpr int32_t R16_OOB = 0x7FFFFFF0;
 static_assert(R16_NB == 8 && R16_NB % R16_NS == 0 && R16_LA < R16_NS,
               "operand sets must rotate over a tile");
 
@@ -146,7 +153,8 @@ __device__ __forceinline__ float* seg_words(void* yv, bool ybf, int64_t row, int
 // (B*D, nT8, 16), for the backward pass.
 // SEG: R16_WHOLE walks whole rows; R16_SEG_ENDS and R16_SEG_FWD are launches
 // (1) and (3) of the segmented form, whose workgroups are (row block,
-// segment) pairs, blockIdx.x = row block * segments of the launch + segment;
+// segment) pairs, logical workgroup = row block * segments of the launch +
+// segment (the logical order is spread over the XCDs in contiguous ranges);
 // a row has nseg segments of Lseg steps, the last one taking the rest.
 template <typename IN, bool OPT, bool CK, int SEG>
 __global__ __launch_bounds__(256) void selective_row16_kernel(
@@ -175,10 +183,12 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   // segment of this workgroup (launch (1) of the records form covers
   // segments 0 .. nseg-2, launch (3) of the correction form 1 .. nseg-1)
   const int64_t nsl = (ENDS || CORR) ? nseg - 1 : nseg;
-  const int64_t sg = SEG != R16_WHOLE ? (int64_t)blockIdx.x % nsl + (CORR ? 1 : 0) : 0;
-  const int64_t rblk = SEG != R16_WHOLE ? (int64_t)blockIdx.x / nsl : (int64_t)blockIdx.x;
+  const int64_t bid = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int64_t sg = SEG != R16_WHOLE ? bid % nsl + (CORR ? 1 : 0) : 0;
+  const int64_t rblk = SEG != R16_WHOLE ? bid / nsl : bid;
   const int64_t ts = SEG != R16_WHOLE ? sg * Lseg : 0;  // first step of the segment
   const int64_t Ls = SEG != R16_WHOLE ? (sg == nseg - 1 ? L - ts : Lseg) : L;  // its steps
+  const int32_t Ls32 = (int32_t)Ls;  // below 2^31 / 16 (row16_fits)
   const int64_t b = rblk / ndb;
   const int64_t d0 = (rblk - b * ndb) * R16_ROWS;
   const int64_t d = d0 + R16_RPW * w + r;
@@ -241,7 +251,9 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   RawVec<IN, V> dlr, xr;  // raw bits of the next super-tile
   float dl[V], dx[V];     // delta and delta*x of the current one
   auto fetch_dx = [&](int64_t sup) {
-    const int32_t off = lrow + (int32_t)((sup * ST + V * n) * ES);
+    // Ls is a multiple of V: a lane's V steps are all in or all out
+    const int32_t t = (int32_t)(sup * ST) + V * n;
+    const int32_t off = t < Ls32 ? lrow + t * ES : R16_OOB;
     dlr.load_buf(rd, off);
     xr.load_buf(rx, off);
   };

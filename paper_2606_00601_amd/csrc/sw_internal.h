@@ -221,6 +221,20 @@ __device__ __forceinline__ void wave_shift_exclusive(T& A, T& U) {
   U = dpp_or<DPP_WAVE_SHR1, 0xf>(U, Ring<T>::zero());
 }
 
+// ------------------------------------------------------- workgroup order
+// The dispatcher deals a launch's workgroups to the 8 XCDs in turn
+// (workgroup i to XCD i % 8), and each XCD has its own L2.  This renumbers
+// the first 8 * floor(n / 8) workgroups so that XCD x takes the contiguous
+// range [x * n/8, (x + 1) * n/8) of logical workgroups: neighbours in the
+// logical order (the row blocks of one batch, which read the same B and C;
+// the row blocks of one segment) then share an L2.  A bijection on [0, n);
+// the tail keeps its place.
+__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t i, uint32_t n) {
+  const uint32_t per = n / 8;
+  if (i >= 8 * per) return i;
+  return (i % 8) * per + i / 8;
+}
+
 // ------------------------------------------------------------- carry words
 // A carry word is 64 bits: status in the high half, a 32-bit payload in the
 // low half, written and read with single relaxed device-scope atomics, so a
