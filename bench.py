@@ -63,6 +63,7 @@ def algorithmic_bytes(w) -> int:
 FWD_SOURCES = ("selective_common.h", "selective_scan.hip", "selective_scan16.hip",
                "selective_scan_quad.hip", "sw_internal.h")
 AFFINE_SOURCES = ("affine_scan.hip", "sw_internal.h")
+BWD_SOURCES = ("selective_bwd.hip", "selective_common.h", "sw_internal.h")
 
 # workload -> committed HBM traffic record (rocprofv3 FETCH_SIZE / WRITE_SIZE)
 TRAFFIC_RECORDS = {
@@ -73,6 +74,10 @@ TRAFFIC_RECORDS = {
     "affine_f32_b1_d5120_l65536": "affine_rows_f32_b1_d5120_l65536_traffic.txt",
     "affine_f32_b8_d1536_l2048": "affine_scan_f32_b8_d1536_l2048_traffic.txt",
 }
+# the backward given the forward's checkpoints (no Mamba-block options)
+BWD_TRAFFIC_RECORDS = {
+    "selective_bf16_b8_d1536_n16_l2048": "selective_bwd_bf16_b8_d1536_n16_l2048_ckpt_traffic.txt",
+}
 
 
 def kernel_source_sha256(path: str = "selective") -> str:
@@ -80,7 +85,7 @@ def kernel_source_sha256(path: str = "selective") -> str:
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_00601_amd", "csrc")
-    names = AFFINE_SOURCES if path == "affine" else FWD_SOURCES
+    names = {"affine": AFFINE_SOURCES, "bwd": BWD_SOURCES}.get(path, FWD_SOURCES)
     for p in sorted(os.path.join(csrc, f) for f in names):
         h.update(os.path.basename(p).encode())
         with open(p, "rb") as f:
@@ -88,17 +93,17 @@ def kernel_source_sha256(path: str = "selective") -> str:
     return h.hexdigest()
 
 
-def measured_traffic(w, launch=None):
+def measured_traffic(w, launch=None, bwd=False):
     """HBM bytes per call from the committed counter summary, if it was taken on
     the current kernel sources, this workload and (for the fused forward) the
-    same launches; else None."""
-    name = TRAFFIC_RECORDS.get(w.name)
+    same launches; else None.  bwd: the backward's record."""
+    name = (BWD_TRAFFIC_RECORDS if bwd else TRAFFIC_RECORDS).get(w.name)
     if name is None:
         return None
     path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
-    sha = kernel_source_sha256(w.path)
+    sha = kernel_source_sha256("bwd" if bwd else w.path)
     rec = {}
     with open(path) as f:
         for line in f:
@@ -519,7 +524,9 @@ def bench_bwd(w, args):
                                else "none"),
                    "forward_checkpoints": bool(args.ckpt), "warmup": warmup_record(args)},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "frac": gbs / HBM_PEAK_GBS,
+                     "traffic": (measured_traffic(w, bwd=True)
+                                 if args.ckpt and not args.options else None),
                      "kernel": "selective_bwd_kernel + selective_bwd_reduce_kernel",
                      "per_launch_us": launch_stats(kern, per, args.graph),
                      "algorithmic_bytes": abytes},
@@ -580,7 +587,7 @@ def main(argv=None):
         return 2
 
     if args.print_kernel_sha:
-        print(kernel_source_sha256(wl.workload(args.workload).path))
+        print(kernel_source_sha256("bwd" if args.which == "bwd" else wl.workload(args.workload).path))
         return 0
 
     import torch

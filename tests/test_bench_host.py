@@ -57,9 +57,27 @@ def test_traffic_records_match_their_sources_and_workloads():
         alg = 12 * w.elems if w.path == "affine" else bench.algorithmic_bytes(w)
         # every algorithmic byte moves at least once, and not many twice
         assert t is not None and alg <= t <= 1.2 * alg, (rec, t, alg)
+    for name, rec in bench.BWD_TRAFFIC_RECORDS.items():
+        w = wl.workload(name)
+        path = os.path.join(ROOT, "profiles", rec)
+        assert os.path.exists(path), rec
+        text = open(path).read()
+        t = bench.measured_traffic(w, bwd=True)
+        if f"kernel_source_sha256: {bench.kernel_source_sha256('bwd')}" not in text:
+            assert t is None, rec
+            continue
+        # every gradient and input moves at least once; on top, the tile
+        # checkpoints (B*D*L/8*16 fp32) are read and the per-workgroup shares of
+        # dB and dC (B * D/16 * L * 16 fp32 each) written and read back
+        es = 2 if w.dtype == "bf16" else 4
+        alg = (3 * es + 8) * w.B * w.D * w.L + (2 * es + 8) * w.B * w.L * w.N
+        extra = 4 * w.B * w.D * w.L * 2 + 2 * 2 * 4 * w.B * (w.D // 16) * w.L * 16
+        assert t is not None and alg <= t <= 1.2 * (alg + extra), (rec, t, alg, extra)
     # no record for a workload without one, and the hashes differ by path
     assert bench.measured_traffic(wl.workload("selective_f32_b2_d256_n16_l512")) is None
+    assert bench.measured_traffic(wl.workload("selective_f32_b2_d256_n16_l512"), bwd=True) is None
     assert bench.kernel_source_sha256("affine") != bench.kernel_source_sha256("selective")
+    assert bench.kernel_source_sha256("bwd") != bench.kernel_source_sha256("selective")
 
 
 def test_launch_stats_fields():
