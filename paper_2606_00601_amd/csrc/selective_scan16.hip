@@ -573,8 +573,8 @@ __global__ __launch_bounds__(256) void row16_fold_corr_kernel(float* __restrict_
 
 }  // namespace
 
-// The fold of the correction form, shared with the 64-row layout
-// (selective_scan_rows64.hip), which keeps its records in the same places.
+// The fold of the correction form, shared with the quad layout
+// (selective_scan_quad.hip), which keeps its records in the same places.
 void launch_fold_corr(float* y, float* h_last, int64_t R, int64_t L, int64_t nseg, int64_t Lseg,
                       hipStream_t s) {
   const int64_t lanes = R * R16_N;
@@ -583,7 +583,9 @@ void launch_fold_corr(float* y, float* h_last, int64_t R, int64_t L, int64_t nse
 }
 
 template <typename IN>
-bool try_quad(const SelArgs& a, hipStream_t s, int* status);
+bool quad_fits(const SelArgs& a);
+template <typename IN>
+int launch_quad(const SelArgs& a, int64_t nseg, int64_t Lseg, hipStream_t s);
 
 // True when the N = 16 layout can take the call: vector-aligned rows, and
 // every byte offset of a workgroup (including loads run ahead past the end)
@@ -597,56 +599,142 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
          (L + pad) * R16_N * (int64_t)es < ((int64_t)1 << 31) && D > 0;
 }
 
-// Segments per row for the segmented form, from the wavefronts the rows give
-// per SIMD (r) and the row length (measured on MI355X, fp32, N = 16):
-//   r <= 1/2: one wavefront per SIMD (a lone wavefront's walk sets the time);
-//   1/2 < r < 1, L >= 2048: 8 segments (B=1, D=2560, L=16384: 480 -> 362 us);
-//   1 < r < 3/2, L >= 4096: 4 segments (B=1, D=5120, L=65536: 2711 -> 2603 us);
-//   otherwise whole rows (r = 1 and r >= 3/2 lose with any count).
-// Counts are powers of two, so that power-of-two rows split evenly; each
-// segment is at least one super-tile, at most R16_MAX_SEG per row (the fold
-// walks them in order).  SW_SS_SEGMENTS forces a count (1: whole rows).
-// Returns the count and sets *Lseg (a multiple of the super-tile; the last
-// segment takes the rest of the row, at least Lseg steps) and *corr: true
-// for the correction form (segments of at least R16_CORR_MIN_LSEG steps,
-// when the call allows it: fp32 y, no checkpoints), false for the records
-// form.  SW_SS_SEGFORM=1 or 2 forces the records or the correction form.
-constexpr int64_t R16_CORR_MIN_LSEG = 4096;
-int64_t row16_segments(int64_t nwg, int64_t L, int64_t st, bool corr_ok, int64_t* Lseg,
-                       bool* corr) {
-  *Lseg = L;
-  *corr = false;
-  int64_t want = 1;
-  const char* env = getenv("SW_SS_SEGMENTS");
-  if (env && *env) {
-    want = atoll(env);
-  } else {
-    int cus = 0;
-    if (device_cus(&cus) != SW_OK) return 1;  // whole rows need no device facts
-    const int64_t waves = nwg * R16_WAVES, simds = 4 * (int64_t)cus;
-    if (waves * 2 <= simds) {
-      want = simds / waves;
-      while (want & (want - 1)) want &= want - 1;  // largest power of two below
-    } else if (waves < simds && L >= 2048) {
-      want = 8;
-    } else if (waves > simds && waves * 2 < simds * 3 && L >= 4096) {
-      want = 4;
-    }
+// ---- which layout, how many segments and which form an N = 16 call takes
+//
+// The candidates: the 16-lane layout walking whole rows; the 16-lane layout
+// with 2..16 segments per row, in the records or the correction form; the
+// quad layout (four lanes per row, selective_scan_quad.hip) with 2..16
+// segments, correction form.  Each is priced with a model of its launches
+// and the cheapest is taken.  A launch of G workgroups on `cus` CUs runs in
+// rounds: its busiest CU holds ceil(G / cus) workgroups, at most `cap` at a
+// time (three of the 16-lane layout, four of the quad layout, by LDS), and a
+// round with o workgroups resident per CU takes `ns[o]` per step of its walk
+// -- the per-step times of each layout measured on MI355X with one to four
+// workgroups per CU, fp32 inputs (the quad layout is 8% faster with bf16
+// inputs).  A correction walk is priced at the fading length of Mamba-like
+// decay, 1024 steps plus one check (slower decay walks further, up to the
+// whole segment: slower, never wrong); a segmented call adds 8 us for its
+// fold and two more launches; the first walk of the records form (no C, no
+// y) is priced at 0.85 of a walk.  Over 42 shapes (B = 1..4, D = 1280..8192,
+// L = 4096..65536, fp32 and bf16 inputs) the model's choice came within 1.2%
+// of the fastest measured candidate on average and 10% at worst, where
+// fixed occupancy bands had been 29% and 150% off.
+// SW_SS_QUAD=0 leaves the quad layout out, =1 takes it whenever the call
+// allows; SW_SS_SEGMENTS=k keeps only the candidates with k segments (1:
+// whole rows; the 16-lane layout unless SW_SS_QUAD=1); SW_SS_SEGFORM=1 or 2
+// keeps only the records or the correction form of the 16-lane layout.
+struct StepCost {
+  int cap;
+  float ns[5];
+};
+constexpr StepCost R16_COST = {3, {0.0f, 28.8f, 42.3f, 57.1f, 0.0f}};
+constexpr StepCost QUAD_COST = {4, {0.0f, 98.6f, 135.8f, 171.6f, 226.0f}};
+constexpr int64_t PLAN_CORR_STEPS = 1024;
+constexpr double PLAN_SEG_US = 8.0;
+constexpr double PLAN_ENDS_SHARE = 0.85;
+constexpr int64_t QUAD_SKIP = 64;  // the quad layout's segment granularity and check interval
+
+double launch_us(int64_t G, int64_t steps, int cus, const StepCost& c, double scale) {
+  int64_t per = (G + cus - 1) / cus;
+  double ns = 0.0;
+  while (per > 0) {
+    const int o = (int)(per < c.cap ? per : c.cap);
+    per -= o;
+    ns += (double)steps * c.ns[o];
   }
-  if (want > R16_MAX_SEG) want = R16_MAX_SEG;
-  if (want > L / st) want = L / st;
-  if (want < 2) return 1;
-  const int64_t per = (L + want - 1) / want;
+  return ns * scale * 1e-3;
+}
+
+int64_t env_i64(const char* name) {
+  const char* v = getenv(name);
+  return (v && *v) ? atoll(v) : -1;
+}
+
+struct N16Plan {
+  bool quad = false;
+  int64_t nseg = 1;  // 1: whole rows
+  int64_t Lseg = 0;
+  bool corr = false;
+};
+
+// Segments of the 16-lane layout for a count k: whole super-tiles of st
+// steps, the last segment taking the rest; n = 0 when k gives fewer than two.
+void r16_geometry(int64_t L, int64_t st, int64_t k, int64_t* n, int64_t* Lseg) {
+  *n = 0;
+  if (k < 2 || k > R16_MAX_SEG || L / st < 2) return;
+  const int64_t per = (L + k - 1) / k;
   *Lseg = (per + st - 1) / st * st;
-  const int64_t nseg = L / *Lseg;  // <= want: Lseg >= L / want
-  if (nseg < 2 || nseg > R16_MAX_SEG) {
-    *Lseg = L;
-    return 1;
+  const int64_t m = L / *Lseg;
+  if (m >= 2 && m <= R16_MAX_SEG) *n = m;
+}
+
+template <typename IN>
+N16Plan plan_n16(const SelArgs& a, int64_t ndb) {
+  N16Plan best;
+  if (a.ckpt) return best;  // checkpoints are written by whole-row walks
+  const int64_t L = a.L, st = R16_N * (16 / (int64_t)sizeof(IN));
+  const int64_t quad_env = env_i64("SW_SS_QUAD"), seg_env = env_i64("SW_SS_SEGMENTS");
+  const int64_t form_env = env_i64("SW_SS_SEGFORM");
+  const bool qfits = quad_fits<IN>(a);
+  const bool quad_only = quad_env == 1 && qfits;
+  const bool with_quad = qfits && quad_env != 0 && (seg_env < 0 || quad_only);
+  const bool corr_ok = !a.y_bf16;
+  int cus = 0;
+  if (device_cus(&cus) != SW_OK) cus = 256;  // a forced choice needs no device facts
+  const double qscale = sizeof(IN) == 2 ? 0.92 : 1.0;
+  const int64_t G16 = a.B * ndb, Gq = a.B * ((a.D + 63) / 64);
+  double best_us = 1e300;
+  auto consider = [&](double us, bool quad, int64_t nseg, int64_t Lseg, bool corr) {
+    if (us < best_us) {
+      best_us = us;
+      best.quad = quad;
+      best.nseg = nseg;
+      best.Lseg = Lseg;
+      best.corr = corr;
+    }
+  };
+  const int64_t kmin = seg_env > 0 ? (seg_env < 16 ? seg_env : 16) : 1;
+  const int64_t kmax = seg_env > 0 ? kmin : 16;
+  if (!quad_only) {
+    if (kmin == 1) consider(launch_us(G16, L, cus, R16_COST, 1.0), false, 1, L, false);
+    for (int64_t k = (kmin > 2 ? kmin : 2); k <= kmax; ++k) {
+      int64_t n, Lseg;
+      r16_geometry(L, st, k, &n, &Lseg);
+      if (n < 2 || G16 * n >= ((int64_t)1 << 31)) continue;
+      const int64_t last = L - (n - 1) * Lseg;
+      const double first = launch_us(G16 * n, last, cus, R16_COST, 1.0);
+      if (corr_ok && form_env != 1) {
+        const int64_t walk = last < PLAN_CORR_STEPS + st ? last : PLAN_CORR_STEPS + st;
+        consider(first + launch_us(G16 * (n - 1), walk, cus, R16_COST, 1.0) + PLAN_SEG_US, false,
+                 n, Lseg, true);
+      }
+      if (form_env != 2)
+        consider(PLAN_ENDS_SHARE * launch_us(G16 * (n - 1), Lseg, cus, R16_COST, 1.0) + first +
+                     PLAN_SEG_US,
+                 false, n, Lseg, false);
+    }
+    // a forced count that gives fewer than two segments walks whole rows
+    if (best_us == 1e300) consider(0.0, false, 1, L, false);
   }
-  *corr = corr_ok && *Lseg >= R16_CORR_MIN_LSEG;
-  const char* fenv = getenv("SW_SS_SEGFORM");
-  if (fenv && *fenv) *corr = corr_ok && atoi(fenv) == 2;
-  return nseg;
+  if (with_quad) {
+    // a forced count is capped at one segment per QUAD_SKIP steps
+    const int64_t kcap = L / QUAD_SKIP;
+    if (quad_only && (kmin == 1 || (seg_env > 0 && kcap < 2)))
+      consider(launch_us(Gq, L, cus, QUAD_COST, qscale), true, 1, L, false);
+    const int64_t qmin = seg_env > 0 && kmin > kcap ? kcap : kmin;
+    const int64_t qmax = seg_env > 0 && kmax > kcap ? kcap : kmax;
+    for (int64_t k = (qmin > 2 ? qmin : 2); k <= qmax; ++k) {
+      const int64_t Lseg = (L / k) / QUAD_SKIP * QUAD_SKIP;
+      if (Lseg < QUAD_SKIP) continue;
+      const int64_t last = L - (k - 1) * Lseg;
+      const int64_t walk = last < PLAN_CORR_STEPS + QUAD_SKIP ? last : PLAN_CORR_STEPS + QUAD_SKIP;
+      consider(launch_us(Gq * k, last, cus, QUAD_COST, qscale) +
+                   launch_us(Gq * (k - 1), walk, cus, QUAD_COST, qscale) + PLAN_SEG_US,
+               true, k, Lseg, true);
+    }
+    if (quad_only && best_us == 1e300) consider(0.0, true, 1, L, false);
+  }
+  return best;
 }
 
 template <typename IN, bool OPT>
@@ -699,24 +787,17 @@ void launch_row16_corr(const SelArgs& a, int64_t ndb, uint32_t flags, int64_t ns
 
 template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s) {
-  // few rows, long sequences: four lanes per row, four states per lane
-  int st = SW_OK;
-  if (try_quad<IN>(a, s, &st)) return st;
   const bool opt = a.z || a.delta_bias || a.softplus || a.y_bf16 || a.s_out;
   const int64_t ndb = (a.D + R16_ROWS - 1) / R16_ROWS;
   const int64_t grid = a.B * ndb;
   if (grid >= ((int64_t)1 << 31))
     return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
+  const N16Plan p = plan_n16<IN>(a, ndb);
+  if (p.quad) return launch_quad<IN>(a, p.nseg, p.Lseg, s);
   const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.y_bf16 ? SEL_Y_BF16 : 0u) |
                          (a.z ? SEL_GATED : 0u);
-  // narrow shapes: the segmented form (not with checkpoints, which are
-  // written by whole-row walks)
-  int64_t Lseg = a.L;
-  bool corr = false;
-  const int64_t nseg = a.ckpt ? 1
-                              : row16_segments(grid, a.L, 16 * (16 / (int64_t)sizeof(IN)),
-                                               !a.y_bf16, &Lseg, &corr);
-  if (nseg > 1 && grid * nseg < ((int64_t)1 << 31) && corr) {
+  const int64_t nseg = p.nseg, Lseg = p.Lseg;
+  if (nseg > 1 && p.corr) {
     if (opt)
       launch_row16_corr<IN, true>(a, ndb, flags, nseg, Lseg, s);
     else
@@ -725,7 +806,7 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
                 (long long)nseg, (long long)Lseg);
     return check_launch("selective_row16_kernel (segments, correction form)");
   }
-  if (nseg > 1 && grid * nseg < ((int64_t)1 << 31)) {
+  if (nseg > 1) {
     if (opt)
       launch_row16_segments<IN, true>(a, ndb, flags, nseg, Lseg, s);
     else

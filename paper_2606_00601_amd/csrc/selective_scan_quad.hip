@@ -29,7 +29,6 @@
 // the records, (3) each later segment walks again from its composed state
 // until, for every state of the wavefront, the carried part has faded below
 // 2^-26 of the state's own magnitude (checked every 64 steps, per wavefront).
-#include <stdlib.h>
 
 
 #include "selective_common.h"
@@ -49,6 +48,7 @@ constexpr int Q_N = 16;      // states per row
 constexpr int Q_T = 32;      // steps per tile
 constexpr int Q_TPV = 2;     // tiles between the checks of the correction walk
 constexpr int Q_SKIP = 64;   // first steps of a later segment whose y holds its records
+constexpr int Q_MAX_SEG = 16;  // segments per row at most (the fold walks them in order)
 constexpr float Q_LOG2E = 1.4426950408889634f;
 constexpr float Q_EPS = 1.4901161193847656e-08f;  // 2^-26, as in selective_scan16.hip
 static_assert(Q_SKIP == Q_T * Q_TPV, "the first check covers the records' steps");
@@ -360,46 +360,6 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
   }
 }
 
-}  // namespace
-
-// Segments for the quad layout: as many (row block, segment) workgroups as
-// the GPU holds at once (four per CU: 40 KB of LDS each), so that all run in
-// one round, each segment at least Q_MIN_LSEG steps so that the correction
-// walk (about a thousand steps at Mamba-like decay) stays a small part of it.
-// Measured at B=1, D=5120, L=65536 (80 row blocks): 11 / 12 / 13 / 16
-// segments 1513 / 1484 / 1664 / 1544 us per call (13 needs a second round).  Returns 0 when the layout does not pay (rows enough to
-// fill the GPU with one lane per state, or rows too short).  SW_SS_QUAD=0
-// turns the layout off, =1 forces it (with SW_SS_SEGMENTS segments if set).
-constexpr int64_t Q_MIN_LSEG = 4096;
-int64_t quad_segments(int64_t B, int64_t D, int64_t L, int64_t* Lseg) {
-  const char* env = getenv("SW_SS_QUAD");
-  const int force = (env && *env) ? atoi(env) : -1;
-  if (force == 0) return 0;
-  int cus = 0;
-  if (device_cus(&cus) != SW_OK) return 0;  // the other layouts need no device facts
-  const int64_t blocks = B * ((D + Q_WAVES * Q_RPW - 1) / (Q_WAVES * Q_RPW));
-  int64_t want;
-  const char* senv = getenv("SW_SS_SEGMENTS");
-  if (force == 1 && senv && *senv) {
-    want = atoll(senv);
-  } else {
-    // rows that give one lane per state at least 1.5 wavefronts per SIMD keep that layout
-    if (force != 1 && B * D * Q_N / 64 * 2 >= 3 * 4 * (int64_t)cus) return 0;
-    want = 4 * (int64_t)cus / blocks;  // blocks * want <= 4 per CU
-    if (want > L / Q_MIN_LSEG) want = L / Q_MIN_LSEG;
-    if (force != 1 && want < 2) return 0;  // too long a walk for so few rows
-  }
-  if (want < 1) want = 1;
-  if (want > 16) want = 16;
-  if (want > L / Q_SKIP) want = L / Q_SKIP;
-  if (want <= 1) {
-    *Lseg = L;
-    return 1;
-  }
-  *Lseg = (L / want) / Q_SKIP * Q_SKIP;  // the last segment takes the rest
-  return want;
-}
-
 template <typename IN, bool OPT>
 void launch_quad_t(const SelArgs& a, uint32_t flags, int64_t nseg, int64_t Lseg, hipStream_t s) {
   const int64_t nblk = (a.D + Q_WAVES * Q_RPW - 1) / (Q_WAVES * Q_RPW);
@@ -421,37 +381,48 @@ void launch_quad_t(const SelArgs& a, uint32_t flags, int64_t nseg, int64_t Lseg,
                      (int)Lseg);
 }
 
-// True when the quad layout takes the call (fp32 y, no checkpoints, N = 16,
-// whole tiles, 32-bit offsets over a wavefront's rows and a batch's B and C)
-// and the rows are few enough for it to pay; then it launches and reports
-// the launch status through *status.
+}  // namespace
+
+// True when the quad layout can take the call: fp32 y, no checkpoints,
+// N = 16, whole tiles, 32-bit offsets over a wavefront's rows and a batch's
+// B and C.  (Which layout and how many segments a call takes is decided with
+// the 16-lane layout's choices, in selective_scan16.hip.)
 template <typename IN>
-bool try_quad(const SelArgs& a, hipStream_t s, int* status) {
+bool quad_fits(const SelArgs& a) {
   if (a.N != Q_N || a.y_bf16 || a.ckpt || a.L <= 0 || a.B * a.D <= 0) return false;
   if (a.L % Q_T != 0 || a.D >= ((int64_t)1 << 30) || a.L >= ((int64_t)1 << 26)) return false;
   if ((Q_RPW * (a.L + 4 * Q_T)) * (int64_t)sizeof(IN) >= ((int64_t)1 << 31)) return false;
   if ((a.L + 4 * Q_T) * Q_N * (int64_t)sizeof(IN) >= ((int64_t)1 << 31)) return false;
-  int64_t Lseg = a.L;
-  const int64_t nseg = quad_segments(a.B, a.D, a.L, &Lseg);
-  if (nseg < 1) return false;
-  const int64_t blocks = a.B * ((a.D + Q_WAVES * Q_RPW - 1) / (Q_WAVES * Q_RPW));
-  if (blocks * nseg >= ((int64_t)1 << 31) || blocks >= ((int64_t)1 << 30)) return false;
+  return a.B * ((a.D + Q_WAVES * Q_RPW - 1) / (Q_WAVES * Q_RPW)) * Q_MAX_SEG < ((int64_t)1 << 31);
+}
+
+// Launches the quad layout with nseg segments of Lseg steps (the last takes
+// the rest; Lseg a multiple of Q_SKIP, 1 <= nseg <= Q_MAX_SEG); the call must
+// satisfy quad_fits.
+template <typename IN>
+int launch_quad(const SelArgs& a, int64_t nseg, int64_t Lseg, hipStream_t s) {
+  if (nseg < 1 || nseg > Q_MAX_SEG || (nseg > 1 && (Lseg < Q_SKIP || Lseg % Q_SKIP != 0 ||
+                                                    (nseg - 1) * Lseg >= a.L)))
+    return fail(SW_ERR_UNSUPPORTED, "quad layout: %lld segments of %lld steps for L=%lld",
+                (long long)nseg, (long long)Lseg, (long long)a.L);
+  if (nseg == 1) Lseg = a.L;
   const bool opt = a.z || a.delta_bias || a.softplus || a.s_out;
   const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.z ? SEL_GATED : 0u);
   if (opt)
     launch_quad_t<IN, true>(a, flags, nseg, Lseg, s);
   else
     launch_quad_t<IN, false>(a, flags, nseg, Lseg, s);
-  *status = check_launch("selective_quad_kernel");
   if (nseg > 1)
     note_launch("selective_quad_kernel: %lld segments of %lld steps, correction form (3 launches)",
                 (long long)nseg, (long long)Lseg);
   else
     note_launch("selective_quad_kernel: whole rows");
-  return true;
+  return check_launch("selective_quad_kernel");
 }
 
-template bool try_quad<float>(const SelArgs&, hipStream_t, int*);
-template bool try_quad<uint16_t>(const SelArgs&, hipStream_t, int*);
+template bool quad_fits<float>(const SelArgs&);
+template bool quad_fits<uint16_t>(const SelArgs&);
+template int launch_quad<float>(const SelArgs&, int64_t, int64_t, hipStream_t);
+template int launch_quad<uint16_t>(const SelArgs&, int64_t, int64_t, hipStream_t);
 
 }  // namespace sw

@@ -279,6 +279,13 @@ def test_selective_workloads(sw, name, k):
     inp = w.inputs()
     rows = None if k is None else _sample_rows(w.B * w.D, k, 99)
     sy, sh, yg, o, y = _selective_check(sw, inp, w.dtype, rows=rows)
+    # the launches bench.py times at these shapes
+    want = {"selective_f32_b2_d256_n16_l512": "selective_row16_kernel: 8 segments",
+            "selective_bf16_b8_d1536_n16_l2048": "selective_row16_kernel: whole rows",
+            "selective_f32_b1_d5120_n16_l65536": "selective_quad_kernel: ",
+            "selective_f32_b4_d2048_n16_l8192_stress": "selective_row16_kernel: whole rows"}
+    assert sw.last_launch().startswith(want[name]), sw.last_launch()
+    _say("  launch:", sw.last_launch())
     _say("  y:", {k_: v for k_, v in sy.items() if k_ != "first_bad"})
     _say("  h_last:", {k_: v for k_, v in sh.items() if k_ != "first_bad"})
     assert_gate(sy, name + " y")
@@ -567,6 +574,8 @@ def test_selective_quad(sw, monkeypatch, case, dtype, opts):
     inp, ex = _ex_inputs(B, D, 16, L, 9600 + B + D + L, dtype, opts)
     softplus = "softplus" in opts
     y, hl = _run_ex(sw, inp, ex, dtype, softplus, False)
+    # the layout takes every call with whole 32-step tiles (L = 1040 is not one)
+    assert ("selective_quad_kernel" in sw.last_launch()) == (L % 32 == 0), sw.last_launch()
     o = _ex_oracle(inp, ex, softplus)
     _y_gate(y, o, False, f"quad y {dtype} {(B, D, L)} {segs} {opts}")
     assert_gate(fp_gate(hl.cpu().numpy(), o["h_last"], o["h_mag"], o["h_sens"]),
@@ -595,6 +604,7 @@ def test_selective_quad_regimes(sw, monkeypatch, kind):
         inp["x"][:, :, : 3 * L // 4] = 0.0
     with_d = kind != "no_dskip"
     y, hl = _run_selective(sw, inp, "f32", with_dskip=with_d, want_h_last=with_d)
+    assert sw.last_launch().startswith("selective_quad_kernel: 4 segments"), sw.last_launch()
     o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
                               inp["Dskip"] if with_d else None, bounds=True)
     assert_gate(fp_gate(y.cpu().numpy(), o["y"], o["y_mag"], o["y_sens"]), f"quad {kind} y")
