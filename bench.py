@@ -537,6 +537,88 @@ def bench_bwd(w, args):
     return 0
 
 
+# shapes of --layout-sweep: D from 1/3 to 2 wavefronts per SIMD at one lane per
+# state and B = 1, three lengths, and a few with B > 1
+LAYOUT_SWEEP_SHAPES = ";".join(
+    [f"1,{D},{L}" for L in (4096, 16384, 65536) for D in (1280, 2560, 4096, 5120, 6144, 8192)]
+    + ["2,2560,8192", "4,1024,16384", "2,2048,32768"])
+
+# forced choices of the N = 16 forward (environment of the library) timed by --layout-sweep
+LAYOUT_CANDIDATES = (
+    [("whole", {"SW_SS_QUAD": "0", "SW_SS_SEGMENTS": "1"})]
+    + [(f"r16c{k}", {"SW_SS_QUAD": "0", "SW_SS_SEGMENTS": str(k), "SW_SS_SEGFORM": "2"})
+       for k in (2, 4, 8, 16)]
+    + [(f"r16r{k}", {"SW_SS_QUAD": "0", "SW_SS_SEGMENTS": str(k), "SW_SS_SEGFORM": "1"})
+       for k in (4, 8)]
+    + [(f"quad{k}", {"SW_SS_QUAD": "1", "SW_SS_SEGMENTS": str(k)}) for k in (4, 8, 12, 16)])
+
+
+def layout_sweep(shapes: str) -> int:
+    """Time each forced layout / segment count / form of the fused forward and
+    the library's own choice on seeded synthetic inputs (Mamba-like: delta =
+    softplus(N(-4, 0.5^2)), A = -exp(U[0, ln 16]), x, B, C, Dskip standard
+    normal), fp32 and bf16 inputs, N = 16; one JSON line per shape."""
+    import torch
+
+    import paper_2606_00601_amd as sw
+    sw.lib()
+    dev = torch.device("cuda:0")
+    keys = ("SW_SS_QUAD", "SW_SS_SEGMENTS", "SW_SS_SEGFORM")
+    saved = {k: os.environ.get(k) for k in keys}
+    g = torch.Generator(device=dev)
+    g.manual_seed(1)
+    clock_warmup(lambda i: torch.cumsum(torch.ones(1 << 24, device=dev), 0), 250.0)
+    for dt in ("f32", "bf16"):
+        for spec in shapes.split(";"):
+            B, D, L = (int(v) for v in spec.split(","))
+            N = 16
+            x = torch.randn(B, D, L, device=dev, generator=g)
+            dl = torch.nn.functional.softplus(
+                torch.randn(B, D, L, device=dev, generator=g) * 0.5 - 4)
+            A = -torch.exp(torch.rand(D, N, device=dev, generator=g) * float(np.log(16)))
+            Bm = torch.randn(B, L, N, device=dev, generator=g)
+            Cm = torch.randn(B, L, N, device=dev, generator=g)
+            if dt == "bf16":
+                x, dl, Bm, Cm = x.bfloat16(), dl.bfloat16(), Bm.bfloat16(), Cm.bfloat16()
+            Dk = torch.randn(D, device=dev, generator=g)
+            y = torch.empty(B, D, L, device=dev)
+            h = torch.empty(B, D, N, device=dev)
+
+            def call():
+                sw.selective_scan_fwd(x, dl, A, Bm, Cm, Dk, y=y, h_last=h)
+
+            n = max(10, min(60, int(4e9 / (B * D * L))))
+            res = {}
+            for name, env in LAYOUT_CANDIDATES + [("auto", {})]:
+                for k in keys:
+                    os.environ.pop(k, None)
+                os.environ.update(env)
+                for _ in range(max(3, n // 4)):
+                    call()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                e0.record()
+                for _ in range(n):
+                    call()
+                e1.record()
+                torch.cuda.synchronize()
+                res[name] = round(1e3 * e0.elapsed_time(e1) / n, 1)
+                if name == "auto":
+                    res["auto_launch"] = sw.last_launch()
+            for k in keys:
+                os.environ.pop(k, None)
+            best = min((v, k) for k, v in res.items() if k not in ("auto", "auto_launch"))
+            print(json.dumps({"B": B, "D": D, "L": L, "N": N, "inputs": dt, "us": res,
+                              "fastest_forced": best[1],
+                              "auto_over_fastest": round(res["auto"] / best[0], 3)}),
+                  flush=True)
+    for k, v in saved.items():
+        if v is not None:
+            os.environ[k] = v
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -575,6 +657,12 @@ def main(argv=None):
                     help="replay the timed launches from one HIP graph (forward and bare "
                          "scan; removes the host's per-call enqueue cost, which bounds the "
                          "launch-sized workloads)")
+    ap.add_argument("--layout-sweep", action="store_true",
+                    help="time every layout, segment count and form of the N = 16 fused "
+                         "forward, and the library's own choice, over --sweep-shapes "
+                         "(one JSON line per shape and input dtype)")
+    ap.add_argument("--sweep-shapes", default=LAYOUT_SWEEP_SHAPES,
+                    help="B,D,L triples separated by ';' for --layout-sweep")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, 5 times "
                          "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -606,6 +694,9 @@ def main(argv=None):
     if args.measure_copy:
         print(json.dumps(measure_copy_bandwidth()), flush=True)
         return 0
+
+    if args.layout_sweep:
+        return layout_sweep(args.sweep_shapes)
 
     import paper_2606_00601_amd as sw
     w = wl.workload(args.workload)

@@ -209,30 +209,26 @@ int sw_affine_scan_proj_i32(const int32_t* a, const int32_t* b, const int32_t* x
  *   y        : (B, D, L) fp32 output   h_last : (B, D, N) fp32 output or NULL
  * 1 <= N <= 64, else SW_ERR_UNSUPPORTED.  State and accumulation are fp32.
  * With L == 0 and B*D > 0, h_last (if given) is set to zero.
- * With N = 16, calls whose rows leave SIMDs idle or unevenly loaded split
- * each row into segments composed with Eq. (7).  With w the wavefronts the
- * rows give per SIMD at one lane per state (16 rows per four wavefronts):
- *   - w < 3/2, fp32 y, L a multiple of 32 and long enough for segments of
- *     at least 4096 steps (e.g. B=1, D=5120, L=65536): four lanes per row,
- *     as many segments as fill the GPU in one round (12 there), correction
- *     form;
- *   - otherwise w <= 1/2 takes one wavefront per SIMD; 1/2 < w < 1 with
- *     L >= 2048 takes 8 segments; 1 < w < 3/2 with L >= 4096 takes 4; other
- *     calls walk whole rows.
- * Segments of at least 4096 steps with fp32 y take the correction form:
- * every segment walks from a zero state, a fold composes the carries, and
- * each later segment is walked again from its composed state only until the
- * part carried in has faded below 2^-26 of the magnitude of the state's own
- * terms (the whole segment when it does not fade).  Shorter segments take
- * the records form: each segment's carry is formed first, then every
- * segment walks once from its initial state.  Results of both agree with a
- * whole-row walk within fp32 rounding, not bit for bit.  The environment
- * variables SW_SS_QUAD (0: never four lanes per row, 1: always when
- * allowed), SW_SS_SEGMENTS (the count, 1: whole rows) and SW_SS_SEGFORM (1:
- * records, 2: correction), read per call, force the choice;
- * sw_last_launch() names what a call enqueued.  y's memory holds the
- * segments' carries between the call's kernels, so y must not be read until
- * the call completes on its stream (as for any output).
+ * With N = 16, a call whose rows leave SIMDs idle or unevenly loaded may
+ * split each row into up to 16 segments composed with Eq. (7), and may walk
+ * each row with four lanes (four states each) instead of sixteen (fp32 y,
+ * L a multiple of 32).  The library prices each choice with a model of its
+ * launches on the device (per-step times measured per layout and occupancy)
+ * and takes the cheapest; calls that write checkpoints walk whole rows.
+ * Segments take one of two forms.  Correction form (fp32 y): every segment
+ * walks from a zero state, a fold composes the carries, and each later
+ * segment is walked again from its composed state only until the part
+ * carried in has faded below 2^-26 of the magnitude of the state's own
+ * terms (the whole segment when it does not fade).  Records form: each
+ * segment's carry is formed first, then every segment walks once from its
+ * initial state.  Results of both agree with a whole-row walk within fp32
+ * rounding, not bit for bit.  The environment variables SW_SS_QUAD (0: never
+ * four lanes per row, 1: whenever the call allows), SW_SS_SEGMENTS (the
+ * count, 1: whole rows) and SW_SS_SEGFORM (1: records, 2: correction), read
+ * per call, force the choice; sw_last_launch() names what a call enqueued.
+ * y's memory holds the segments' carries between the call's kernels, so y
+ * must not be read until the call completes on its stream (as for any
+ * output).
  */
 int sw_selective_scan_fwd(const float* x, const float* delta, const float* A, const float* Bm,
                           const float* Cm, const float* Dskip, float* y, float* h_last,
