@@ -611,7 +611,9 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
 // round with o workgroups resident per CU takes `ns[o]` per step of its walk
 // -- the per-step times of each layout measured on MI355X with one to four
 // workgroups per CU, fp32 inputs (the quad layout is 8% faster with bf16
-// inputs).  A correction walk is priced at the fading length of Mamba-like
+// inputs; its four-per-CU time, 226 ns with every CU at four, is set at 220
+// ns, what B=1, D=5120, L=65536 measures with three quarters of the CUs at
+// four: on four boxes 12 segments took 1489 us on average, 9 segments 1516).  A correction walk is priced at the fading length of Mamba-like
 // decay, 1024 steps plus one check (slower decay walks further, up to the
 // whole segment: slower, never wrong); a segmented call adds 8 us for its
 // fold and two more launches; the first walk of the records form (no C, no
@@ -628,7 +630,7 @@ struct StepCost {
   float ns[5];
 };
 constexpr StepCost R16_COST = {3, {0.0f, 28.8f, 42.3f, 57.1f, 0.0f}};
-constexpr StepCost QUAD_COST = {4, {0.0f, 98.6f, 135.8f, 171.6f, 226.0f}};
+constexpr StepCost QUAD_COST = {4, {0.0f, 98.6f, 135.8f, 171.6f, 220.0f}};
 constexpr int64_t PLAN_CORR_STEPS = 1024;
 constexpr double PLAN_SEG_US = 8.0;
 constexpr double PLAN_ENDS_SHARE = 0.85;
