@@ -553,6 +553,38 @@ def test_selective_segments_correction_regimes(sw, monkeypatch, kind):
     assert rownorm_rel(y.cpu().numpy(), y1.cpu().numpy()) <= 1e-5
 
 
+# The planner's choices on a 256-CU part (section "Choosing the layout" of the
+# design notes): few rows at L = 16384 take the correction form of the 16-lane
+# layout, long rows the quad layout, rows that fill the GPU whole rows, and
+# bf16 y keeps the records form.  Each call is also checked against the
+# oracle on sampled rows.
+_PLAN_CASES = [((1, 1280, 16384), "f32", False, "selective_row16_kernel: 8 segments of 2048 steps, correction"),
+               ((1, 2560, 65536), "f32", False, "selective_quad_kernel: 16 segments"),
+               ((1, 8192, 4096), "f32", False, "selective_row16_kernel: whole rows"),
+               ((1, 1280, 4096), "f32", True, "selective_row16_kernel: 16 segments of 256 steps, records")]
+
+
+@pytest.mark.parametrize("case", _PLAN_CASES)
+def test_planner_choices(sw, case):
+    (B, D, L), dtype, y_bf16, want = case
+    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
+        pytest.skip("the expected choices are those of a 256-CU part")
+    _say("case planner", (B, D, L), dtype, "bf16 y" if y_bf16 else "")
+    inp = wl.selective_inputs(B, D, 16, L, 9800 + D, dtype)
+    x, dl = dev(inp["x"]), dev(inp["delta"])
+    Bm, Cm = dev(inp["Bm"]), dev(inp["Cm"])
+    y, hl = sw.selective_scan_fwd(x, dl, dev(inp["A"]), Bm, Cm, dev(inp["Dskip"]),
+                                  y_dtype=torch.bfloat16 if y_bf16 else torch.float32)
+    assert sw.last_launch().startswith(want), sw.last_launch()
+    rows = _sample_rows(B * D, 24, 7)
+    o = oracle.selective_scan(inp["x"], inp["delta"], inp["A"], inp["Bm"], inp["Cm"],
+                              inp["Dskip"], rows=rows, bounds=True)
+    ridx = torch.as_tensor(np.asarray(rows), device="cuda")
+    _y_gate(y.reshape(B * D, L).index_select(0, ridx), o, y_bf16, f"planner y {(B, D, L)}")
+    hg = hl.reshape(B * D, 16).index_select(0, ridx).cpu().numpy()
+    assert_gate(fp_gate(hg, o["h_last"], o["h_mag"], o["h_sens"]), f"planner h_last {(B, D, L)}")
+
+
 # The quad layout (four lanes per row, four states per lane, 16 rows per
 # wavefront) taken by few-row, long calls; forced here on small shapes
 # (SW_SS_QUAD=1) with the segment count given: D not a multiple of 64 leaves
