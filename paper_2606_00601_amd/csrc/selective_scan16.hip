@@ -637,14 +637,10 @@ constexpr double PLAN_ENDS_SHARE = 0.85;
 constexpr int64_t QUAD_SKIP = 64;  // the quad layout's segment granularity and check interval
 
 double launch_us(int64_t G, int64_t steps, int cus, const StepCost& c, double scale) {
-  int64_t per = (G + cus - 1) / cus;
-  double ns = 0.0;
-  while (per > 0) {
-    const int o = (int)(per < c.cap ? per : c.cap);
-    per -= o;
-    ns += (double)steps * c.ns[o];
-  }
-  return ns * scale * 1e-3;
+  const int64_t per = (G + cus - 1) / cus;  // workgroups on the busiest CU
+  const int64_t full = per / c.cap, rest = per % c.cap;
+  const double ns = (double)full * c.ns[c.cap] + (rest > 0 ? c.ns[rest] : 0.0);
+  return (double)steps * ns * scale * 1e-3;
 }
 
 int64_t env_i64(const char* name) {
