@@ -35,7 +35,8 @@
 //
 // Narrow shapes (too few rows to give every SIMD a wavefront) split each row
 // into segments instead, composed with Eq. (7) in three launches that need no
-// memory beyond y, in one of two forms.
+// memory beyond y, in one of two forms; plan_n16 below prices these choices,
+// and the quad layout of selective_scan_quad.hip, per call.
 // Records form: (1) each segment but the last walks from a zero state (the
 // first from h0) and records its end state U and the product P of its a_t,
 // formed as exp(A * the segment's sum of delta); (2) a fold turns these into
@@ -44,7 +45,7 @@
 // s live in y's first 32 words of segment s+1 (P in 16, U in 16; the fold
 // leaves h_in in the first 16), which launch (3) reads before it overwrites
 // them with y.
-// Correction form (long segments, fp32 y): (1) every segment walks from a
+// Correction form (fp32 y): (1) every segment walks from a
 // zero state (the first from h0), stores y except in its first super-tile,
 // and records P and U as above (the last segment its P beside the records
 // of its own first words, its U in h_last); (2) the fold composes them and
