@@ -259,15 +259,19 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     xr.load_buf(rx, off);
   };
   auto widen_dx = [&](int64_t sup) {
-    const int64_t t0 = sup * ST + V * n;
+    // steps past the segment are identity steps (a = 1, u = 0): the loads
+    // there returned zeros (fetch_dx), which is that already, unless the
+    // options turn delta = 0 into something else; Ls is a multiple of V, so
+    // a lane's V steps are all inside or all past
+    const bool past = OPT && (int32_t)(sup * ST) + V * n >= Ls32;
 #pragma unroll
     for (int k = 0; k < V; ++k) {
       float dv = dlr.get(k), xv = xr.get(k);
       if constexpr (OPT) {
         dv += dbv;
         if (flags & SEL_SOFTPLUS) dv = softplus_f32(dv);
+        if (past) dv = xv = 0.0f;
       }
-      if (t0 + k >= Ls) dv = xv = 0.0f;  // identity step: a = 1, u = 0
       dl[k] = dv;
       dx[k] = dv * xv;
       if constexpr (DSUM) dsum += dv;
@@ -287,10 +291,21 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   };
   float* const p_w = &sm.p[w][r * R16_PRS + n * R16_TS];
   const float* const p_r = &sm.p[w][r * R16_PRS + 8 * rh * R16_TS + 4 * rq];
-  float* const y_row = static_cast<float*>(yv) + (b * D + dcl) * L + ts;
-  // OPT: y before the output gate, for the backward of a gated call (or NULL)
-  float* const s_row = (OPT && s_out) ? s_out + (b * D + dcl) * L + ts : nullptr;
-  uint16_t* const y16_row = static_cast<uint16_t*>(yv) + (b * D + dcl) * L + ts;
+  // y (and, OPT, y before the output gate, for the backward of a gated call)
+  // leave through buffer resources over the workgroup's rows from the
+  // segment's start: a 32-bit offset per lane, and lanes with nothing to
+  // store aim at the resource's end, where the hardware drops the store.
+  // Sizes fit 32 bits: 16 rows of L < 2^26 steps of at most 4 bytes.
+  const uint32_t ys = ybf ? 2u : 4u;
+  const uint32_t y_bytes = (uint32_t)((rows * L - ts) * ys);
+  const __amdgpu_buffer_rsrc_t ry =
+      ybf ? buffer_rsrc(static_cast<uint16_t*>(yv) + row0 * L + ts, y_bytes)
+          : buffer_rsrc(static_cast<float*>(yv) + row0 * L + ts, y_bytes);
+  const uint32_t y_lrow = (uint32_t)((dcl - d0) * L) * ys;
+  const uint32_t s_bytes = (uint32_t)((rows * L - ts) * 4);
+  const __amdgpu_buffer_rsrc_t rs =
+      buffer_rsrc((OPT && s_out) ? s_out + row0 * L + ts : static_cast<float*>(yv), s_bytes);
+  const uint32_t s_lrow = (uint32_t)((dcl - d0) * L) * 4u;
 
   auto read_partials = [&](float4 (&pr)[8]) {
 #pragma unroll
@@ -309,23 +324,29 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     // add the other half of the row (lane n ^ 8), then Dskip*x, then the gate
 #pragma unroll
     for (int q = 0; q < 4; ++q) s4[q] = __builtin_fmaf(dsk, yx[q], s4[q] + row_ror8(s4[q]));
-    const int64_t t = kt * R16_T + 4 * rq;
+    const int32_t t = (int32_t)(kt * R16_T) + 4 * rq;
+    const bool mine = dok && rh == 0 && t < Ls32;
     // ALL: the first super-tile of every segment but the first holds the
     // records until the correction walk writes its y
     const bool skip = ALL && sg > 0 && t < ST;
     if constexpr (OPT) {
-      if (s_row && dok && rh == 0 && t < Ls)
-        *reinterpret_cast<float4*>(s_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
+      if (s_out) {
+        const uint32_t so = mine ? s_lrow + 4u * (uint32_t)t : s_bytes;
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(sw_u32x4, make_float4(s4[0], s4[1], s4[2], s4[3])), rs, (int)so,
+            0, 0);
+      }
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) s4[q] *= gt[q];
-    if (dok && rh == 0 && t < Ls && !skip) {
-      if (ybf)
-        *reinterpret_cast<uint2*>(y16_row + t) =
-            make_uint2(bf16x2_rne(s4[0], s4[1]), bf16x2_rne(s4[2], s4[3]));
-      else
-        *reinterpret_cast<float4*>(y_row + t) = make_float4(s4[0], s4[1], s4[2], s4[3]);
-    }
+    const uint32_t yo = (mine && !skip) ? y_lrow + ys * (uint32_t)t : y_bytes;
+    if (ybf)
+      __builtin_amdgcn_raw_buffer_store_b64(
+          __builtin_bit_cast(sw_u32x2, make_uint2(bf16x2_rne(s4[0], s4[1]), bf16x2_rne(s4[2], s4[3]))),
+          ry, (int)yo, 0, 0);
+    else
+      __builtin_amdgcn_raw_buffer_store_b128(
+          __builtin_bit_cast(sw_u32x4, make_float4(s4[0], s4[1], s4[2], s4[3])), ry, (int)yo, 0, 0);
   };
 
   auto read_ops = [&](R16Ops& o, int buf, int bi) {
