@@ -176,6 +176,13 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
   const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(Bm + ((int64_t)b * L + ts) * Q_N, bcbytes);
   const __amdgpu_buffer_rsrc_t rc = buffer_rsrc(Cm + ((int64_t)b * L + ts) * Q_N, bcbytes);
   const int32_t boff = ((lane >> 2) * Q_N + Q_S * (lane & 3)) * ES;
+  // y (and the pre-gate output) leave through resources over the
+  // wavefront's rows from the segment's start; a lane with nothing to store
+  // aims at the resource's end, where the store is dropped (16 rows of
+  // L < 2^26 fp32 steps fit 32 bits)
+  const uint32_t ybytes = (uint32_t)(((int64_t)rows * L - ts) * 4);
+  const __amdgpu_buffer_rsrc_t ry = buffer_rsrc(y + row0 * L + ts, ybytes);
+  const __amdgpu_buffer_rsrc_t rso = buffer_rsrc(OPT && s_out ? s_out + row0 * L + ts : y, ybytes);
   struct Raw {
     RawVec<IN, 4> d[2], x[2], z[2], b[2], c[2];
   };
@@ -285,15 +292,17 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
       s.w = __builtin_fmaf(idsk[k], xc[k][3], s.w);
       const int t = kt * Q_T + 4 * ij;
       const bool store = iok[k] && !(!CORR && sg > 0 && t < Q_SKIP);
-      const int64_t at = (row0 + iro[k]) * L + ts + t;
+      const uint32_t at = store ? (uint32_t)(iro[k] * L + t) * 4u : ybytes;
       if constexpr (OPT) {
-        if (s_out && store) *reinterpret_cast<float4*>(s_out + at) = s;
+        if (s_out)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(sw_u32x4, s), rso, (int)at, 0,
+                                                 0);
         s.x *= zc[k][0];
         s.y *= zc[k][1];
         s.z *= zc[k][2];
         s.w *= zc[k][3];
       }
-      if (store) *reinterpret_cast<float4*>(y + at) = s;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(sw_u32x4, s), ry, (int)at, 0, 0);
     }
   };
 
