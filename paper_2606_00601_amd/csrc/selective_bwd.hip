@@ -222,6 +222,19 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   const __amdgpu_buffer_rsrc_t rck =
       buffer_rsrc(w.ck + row0 * ntile * BW_N, (uint32_t)(nrows * ntile * BW_N * 4));
   const int32_t eck = (int32_t)(((dok ? d : D - 1) - d0) * ntile * BW_N) + n;
+  const uint32_t ck_b = (uint32_t)(nrows * ntile * BW_N * 4);
+  // BUF: the reduce's outputs through resources too, picked by the
+  // wavefront's role: role a the workgroup's rows of ddelta, dx (and dz),
+  // role b this workgroup's share of dB, dC; a lane with nothing to store
+  // aims at the resource's end, where the store is dropped (and a load
+  // returns zero)
+  const uint32_t out_b = role_a ? (uint32_t)(nrows * L * 4) : (uint32_t)(L * BW_N * 4);
+  const __amdgpu_buffer_rsrc_t ro0 =
+      buffer_rsrc(role_a ? a.ddelta + row0 * L : w.dB_p + (b * G + g) * L * BW_N, out_b);
+  const __amdgpu_buffer_rsrc_t ro1 =
+      buffer_rsrc(role_a ? a.dx + row0 * L : w.dC_p + (b * G + g) * L * BW_N, out_b);
+  const __amdgpu_buffer_rsrc_t roz =
+      buffer_rsrc(GATED ? a.dz + row0 * L : a.dx, GATED && role_a ? out_b : 0u);
   auto load_tile = [&](int64_t k, Raw& v) {
     if constexpr (BUF) {
       // a tile before the start reads tile 0 (unused); past the end, the
@@ -310,7 +323,11 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
       }
       load_tile(k + BW_RING - 1, ring[(u + BW_RING - 1) % BW_RING]);
       bw_barrier();  // one per tile: the other buffer is the one staged next
-      *(dok ? w.ck + (ck_row + k) * BW_N + n : w.trash + tid) = h;
+      if constexpr (BUF)
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), rck, dok ? eck * 4 : (int32_t)ck_b,
+                                              (int32_t)k * (BW_N * 4), 0);
+      else
+        *(dok ? w.ck + (ck_row + k) * BW_N + n : w.trash + tid) = h;
 #pragma unroll
       for (int q = 0; q < BW_T; q += 4) {
         const float4 dl4 = *reinterpret_cast<const float4*>(&sm.rv[buf][0][rr][q]);
@@ -348,6 +365,7 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
   auto reduce_tile = [&](int64_t k, int pb) {
     float v0, v1, v2 = 0.f;
     float *p0, *p1, *p2 = w.trash + tid;
+    uint32_t o = out_b;  // BUF: the byte offset of both outputs
     if (role_a) {
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll
@@ -358,13 +376,15 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
       const float ddl = p_live ? (s1 + p_xv * s2) * p_sg : 0.0f;
       v0 = ddl;
       v1 = __builtin_fmaf(p_dlv, s2, first ? p_ds * Dsk : 0.0f);
-      const int64_t i = srow * L + (p_live ? k * BW_T + st : 0);
-      p0 = p_live ? a.ddelta + i : w.trash + tid;
-      p1 = p_live ? a.dx + i : w.trash + tid;
-      if constexpr (GATED) {
-        v2 = p_dyv * p_sv * p_gp;
-        p2 = p_live ? a.dz + i : w.trash + tid;
+      if constexpr (BUF) {
+        if (p_live) o = (uint32_t)(ea + (int32_t)k * BW_T) * 4u;
+      } else {
+        const int64_t i = srow * L + (p_live ? k * BW_T + st : 0);
+        p0 = p_live ? a.ddelta + i : w.trash + tid;
+        p1 = p_live ? a.dx + i : w.trash + tid;
+        if constexpr (GATED) p2 = p_live ? a.dz + i : w.trash + tid;
       }
+      if constexpr (GATED) v2 = p_dyv * p_sv * p_gp;
       if (first) dD_acc = __builtin_fmaf(p_ds, p_xv, dD_acc);
       db_acc += ddl;
     } else {
@@ -378,20 +398,36 @@ __global__ __launch_bounds__(256) void selective_bwd_kernel(const BwdArgs a, con
         sc += sm.pw[pb][m][(32 + lb) * 4 + tb];
       }
       const int64_t t = k * BW_T + bt;
-      const int64_t i = ((b * G + g) * L + (t < L ? t : 0)) * BW_N + bn;
       v0 = sb;
       v1 = sc;
-      p0 = t < L ? w.dB_p + i : w.trash + tid;
-      p1 = t < L ? w.dC_p + i : w.trash + tid;
+      if constexpr (BUF) {
+        if (t < L) o = (uint32_t)((int32_t)t * BW_N + bn) * 4u;
+      } else {
+        const int64_t i = ((b * G + g) * L + (t < L ? t : 0)) * BW_N + bn;
+        p0 = t < L ? w.dB_p + i : w.trash + tid;
+        p1 = t < L ? w.dC_p + i : w.trash + tid;
+      }
     }
-    if (role_a && !first) {  // later state groups add to the sums over the states
-      v0 += *p0;
-      v1 += *p1;
-    }
-    *p0 = v0;
-    *p1 = v1;
-    if constexpr (GATED) {
-      if (first) *p2 = v2;
+    if constexpr (BUF) {
+      if (role_a && !first) {  // later state groups add to the sums over the states
+        v0 += buf_ld<float>(ro0, (int32_t)o, 0);
+        v1 += buf_ld<float>(ro1, (int32_t)o, 0);
+      }
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v0), ro0, (int32_t)o, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v1), ro1, (int32_t)o, 0, 0);
+      if constexpr (GATED) {
+        if (first) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v2), roz, (int32_t)o, 0, 0);
+      }
+    } else {
+      if (role_a && !first) {  // later state groups add to the sums over the states
+        v0 += *p0;
+        v1 += *p1;
+      }
+      *p0 = v0;
+      *p1 = v1;
+      if constexpr (GATED) {
+        if (first) *p2 = v2;
+      }
     }
   };
 
@@ -602,7 +638,8 @@ __global__ __launch_bounds__(256) void selective_bwd_reduce_kernel(const BwdArgs
 bool bwd_buf_fits(const BwdArgs& a, int64_t ntile) {
   const int64_t lim = (int64_t)1 << 31;
   const int64_t Lp = a.L + 4 * BW_RING * BW_T;
-  return BW_ROWS * Lp * 4 < lim && Lp * a.N * 4 < lim && BW_ROWS * (ntile + 2 * BW_RING) * BW_N * 4 < lim;
+  return BW_ROWS * Lp * 4 < lim && Lp * a.N * 4 < lim && Lp * BW_N * 4 < lim &&
+         BW_ROWS * (ntile + 2 * BW_RING) * BW_N * 4 < lim;
 }
 
 template <typename IN, typename DYT>
