@@ -547,10 +547,10 @@ LAYOUT_SWEEP_SHAPES = ";".join(
 LAYOUT_CANDIDATES = (
     [("whole", {"SW_SS_QUAD": "0", "SW_SS_SEGMENTS": "1"})]
     + [(f"r16c{k}", {"SW_SS_QUAD": "0", "SW_SS_SEGMENTS": str(k), "SW_SS_SEGFORM": "2"})
-       for k in (2, 4, 8, 16)]
+       for k in (2, 4, 6, 8, 16)]
     + [(f"r16r{k}", {"SW_SS_QUAD": "0", "SW_SS_SEGMENTS": str(k), "SW_SS_SEGFORM": "1"})
        for k in (4, 8)]
-    + [(f"quad{k}", {"SW_SS_QUAD": "1", "SW_SS_SEGMENTS": str(k)}) for k in (4, 8, 12, 16)])
+    + [(f"quad{k}", {"SW_SS_QUAD": "1", "SW_SS_SEGMENTS": str(k)}) for k in (4, 8, 9, 12, 16)])
 
 
 def layout_sweep(shapes: str) -> int:

@@ -226,6 +226,11 @@ int sw_affine_scan_proj_i32(const int32_t* a, const int32_t* b, const int32_t* x
  * four lanes per row, 1: whenever the call allows), SW_SS_SEGMENTS (the
  * count, 1: whole rows) and SW_SS_SEGFORM (1: records, 2: correction), read
  * per call, force the choice; sw_last_launch() names what a call enqueued.
+ * A count k gives segments of L / k steps rounded up to the layout's
+ * granularity (a 64- or 128-step super-tile with sixteen lanes per row, 64
+ * steps with four), the last one the rest (a rest shorter than that
+ * granularity joins the segment before, or, with four lanes per row, the
+ * length is rounded down instead).
  * y's memory holds the segments' carries between the call's kernels, so y
  * must not be read until the call completes on its stream (as for any
  * output).
@@ -362,7 +367,7 @@ const char* sw_last_error(void);
 /* Which kernels the calling thread's last successful fused forward call
  * (sw_selective_scan_fwd*, "" before any) enqueued: the layout, and for a
  * call split into segments their count, length and form -- e.g.
- * "selective_quad_kernel: 12 segments of 5440 steps, correction form (3
+ * "selective_quad_kernel: 9 segments of 7296 steps, correction form (3
  * launches)".  For tuning and benchmarks; the text is not a stable format. */
 const char* sw_last_launch(void);
 

@@ -156,7 +156,8 @@ __device__ __forceinline__ float* seg_words(void* yv, bool ybf, int64_t row, int
 // (1) and (3) of the segmented form, whose workgroups are (row block,
 // segment) pairs, logical workgroup = row block * segments of the launch +
 // segment (the logical order is spread over the XCDs in contiguous ranges);
-// a row has nseg segments of Lseg steps, the last one taking the rest.
+// a row has nseg segments of Lseg steps, the last one taking the rest
+// (shorter than Lseg, or up to a super-tile longer).
 template <typename IN, bool OPT, bool CK, int SEG>
 __global__ __launch_bounds__(256) void selective_row16_kernel(
     const IN* __restrict__ x, const IN* __restrict__ delta, const float* __restrict__ A,
@@ -635,7 +636,8 @@ bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es) {
 // workgroups per CU, fp32 inputs (the quad layout is 8% faster with bf16
 // inputs; its four-per-CU time, 226 ns with every CU at four, is set at 220
 // ns, what B=1, D=5120, L=65536 measures with three quarters of the CUs at
-// four: on four boxes 12 segments took 1489 us on average, 9 segments 1516).  A correction walk is priced at the fading length of Mamba-like
+// four).  Every segment of a launch walks at once, so a launch is priced at
+// its longest segment.  A correction walk is priced at the fading length of Mamba-like
 // decay, 1024 steps plus one check (slower decay walks further, up to the
 // whole segment: slower, never wrong); a segmented call adds 8 us for its
 // fold and two more launches; the first walk of the records form (no C, no
@@ -677,15 +679,31 @@ struct N16Plan {
   bool corr = false;
 };
 
-// Segments of the 16-lane layout for a count k: whole super-tiles of st
-// steps, the last segment taking the rest; n = 0 when k gives fewer than two.
+// Segments of the 16-lane layout for a count k: L / k rounded up to whole
+// super-tiles of st steps, as many segments as that takes, the last one the
+// rest; a rest shorter than a super-tile (too short for the records the
+// segment before leaves in its first words) joins the segment before.  n = 0
+// when k gives fewer than two.
 void r16_geometry(int64_t L, int64_t st, int64_t k, int64_t* n, int64_t* Lseg) {
   *n = 0;
   if (k < 2 || k > R16_MAX_SEG || L / st < 2) return;
   const int64_t per = (L + k - 1) / k;
   *Lseg = (per + st - 1) / st * st;
-  const int64_t m = L / *Lseg;
+  int64_t m = (L + *Lseg - 1) / *Lseg;
+  if (L - (m - 1) * *Lseg < st) --m;
   if (m >= 2 && m <= R16_MAX_SEG) *n = m;
+}
+
+// Segments of the quad layout for a count k: k - 1 segments of Lseg steps (a
+// multiple of QUAD_SKIP) and the last taking the rest.  Lseg is L / k rounded
+// up, which leaves the last segment the shortest, unless that leaves it fewer
+// than QUAD_SKIP steps (its first words hold 48 words of records); then
+// rounded down (the last the longest).  Lseg < QUAD_SKIP: no such geometry.
+void quad_geometry(int64_t L, int64_t k, int64_t* Lseg, int64_t* last) {
+  const int64_t per = (L + k - 1) / k;
+  *Lseg = (per + QUAD_SKIP - 1) / QUAD_SKIP * QUAD_SKIP;
+  if (L - (k - 1) * *Lseg < QUAD_SKIP) *Lseg = (L / k) / QUAD_SKIP * QUAD_SKIP;
+  *last = L - (k - 1) * *Lseg;
 }
 
 template <typename IN>
@@ -721,10 +739,12 @@ N16Plan plan_n16(const SelArgs& a, int64_t ndb) {
       int64_t n, Lseg;
       r16_geometry(L, st, k, &n, &Lseg);
       if (n < 2 || G16 * n >= ((int64_t)1 << 31)) continue;
+      // every segment walks at once: the longest sets the launch's time
       const int64_t last = L - (n - 1) * Lseg;
-      const double first = launch_us(G16 * n, last, cus, R16_COST, 1.0);
+      const int64_t longest = last > Lseg ? last : Lseg;
+      const double first = launch_us(G16 * n, longest, cus, R16_COST, 1.0);
       if (corr_ok && form_env != 1) {
-        const int64_t walk = last < PLAN_CORR_STEPS + st ? last : PLAN_CORR_STEPS + st;
+        const int64_t walk = longest < PLAN_CORR_STEPS + st ? longest : PLAN_CORR_STEPS + st;
         consider(first + launch_us(G16 * (n - 1), walk, cus, R16_COST, 1.0) + PLAN_SEG_US, false,
                  n, Lseg, true);
       }
@@ -744,11 +764,14 @@ N16Plan plan_n16(const SelArgs& a, int64_t ndb) {
     const int64_t qmin = seg_env > 0 && kmin > kcap ? kcap : kmin;
     const int64_t qmax = seg_env > 0 && kmax > kcap ? kcap : kmax;
     for (int64_t k = (qmin > 2 ? qmin : 2); k <= qmax; ++k) {
-      const int64_t Lseg = (L / k) / QUAD_SKIP * QUAD_SKIP;
+      int64_t Lseg, last;
+      quad_geometry(L, k, &Lseg, &last);
       if (Lseg < QUAD_SKIP) continue;
-      const int64_t last = L - (k - 1) * Lseg;
-      const int64_t walk = last < PLAN_CORR_STEPS + QUAD_SKIP ? last : PLAN_CORR_STEPS + QUAD_SKIP;
-      consider(launch_us(Gq * k, last, cus, QUAD_COST, qscale) +
+      // every segment walks at once: the longest sets the launch's time
+      const int64_t longest = last > Lseg ? last : Lseg;
+      const int64_t walk =
+          longest < PLAN_CORR_STEPS + QUAD_SKIP ? longest : PLAN_CORR_STEPS + QUAD_SKIP;
+      consider(launch_us(Gq * k, longest, cus, QUAD_COST, qscale) +
                    launch_us(Gq * (k - 1), walk, cus, QUAD_COST, qscale) + PLAN_SEG_US,
                true, k, Lseg, true);
     }

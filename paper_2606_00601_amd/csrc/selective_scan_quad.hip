@@ -406,12 +406,13 @@ bool quad_fits(const SelArgs& a) {
 }
 
 // Launches the quad layout with nseg segments of Lseg steps (the last takes
-// the rest; Lseg a multiple of Q_SKIP, 1 <= nseg <= Q_MAX_SEG); the call must
-// satisfy quad_fits.
+// the rest, at least Q_SKIP steps: its first words hold the records of the
+// segment before and its own P; Lseg a multiple of Q_SKIP, 1 <= nseg <=
+// Q_MAX_SEG); the call must satisfy quad_fits.
 template <typename IN>
 int launch_quad(const SelArgs& a, int64_t nseg, int64_t Lseg, hipStream_t s) {
   if (nseg < 1 || nseg > Q_MAX_SEG || (nseg > 1 && (Lseg < Q_SKIP || Lseg % Q_SKIP != 0 ||
-                                                    (nseg - 1) * Lseg >= a.L)))
+                                                    a.L - (nseg - 1) * Lseg < Q_SKIP)))
     return fail(SW_ERR_UNSUPPORTED, "quad layout: %lld segments of %lld steps for L=%lld",
                 (long long)nseg, (long long)Lseg, (long long)a.L);
   if (nseg == 1) Lseg = a.L;

@@ -446,8 +446,10 @@ def test_selective_continued_across_calls_bitexact(sw, monkeypatch, dtype, layou
 # Narrow calls split rows into segments (three launches composed with Eq. (7),
 # carries kept in y's memory).  (B, D, L) and the forced count ("auto": the
 # library's choice); D not a multiple of 16 leaves rows past D in the last
-# workgroup; counts that do not divide L give a longer last segment; L below
-# two super-tiles stays whole.
+# workgroup; counts that do not divide L leave the last segment shorter
+# (1000 / 3: 384, 384, 232), or, where the rest would be under a super-tile,
+# add it to the last one (776 / 5 in fp32: 192 x 3 + 200); L below two
+# super-tiles stays whole.
 _SEG_CASES = [((1, 37, 1000), "3"), ((2, 16, 512), "16"), ((1, 5, 4096), "auto"),
               ((1, 48, 2048), "auto"), ((1, 20, 64), "16"), ((3, 7, 776), "5")]
 
@@ -558,7 +560,7 @@ def test_selective_segments_correction_regimes(sw, monkeypatch, kind):
 # layout, long rows the quad layout, rows that fill the GPU whole rows, and
 # bf16 y keeps the records form.  Each call is also checked against the
 # oracle on sampled rows.
-_PLAN_CASES = [((1, 1280, 16384), "f32", False, "selective_row16_kernel: 8 segments of 2048 steps, correction"),
+_PLAN_CASES = [((1, 1280, 16384), "f32", False, "selective_row16_kernel: 6 segments of 2752 steps, correction"),
                ((1, 2560, 65536), "f32", False, "selective_quad_kernel: 16 segments"),
                ((1, 8192, 4096), "f32", False, "selective_row16_kernel: whole rows"),
                ((1, 1280, 4096), "f32", True, "selective_row16_kernel: 16 segments of 256 steps, records")]
@@ -588,11 +590,15 @@ def test_planner_choices(sw, case):
 # The quad layout (four lanes per row, four states per lane, 16 rows per
 # wavefront) taken by few-row, long calls; forced here on small shapes
 # (SW_SS_QUAD=1) with the segment count given: D not a multiple of 64 leaves
-# wavefronts with rows past D and wavefronts with none, L a multiple of 16 but
-# not of 64 gives a last segment longer than the others, one segment is the
-# whole-row walk.  (B, D, L), segments.
+# wavefronts with rows past D and wavefronts with none; L / k rounded up to 64
+# steps leaves the last segment the shortest (2048 / 3: 704, 704, 640; 8192 /
+# 7), and where that would leave it under 64 steps the length is rounded down
+# and the last segment is the longest (160 / 2: 64 + 96; 1056 / 16: 15 x 64 +
+# 96); one segment is the whole-row walk; L = 1040 (not whole 32-step tiles)
+# falls back to the 16-lane layout.  (B, D, L), segments.
 _QUAD_CASES = [((1, 37, 1040), "2"), ((2, 100, 2048), "3"), ((1, 64, 4096), "4"),
-                 ((1, 5, 16), "1"), ((3, 130, 512), "1"), ((1, 70, 8192), "7")]
+                 ((1, 5, 16), "1"), ((3, 130, 512), "1"), ((1, 70, 8192), "7"),
+                 ((1, 37, 160), "2"), ((1, 37, 1056), "16")]
 
 
 @pytest.mark.parametrize("case", _QUAD_CASES)
