@@ -95,13 +95,13 @@ struct RawVec {
   }
 };
 
-// Raw buffer resource over `bytes` bytes from `base` (stride 0, the gfx9
-// default data format): loads at byte offsets past the range return zero
-// instead of faulting.
 // 16- and 8-byte payloads of raw buffer stores
 typedef unsigned int sw_u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int sw_u32x2 __attribute__((ext_vector_type(2)));
 
+// Raw buffer resource over `bytes` bytes from `base` (stride 0, the gfx9
+// default data format): loads at byte offsets past the range return zero
+// instead of faulting, and stores there are dropped.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
                                            0x00020000);
