@@ -50,7 +50,10 @@
  *    fp32, 16-byte aligned arrays and a workgroup's byte offsets below 2^31;
  *    the bare scan and its projection form when a row fits one chunk
  *    (L <= 2048) or the rows alone fill the GPU (B*D >= 8 per compute unit);
- *    and the Blelloch schedule entry points.  A call that uses the scratch
+ *    sw_affine_scan_noalloc on every path (its look-back words live in a
+ *    static array that each call clears with a fill kernel and starts from
+ *    the same epoch and ticket, so a replay repeats the call exactly); and
+ *    the Blelloch schedule entry points.  A call that uses the scratch
  *    is not replay-safe (a replay would repeat the ticket range and epoch the
  *    host gave the captured launch), and the backward allocates a workspace
  *    per call: while the stream is capturing, those calls return

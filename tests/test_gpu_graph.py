@@ -6,13 +6,17 @@ The N = 16 forward takes no scratch memory and allocates nothing, so it can be
 captured; the calls that use the per-stream scratch (the bare scan's
 look-back, the persistent kernel of N != 16) or allocate (the backward) are
 not graph-replay safe, and the library refuses them while the stream is
-capturing (checked here).
+capturing (checked here).  The bare scan's entry point that allocates
+nothing keeps its look-back words in a static array that every call clears
+with a fill kernel and starts from the same epoch and ticket, so its
+look-back path can be captured too (checked here).
 """
 import sys
 
 import numpy as np
 import pytest
 
+import oracle
 import workloads as wl
 
 torch = pytest.importorskip("torch")
@@ -149,3 +153,47 @@ def test_capture_refuses_calls_that_need_scratch_or_workspace(sw):
         assert len(got) == len(ref) and len(got) > 0, name
         for gi, ri in zip(got, ref):
             assert torch.equal(gi, ri), name
+
+
+def test_noalloc_scan_graph_replays_match_eager(sw):
+    """The bare scan through the entry point that allocates nothing, on its
+    look-back path (three rows of 40 chunks: carries and tickets in the
+    library's static array, cleared by a fill kernel at every call), captured
+    into a HIP graph: every replay, with eager calls of both bare-scan entry
+    points between the replays, gives the eager result bit for bit.  The
+    inputs keep every partial composition an integer below 2^24 (a in {0, 1},
+    small integer bx), exact in fp32 in any association order, so the
+    look-back's order cannot change a bit."""
+    B, D, L = 1, 3, 40 * 2048 - 5
+    _say("case graph replay noalloc", B, D, L)
+    g_ = np.random.default_rng(780)
+    a_np = (g_.random((B, D, L)) < 0.9995).astype(np.float32)
+    bx_np = g_.integers(-8, 9, (B, D, L)).astype(np.float32)
+    a = torch.from_numpy(a_np).to("cuda")
+    bx = torch.from_numpy(bx_np).to("cuda")
+    h_ref = sw.affine_scan_noalloc(a, bx)  # also looks up the static array's address
+    torch.cuda.synchronize()
+    assert torch.equal(h_ref, sw.affine_scan(a, bx))
+    h = torch.empty_like(h_ref)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up on the capture stream
+        sw.affine_scan_noalloc(a, bx, out=h)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sw.affine_scan_noalloc(a, bx, out=h)
+    for i in range(4):
+        h.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(h, h_ref), f"replay {i}: h differs"
+        # eager work of the program between replays, on the same static array
+        h2 = sw.affine_scan_noalloc(a, bx)
+        h3 = sw.affine_scan(a, bx)
+        torch.cuda.synchronize()
+        assert torch.equal(h2, h_ref) and torch.equal(h3, h_ref)
+    assert np.array_equal(h_ref.cpu().numpy()[:, :1, :4096],
+                          oracle.affine_scan(a_np[:, :1, :4096], bx_np[:, :1, :4096]))
