@@ -111,8 +111,9 @@ int sw_affine_scan_i32(const int32_t* a, const int32_t* bx, const int32_t* h0, i
  * carries live in a static array in the library's device code (256 bytes +
  * 24 bytes per chunk, 1.5 MiB for SW_NOALLOC_MAX_CHUNKS chunks), one copy per
  * GPU, held until the process ends; its address is looked up on the first
- * call on each device.  Each call clears the part it uses with a fill kernel
- * on the call's stream before the scan.
+ * call on each device (make that call before capturing one into a HIP
+ * graph).  Each call clears the part it uses with a fill kernel on the
+ * call's stream before the scan.
  *   - Calls whose chunk-parallel look-back kernel would need more than
  *     SW_NOALLOC_MAX_CHUNKS chunks return SW_ERR_UNSUPPORTED before enqueuing
  *     anything.  That kernel runs when L > 2048 and B*D < 8 * (compute
