@@ -325,7 +325,10 @@ int sw_selective_scan_fwd_train(const void* x, const void* delta, const float* A
  *   dy      : (B, D, L) of dy_dtype (fp32 or bf16), required
  *   dh_last : (B, D, N) fp32 or NULL (zero)
  *   ckpt    : the ckpt of sw_selective_scan_fwd_train on the same inputs,
- *             or NULL (the backward then rebuilds it in its workspace)
+ *             or NULL (the backward then rebuilds it in its workspace: for
+ *             N = 16 where the forward takes its 16-lane layout, with the
+ *             forward's walk without y; else in its own kernel; the results
+ *             are the same bits either way)
  *   s_pre   : with z, the s_pre of sw_selective_scan_fwd_train on the same
  *             inputs, or NULL (the backward then reruns the forward without
  *             the gate, which also writes the checkpoints when N <= 16);
@@ -368,11 +371,13 @@ const char* sw_status_string(int status);
 /* Message for the calling thread's last non-OK return ("" if none). */
 const char* sw_last_error(void);
 
-/* Which kernels the calling thread's last successful fused forward call
- * (sw_selective_scan_fwd*, "" before any) enqueued: the layout, and for a
- * call split into segments their count, length and form -- e.g.
- * "selective_quad_kernel: 9 segments of 7296 steps, correction form (3
- * launches)".  For tuning and benchmarks; the text is not a stable format. */
+/* Which kernels the calling thread's last successful fused forward or
+ * backward call (sw_selective_scan_fwd*, sw_selective_scan_bwd; "" before
+ * any) enqueued: for the forward the layout, and for a call split into
+ * segments their count, length and form -- e.g. "selective_quad_kernel: 9
+ * segments of 7296 steps, correction form (3 launches)"; for the backward
+ * where its checkpoints came from.  For tuning and benchmarks; the text is
+ * not a stable format. */
 const char* sw_last_launch(void);
 
 #ifdef __cplusplus

@@ -740,6 +740,39 @@ int selective_bwd(const BwdArgs& a) {
       return st;
     }
   }
+  // still without checkpoints: where the forward takes its 16-lane layout,
+  // its walk without y writes them (the states do not depend on the gate),
+  // cheaper than the backward kernel's own sweep and bit-identical to it
+  const char* ck_from = a.ckpt ? "given" : ab.ckpt ? "from the ungated forward" : nullptr;
+  if (!ab.ckpt && a.N == BW_N) {
+    SelArgs fa{};
+    fa.x = a.x;
+    fa.delta = a.delta;
+    fa.Bm = a.Bm;
+    fa.Cm = a.Cm;
+    fa.A = a.A;
+    fa.delta_bias = a.delta_bias;
+    fa.h0 = a.h0;
+    fa.B = B;
+    fa.D = D;
+    fa.N = a.N;
+    fa.L = L;
+    fa.bf16_in = a.bf16_in;
+    fa.softplus = a.softplus;
+    fa.vec = a.vec;
+    fa.ckpt = w.ck;
+    bool taken = false;
+    st = selective_states_fwd(fa, &taken);
+    if (st != SW_OK) {
+      workspace_free(base, s);
+      return st;
+    }
+    if (taken) {
+      ab.ckpt = w.ck;
+      ck_from = "from the forward's walk without y";
+    }
+  }
+  if (!ck_from) ck_from = "rebuilt by the backward kernel";
   // the states in groups of 16: each group's main kernel, then its reduction
   // (dA, dB, dC of its states; the sums over the states accumulate)
   for (int n0 = 0; n0 < a.N && st == SW_OK; n0 += BW_N) {
@@ -756,6 +789,10 @@ int selective_bwd(const BwdArgs& a) {
     st = check_launch("selective_bwd_reduce_kernel");
   }
   workspace_free(base, s);
+  if (st == SW_OK)
+    note_launch("selective_bwd_kernel + selective_bwd_reduce_kernel (%lld state group%s), "
+                "checkpoints %s",
+                (long long)((a.N + BW_N - 1) / BW_N), a.N > BW_N ? "s" : "", ck_from);
   return st;
 }
 

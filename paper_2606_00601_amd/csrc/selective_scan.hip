@@ -638,24 +638,36 @@ int launch_npl(const SelArgs& a, bool vec, hipStream_t s) {
 bool row16_fits(int64_t D, int64_t N, int64_t L, size_t es);
 template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s);
+template <typename IN>
+int launch_row16_states(const SelArgs& a, hipStream_t s);
 
 namespace {
+
+// The vector path loads through buffer resources with 32-bit byte offsets:
+// it needs 16-byte aligned B and C (tile starts are then aligned) and every
+// offset of a task, including the tiles fetched past the end, below 2^31.
+template <typename IN>
+bool vector_path(const SelArgs& a) {
+  const int64_t es = (int64_t)sizeof(IN), pad = 4 * SS_T;
+  const bool fits = SS_RPW * (a.L + pad) * es < ((int64_t)1 << 31) &&
+                    (a.L + pad) * a.N * es < ((int64_t)1 << 31);
+  return a.vec && fits && ((uintptr_t)a.Bm % 16 == 0) && ((uintptr_t)a.Cm % 16 == 0);
+}
+
+// N = 16 on the vector path: one state per lane, 16-lane rows
+// (selective_scan16.hip); SW_SS_LAYOUT=8 keeps the 8-lane layout.
+template <typename IN>
+bool row16_path(const SelArgs& a) {
+  return vector_path<IN>(a) && env_int("SW_SS_LAYOUT", 16) == 16 &&
+         row16_fits(a.D, a.N, a.L, sizeof(IN));
+}
 
 template <typename IN>
 int launch_selective(const SelArgs& a) {
   hipStream_t s = current_stream();
-  const int64_t N = a.N, L = a.L;
-  // The vector path loads through buffer resources with 32-bit byte offsets:
-  // it needs 16-byte aligned B and C (tile starts are then aligned) and every
-  // offset of a task, including the tiles fetched past the end, below 2^31.
-  const int64_t es = (int64_t)sizeof(IN), pad = 4 * SS_T;
-  const bool fits = SS_RPW * (L + pad) * es < ((int64_t)1 << 31) &&
-                    (L + pad) * N * es < ((int64_t)1 << 31);
-  const bool v = a.vec && fits && ((uintptr_t)a.Bm % 16 == 0) && ((uintptr_t)a.Cm % 16 == 0);
-  // N = 16 on the vector path: one state per lane, 16-lane rows
-  // (selective_scan16.hip); SW_SS_LAYOUT=8 keeps the 8-lane layout.
-  if (v && env_int("SW_SS_LAYOUT", 16) == 16 && row16_fits(a.D, N, L, sizeof(IN)))
-    return launch_row16<IN>(a, s);
+  const int64_t N = a.N;
+  const bool v = vector_path<IN>(a);
+  if (row16_path<IN>(a)) return launch_row16<IN>(a, s);
   if (N <= 8) return launch_npl<IN, 1>(a, v, s);
   if (N <= 16) return launch_npl<IN, 2>(a, v, s);
   if (N <= 32) return launch_npl<IN, 4>(a, v, s);
@@ -666,6 +678,15 @@ int launch_selective(const SelArgs& a) {
 
 int selective_fwd(const SelArgs& a) {
   return a.bf16_in ? launch_selective<uint16_t>(a) : launch_selective<float>(a);
+}
+
+int selective_states_fwd(const SelArgs& a, bool* taken) {
+  *taken = false;
+  if (a.N != 16 || !a.ckpt || a.z || a.y_bf16 || a.s_out) return SW_OK;
+  if (a.bf16_in ? !row16_path<uint16_t>(a) : !row16_path<float>(a)) return SW_OK;
+  *taken = true;
+  hipStream_t s = current_stream();
+  return a.bf16_in ? launch_row16_states<uint16_t>(a, s) : launch_row16_states<float>(a, s);
 }
 
 }  // namespace sw

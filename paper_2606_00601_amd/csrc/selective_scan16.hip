@@ -128,7 +128,16 @@ struct R16Ops {
 // Segment modes of the kernel (see the top of the file).
 //   R16_SEG_ENDS, R16_SEG_FWD: launches (1) and (3) of the records form;
 //   R16_SEG_ALL, R16_SEG_CORR: launches (1) and (3) of the correction form.
-enum : int { R16_WHOLE = 0, R16_SEG_ENDS = 1, R16_SEG_FWD = 2, R16_SEG_ALL = 3, R16_SEG_CORR = 4 };
+//   R16_STATES: a whole-row walk that writes only the states (the 8-step
+//   checkpoints and h_last), for a backward call without them.
+enum : int {
+  R16_WHOLE = 0,
+  R16_SEG_ENDS = 1,
+  R16_SEG_FWD = 2,
+  R16_SEG_ALL = 3,
+  R16_SEG_CORR = 4,
+  R16_STATES = 5
+};
 constexpr int R16_MAX_SEG = 16;  // segments per row at most
 // The correction walk of a segment stops once, for every state of its
 // workgroup, the part of the state carried in from the segment's start,
@@ -166,8 +175,10 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     void* __restrict__ yv, float* __restrict__ h_last, int64_t D, int64_t L, int64_t ndb,
     uint32_t flags_in, float* __restrict__ ck, int64_t nT8, float* __restrict__ s_out,
     int64_t nseg, int64_t Lseg) {
-  static_assert(!(CK && SEG != R16_WHOLE), "checkpoints are written by whole-row walks only");
+  constexpr bool WHOLE = SEG == R16_WHOLE || SEG == R16_STATES;  // one walk per row
+  static_assert(!(CK && !WHOLE), "checkpoints are written by whole-row walks only");
   constexpr bool ENDS = SEG == R16_SEG_ENDS;  // no y: the segment's P and end state
+  constexpr bool NOY = ENDS || SEG == R16_STATES;  // no C, no y
   constexpr bool ALL = SEG == R16_SEG_ALL;    // y from a zero state, and the segment's records
   constexpr bool CORR = SEG == R16_SEG_CORR;  // the walk from the composed initial state
   constexpr bool DSUM = ENDS || ALL || CORR;  // sum of delta over the segment
@@ -186,10 +197,10 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   // segments 0 .. nseg-2, launch (3) of the correction form 1 .. nseg-1)
   const int64_t nsl = (ENDS || CORR) ? nseg - 1 : nseg;
   const int64_t bid = xcd_contiguous(blockIdx.x, gridDim.x);
-  const int64_t sg = SEG != R16_WHOLE ? bid % nsl + (CORR ? 1 : 0) : 0;
-  const int64_t rblk = SEG != R16_WHOLE ? bid / nsl : bid;
-  const int64_t ts = SEG != R16_WHOLE ? sg * Lseg : 0;  // first step of the segment
-  const int64_t Ls = SEG != R16_WHOLE ? (sg == nseg - 1 ? L - ts : Lseg) : L;  // its steps
+  const int64_t sg = !WHOLE ? bid % nsl + (CORR ? 1 : 0) : 0;
+  const int64_t rblk = !WHOLE ? bid / nsl : bid;
+  const int64_t ts = !WHOLE ? sg * Lseg : 0;  // first step of the segment
+  const int64_t Ls = !WHOLE ? (sg == nseg - 1 ? L - ts : Lseg) : L;  // its steps
   const int32_t Ls32 = (int32_t)Ls;  // below 2^31 / 16 (row16_fits)
   const int64_t b = rblk / ndb;
   const int64_t d0 = (rblk - b * ndb) * R16_ROWS;
@@ -238,15 +249,17 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   auto fetch_bc = [&](RawVec<IN, 2>& rbv, RawVec<IN, 2>& rcv, int64_t kt) {
     const int32_t off = (int32_t)(((kt * R16_T + stt) * R16_N + sn) * ES);
     rbv.load_buf(rb, off);
-    rcv.load_buf(rc, off);
+    if constexpr (!NOY) rcv.load_buf(rc, off);  // NOY: C is not read
   };
   auto stage_bc = [&](const RawVec<IN, 2>& rbv, const RawVec<IN, 2>& rcv, int buf) {
     float* bb = &sm.bc[buf][0][sn * R16_TS + stt];
     float* cc = &sm.bc[buf][1][sn * R16_TS + stt];
     bb[0] = rbv.get(0);
     bb[R16_TS] = rbv.get(1);
-    cc[0] = rcv.get(0);
-    cc[R16_TS] = rcv.get(1);
+    if constexpr (!NOY) {
+      cc[0] = rcv.get(0);
+      cc[R16_TS] = rcv.get(1);
+    }
   };
 
   // ---- delta / x of a super-tile: this lane's V steps starting at V*n
@@ -285,7 +298,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   const int rq = n % 8, rh = n / 8;
   RawVec<IN, 4> yxr, yzr;  // raw x and z of those four steps, for the tile awaiting its reduce
   auto fetch_yx = [&](int64_t kt) {
-    if constexpr (ENDS) return;
+    if constexpr (NOY) return;
     const int32_t off = lrow + (int32_t)((kt * R16_T + 4 * rq) * ES);
     yxr.load_buf(rx, off);
     if constexpr (OPT) yzr.load_buf(rz, off);
@@ -352,7 +365,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
 
   auto read_ops = [&](R16Ops& o, int buf, int bi) {
     o.b = *reinterpret_cast<const float4*>(&sm.bc[buf][0][n * R16_TS + 4 * bi]);
-    if constexpr (!ENDS) o.c = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n * R16_TS + 4 * bi]);
+    if constexpr (!NOY) o.c = *reinterpret_cast<const float4*>(&sm.bc[buf][1][n * R16_TS + 4 * bi]);
   };
 
   // ---- prologue: delta/x of super-tile 0, B/C of tiles 0..2, y-x of tile 0
@@ -391,7 +404,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     // this wavefront's own partials: after the barrier, so that the barrier
     // only drains the staging writes
     float4 pr[8];
-    if (!ENDS && kt > 0) read_partials(pr);
+    if (!NOY && kt > 0) read_partials(pr);
 #pragma unroll
     for (int bi = 0; bi < R16_NB; ++bi) {
       const int nb = bi + R16_LA;
@@ -433,13 +446,13 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
         const float u = dxv * bq[q];
         h = __builtin_fmaf(a, h, u);
         if constexpr (CORR) mag = __builtin_fmaf(a, mag, __builtin_fabsf(u));
-        if constexpr (ENDS) {
+        if constexpr (NOY) {
           p4[q] = 0.0f;
         } else {
           p4[q] = cq[q] * h;
         }
       }
-      if constexpr (!ENDS) {
+      if constexpr (!NOY) {
         *reinterpret_cast<float4*>(p_w + 4 * bi) = make_float4(p4[0], p4[1], p4[2], p4[3]);
         if (bi == 0 && kt > 0) finish_reduce(kt - 1, pr, yx_prev, gt_prev);
       }
@@ -500,6 +513,8 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
       wd[n] = __builtin_amdgcn_exp2f(Al * dsum);
       wd[R16_N + n] = h;
     }
+  } else if constexpr (SEG == R16_STATES) {
+    if (h_last && dok) h_last[(b * D + d) * R16_N + n] = h;
   } else {
     float4 pr[8];
     read_partials(pr);
@@ -522,7 +537,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
       }
     }
     if constexpr (!CORR) {
-      if (h_last && dok && (SEG == R16_WHOLE || sg == nseg - 1))
+      if (h_last && dok && (WHOLE || sg == nseg - 1))
         h_last[(b * D + d) * R16_N + n] = h;
     }
   }
@@ -871,7 +886,32 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
   return check_launch("selective_row16_kernel");
 }
 
+// The states of a whole-row walk without y (R16_STATES): the 8-step
+// checkpoints into a.ckpt and, if given, h_last; x, delta, B, A, h0 and the
+// delta options are read, C, Dskip, z and y are not.  The call must satisfy
+// row16_fits and the forward's vector-path conditions.
+template <typename IN>
+int launch_row16_states(const SelArgs& a, hipStream_t s) {
+  const int64_t ndb = (a.D + R16_ROWS - 1) / R16_ROWS;
+  const int64_t grid = a.B * ndb;
+  if (grid >= ((int64_t)1 << 31))
+    return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
+  const bool opt = a.delta_bias || a.softplus;
+  const uint32_t flags = a.softplus ? SEL_SOFTPLUS : 0u;
+  auto kern = opt ? selective_row16_kernel<IN, true, true, R16_STATES>
+                  : selective_row16_kernel<IN, false, true, R16_STATES>;
+  // y is never written in this mode: x stands in for its pointer
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, s, static_cast<const IN*>(a.x),
+                     static_cast<const IN*>(a.delta), a.A, static_cast<const IN*>(a.Bm),
+                     static_cast<const IN*>(a.Cm), a.Dskip, static_cast<const IN*>(nullptr),
+                     a.delta_bias, a.h0, const_cast<void*>(a.x), a.h_last, a.D, a.L, ndb, flags,
+                     a.ckpt, (a.L + 7) / 8, static_cast<float*>(nullptr), (int64_t)1, a.L);
+  return check_launch("selective_row16_kernel (states)");
+}
+
 template int launch_row16<float>(const SelArgs&, hipStream_t);
 template int launch_row16<uint16_t>(const SelArgs&, hipStream_t);
+template int launch_row16_states<float>(const SelArgs&, hipStream_t);
+template int launch_row16_states<uint16_t>(const SelArgs&, hipStream_t);
 
 }  // namespace sw

@@ -20,7 +20,7 @@ int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)))
 hipStream_t current_stream();
 int check_launch(const char* what);  // hipGetLastError -> SW_ERR_HIP with a message
 // Records, for sw_last_launch(), which kernels the calling thread's last
-// fused forward enqueued.
+// fused forward or backward call enqueued.
 void note_launch(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 
 // Compute units of the current device (looked up once per device), written
@@ -76,6 +76,12 @@ struct SelArgs {
 };
 int selective_fwd(const SelArgs& a);
 int selective_blelloch_fwd(const SelArgs& a);
+// The states of the forward walk without y: the 8-step checkpoints (a.ckpt,
+// required) and h_last if given, for a backward call without the forward's
+// checkpoints.  Enqueues (*taken = true) only where the forward takes its
+// 16-lane layout and no gate, bf16 y or pre-gate output is asked for;
+// otherwise returns SW_OK with nothing enqueued.
+int selective_states_fwd(const SelArgs& a, bool* taken);
 
 // Arguments of one backward call of the fused form, already validated.
 // x, delta, Bm, Cm, z are fp32 or bf16 as `bf16_in` says, dy as `dy_bf16`

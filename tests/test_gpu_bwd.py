@@ -329,3 +329,45 @@ def test_autograd_chained_segments_match_one_call(sw):
            "dC": leaves["Cm"].grad, "dDskip": leaves["Dskip"].grad}
     for k, v in got.items():
         assert_gate(fp_gate(v.cpu().numpy(), o[k], o["m_" + k]), f"chained autograd {k}")
+
+
+@pytest.mark.parametrize("shape", [(2, 21, 16, 512), (1, 16, 16, 64), (2, 37, 16, 203)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("opts", [(), ("bias", "softplus", "h0", "dhl")])
+def test_backward_without_checkpoints_takes_the_states_walk(sw, monkeypatch, shape, dtype, opts):
+    """Without the forward's checkpoints and without a gate, a call the
+    16-lane forward layout takes (N = 16, L a multiple of the vector width)
+    gets its checkpoints from the forward's walk without y; other calls
+    (L = 203) rebuild them in the backward kernel.  Either way the gradients
+    are the oracle's and the same bits as with the training forward's
+    checkpoints."""
+    monkeypatch.setenv("SW_SS_SEGMENTS", "1")  # the training forward walks whole rows
+    B, D, N, L = shape
+    _say("case bwd states walk", dtype, shape, opts)
+    inp, ex = _inputs(B, D, N, L, 970 + L, dtype, opts)
+    if dtype == "bf16":
+        x, dl = _bf16_dev(inp["x_bf16"]), _bf16_dev(inp["delta_bf16"])
+        Bm, Cm = _bf16_dev(inp["Bm_bf16"]), _bf16_dev(inp["Cm_bf16"])
+    else:
+        x, dl, Bm, Cm = (_dev(inp[k]) for k in ("x", "delta", "Bm", "Cm"))
+    kw = {}
+    if "bias" in opts:
+        kw = dict(delta_bias=_dev(ex["delta_bias"]), h0=_dev(ex["h0"]), delta_softplus=True)
+    A, Dk = _dev(inp["A"]), _dev(inp["Dskip"])
+    dhl = _dev(ex["dh_last"]) if "dhl" in opts else None
+    args = (x, dl, A, Bm, Cm, Dk, _dev(ex["dy"]), dhl)
+    g0 = sw.selective_scan_bwd(*args, **kw)
+    torch.cuda.synchronize()
+    walked = "walk without y" in sw.last_launch()
+    assert walked == (L % (8 if dtype == "bf16" else 4) == 0), sw.last_launch()
+    ck = sw.new_ckpt(x, N)
+    sw.selective_scan_fwd(x, dl, A, Bm, Cm, Dk, ckpt=ck, **kw)
+    g1 = sw.selective_scan_bwd(*args, ckpt=ck, **kw)
+    torch.cuda.synchronize()
+    assert sw.last_launch().endswith("checkpoints given"), sw.last_launch()
+    for k in g0:
+        assert torch.equal(g0[k], g1[k]), k
+    keys = ["dx", "ddelta", "dA", "dB", "dC", "dDskip", "dh0"]
+    if "bias" in opts:
+        keys.append("ddelta_bias")
+    _check_all(g0, _ref(inp, ex, opts), f"bwd states walk {dtype} {shape} {opts}", keys)
