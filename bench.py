@@ -502,6 +502,7 @@ def bench_bwd(w, args):
                               ckpt=ck, s_pre=sp, **opt)
 
     wall, kern, per = run_timed(step, args)
+    launch = sw.last_launch()  # the backward's kernels and where its checkpoints came from
     elems = w.elems
     # algorithmic bytes: x, delta, dy read; dx, ddelta written (fp32); B, C
     # read, dB, dC written (fp32); A, Dskip read, dA, dDskip, dh0 written
@@ -527,7 +528,7 @@ def bench_bwd(w, args):
                      "frac": gbs / HBM_PEAK_GBS,
                      "traffic": (measured_traffic(w, bwd=True)
                                  if args.ckpt and not args.options else None),
-                     "kernel": "selective_bwd_kernel + selective_bwd_reduce_kernel",
+                     "kernel": launch,
                      "per_launch_us": launch_stats(kern, per, args.graph),
                      "algorithmic_bytes": abytes},
         "alu": {"achieved": flops / 1e12, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
