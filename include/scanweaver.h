@@ -371,6 +371,29 @@ const char* sw_status_string(int status);
 /* Message for the calling thread's last non-OK return ("" if none). */
 const char* sw_last_error(void);
 
+/*
+ * The kernels sw_selective_scan_fwd_ex (train = 0) or
+ * sw_selective_scan_fwd_train (train = 1) would enqueue for these sizes and
+ * dtypes, with 16-byte aligned arrays, on a part with `cus` compute units
+ * (cus <= 0: the current device's), under the same SW_SS_* environment;
+ * nothing is launched and no device memory is touched, so with cus > 0 it
+ * needs no GPU.  Outputs (all required):
+ *   layout : 16 (one lane per state), 4 (four lanes per row, four states
+ *            each), 8 (the kernel for any N, which chains its own sequence
+ *            chunks), or 0 when there is nothing to launch (B*D or L zero)
+ *   nseg, lseg : the row is walked as nseg segments of lseg steps, the last
+ *            taking the rest (1 and L: whole rows; 0 and 0 with layout 0)
+ *   form   : 0 whole rows, 1 records form, 2 correction form (see
+ *            sw_selective_scan_fwd)
+ * Errors as the forward call's for the same sizes: SW_ERR_INVALID_ARG
+ * (unknown dtype, negative size, NULL output), SW_ERR_UNSUPPORTED (N outside
+ * [1, 64], train with N > 16, sizes past the launch limits); SW_ERR_HIP when
+ * cus <= 0 and the device cannot be queried.
+ */
+int sw_selective_scan_plan(int64_t B, int64_t D, int64_t N, int64_t L, int in_dtype,
+                           int out_dtype, int train, int cus, int* layout, int64_t* nseg,
+                           int64_t* lseg, int* form);
+
 /* Which kernels the calling thread's last successful fused forward or
  * backward call (sw_selective_scan_fwd*, sw_selective_scan_bwd; "" before
  * any) enqueued: for the forward the layout, and for a call split into

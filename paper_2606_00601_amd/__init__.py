@@ -27,6 +27,8 @@ C ABI one function per entry point; ``lib()`` is the same ABI through ctypes.
   every gradient of the fused form (fp32), deterministic.
 * ``selective_scan_fn(...)``: the fused form as a torch autograd function
   (forward with checkpoints, the library's backward).
+* ``selective_scan_plan(B, D, N, L, ...)``: the kernels, segments and form
+  the fused forward would take for those sizes, without launching anything.
 """
 from __future__ import annotations
 
@@ -35,7 +37,7 @@ import torch
 from ._lib import (SW_DELTA_SOFTPLUS, SW_DTYPE_BF16, SW_DTYPE_F32,  # noqa: F401
                    ScanWeaverError, check, fast, last_error, lib, status_string)
 
-__all__ = ["last_launch", "affine_scan", "affine_scan_noalloc", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
+__all__ = ["last_launch", "selective_scan_plan", "affine_scan", "affine_scan_noalloc", "affine_scan_i32", "affine_scan_schedule", "affine_scan_schedule_i32",
            "affine_scan_proj", "affine_scan_proj_i32",
            "selective_scan_fwd", "selective_scan_fwd_schedule", "selective_scan_bwd", "new_ckpt",
            "selective_scan_fn",
@@ -48,9 +50,31 @@ def version() -> int:
 
 
 def last_launch() -> str:
-    """Which kernels this thread's last fused forward call enqueued (layout,
-    segment count and form); for tuning and benchmarks, not a stable format."""
+    """Which kernels this thread's last fused forward or backward call
+    enqueued (forward: layout, segment count and form; backward: where its
+    checkpoints came from); for tuning and benchmarks, not a stable format."""
     return lib().sw_last_launch().decode()
+
+
+_FORMS = {0: "whole", 1: "records", 2: "correction"}
+
+
+def selective_scan_plan(B, D, N, L, dtype="f32", y_dtype=None, train=False, cus=0) -> dict:
+    """The kernels the fused forward would take for these sizes (16-byte
+    aligned arrays) on a part with ``cus`` compute units (0: the current
+    device's), without launching anything: ``layout`` 16, 4, 8 (or 0: nothing
+    to launch), ``segments`` and ``segment_steps`` (the last segment takes
+    the rest) and ``form`` ("whole", "records" or "correction")."""
+    import ctypes
+    codes = {"f32": SW_DTYPE_F32, "bf16": SW_DTYPE_BF16}
+    layout, form = ctypes.c_int(), ctypes.c_int()
+    nseg, lseg = ctypes.c_int64(), ctypes.c_int64()
+    check(lib().sw_selective_scan_plan(
+        B, D, N, L, codes[dtype], codes[y_dtype or "f32"], int(bool(train)), int(cus),
+        ctypes.byref(layout), ctypes.byref(nseg), ctypes.byref(lseg), ctypes.byref(form)),
+        "sw_selective_scan_plan")
+    return {"layout": layout.value, "segments": nseg.value, "segment_steps": lseg.value,
+            "form": _FORMS[form.value]}
 
 
 def _ptr(t):

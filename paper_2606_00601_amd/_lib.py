@@ -35,6 +35,7 @@ SIGNATURES = {
     "sw_affine_scan_proj": (_int, [_vp] * 7 + [_i64] * 3),
     "sw_selective_scan_bwd": (_int, [_vp] * 22 + [_i64] * 4 + [_int] * 3),
     "sw_selective_scan_fwd_train": (_int, [_vp] * 13 + [_i64] * 4 + [_int] * 3),
+    "sw_selective_scan_plan": (_int, [_i64] * 4 + [_int] * 4 + [_vp] * 4),
     "sw_affine_scan_proj_i32": (_int, [_vp] * 7 + [_i64] * 3),
     "sw_selective_scan_fwd": (_int, [_vp] * 8 + [_i64] * 4),
     "sw_selective_scan_fwd_bf16": (_int, [_vp] * 8 + [_i64] * 4),

@@ -640,6 +640,8 @@ template <typename IN>
 int launch_row16(const SelArgs& a, hipStream_t s);
 template <typename IN>
 int launch_row16_states(const SelArgs& a, hipStream_t s);
+template <typename IN>
+SelPlan plan_row16(const SelArgs& a, int cus);
 
 namespace {
 
@@ -678,6 +680,17 @@ int launch_selective(const SelArgs& a) {
 
 int selective_fwd(const SelArgs& a) {
   return a.bf16_in ? launch_selective<uint16_t>(a) : launch_selective<float>(a);
+}
+
+SelPlan selective_plan(const SelArgs& a, int cus) {
+  SelPlan q;
+  if (a.B * a.D == 0 || a.L == 0) return q;
+  if (a.bf16_in ? row16_path<uint16_t>(a) : row16_path<float>(a))
+    return a.bf16_in ? plan_row16<uint16_t>(a, cus) : plan_row16<float>(a, cus);
+  q.layout = 8;
+  q.nseg = 1;
+  q.lseg = a.L;
+  return q;
 }
 
 int selective_states_fwd(const SelArgs& a, bool* taken) {

@@ -721,8 +721,9 @@ void quad_geometry(int64_t L, int64_t k, int64_t* Lseg, int64_t* last) {
   *last = L - (k - 1) * *Lseg;
 }
 
+// `cus`: the compute units the launches are priced for.
 template <typename IN>
-N16Plan plan_n16(const SelArgs& a, int64_t ndb) {
+N16Plan plan_n16(const SelArgs& a, int64_t ndb, int cus) {
   N16Plan best;
   if (a.ckpt) return best;  // checkpoints are written by whole-row walks
   const int64_t L = a.L, st = R16_N * (16 / (int64_t)sizeof(IN));
@@ -732,8 +733,6 @@ N16Plan plan_n16(const SelArgs& a, int64_t ndb) {
   const bool quad_only = quad_env == 1 && qfits;
   const bool with_quad = qfits && quad_env != 0 && (seg_env < 0 || quad_only);
   const bool corr_ok = !a.y_bf16;
-  int cus = 0;
-  if (device_cus(&cus) != SW_OK) cus = 256;  // a forced choice needs no device facts
   const double qscale = sizeof(IN) == 2 ? 0.92 : 1.0;
   const int64_t G16 = a.B * ndb, Gq = a.B * ((a.D + 63) / 64);
   double best_us = 1e300;
@@ -850,7 +849,9 @@ int launch_row16(const SelArgs& a, hipStream_t s) {
   const int64_t grid = a.B * ndb;
   if (grid >= ((int64_t)1 << 31))
     return fail(SW_ERR_UNSUPPORTED, "%lld workgroups exceed the grid range", (long long)grid);
-  const N16Plan p = plan_n16<IN>(a, ndb);
+  int cus = 0;
+  if (device_cus(&cus) != SW_OK) cus = 256;  // a forced choice needs no device facts
+  const N16Plan p = plan_n16<IN>(a, ndb, cus);
   if (p.quad) return launch_quad<IN>(a, p.nseg, p.Lseg, s);
   const uint32_t flags = (a.softplus ? SEL_SOFTPLUS : 0u) | (a.y_bf16 ? SEL_Y_BF16 : 0u) |
                          (a.z ? SEL_GATED : 0u);
@@ -909,8 +910,22 @@ int launch_row16_states(const SelArgs& a, hipStream_t s) {
   return check_launch("selective_row16_kernel (states)");
 }
 
+// What launch_row16 would enqueue for `a` on a part with `cus` compute units.
+template <typename IN>
+SelPlan plan_row16(const SelArgs& a, int cus) {
+  const N16Plan p = plan_n16<IN>(a, (a.D + R16_ROWS - 1) / R16_ROWS, cus);
+  SelPlan q;
+  q.layout = p.quad ? 4 : 16;
+  q.nseg = p.nseg;
+  q.lseg = p.nseg > 1 ? p.Lseg : a.L;
+  q.form = p.nseg > 1 ? (p.corr ? 2 : 1) : 0;
+  return q;
+}
+
 template int launch_row16<float>(const SelArgs&, hipStream_t);
 template int launch_row16<uint16_t>(const SelArgs&, hipStream_t);
+template SelPlan plan_row16<float>(const SelArgs&, int);
+template SelPlan plan_row16<uint16_t>(const SelArgs&, int);
 template int launch_row16_states<float>(const SelArgs&, hipStream_t);
 template int launch_row16_states<uint16_t>(const SelArgs&, hipStream_t);
 

@@ -669,6 +669,48 @@ SW_API int sw_selective_scan_fwd_ex(const void* x, const void* delta, const floa
   return sw::selective_common(a);
 }
 
+SW_API int sw_selective_scan_plan(int64_t B, int64_t D, int64_t N, int64_t L, int in_dtype,
+                                  int out_dtype, int train, int cus, int* layout, int64_t* nseg,
+                                  int64_t* lseg, int* form) {
+  if (!layout || !nseg || !lseg || !form)
+    return sw::fail(SW_ERR_INVALID_ARG, "an output pointer is NULL");
+  if ((in_dtype != SW_DTYPE_F32 && in_dtype != SW_DTYPE_BF16) ||
+      (out_dtype != SW_DTYPE_F32 && out_dtype != SW_DTYPE_BF16))
+    return sw::fail(SW_ERR_INVALID_ARG, "unknown dtype (in=%d out=%d)", in_dtype, out_dtype);
+  if (B < 0 || D < 0 || L < 0 || N < 0)
+    return sw::fail(SW_ERR_INVALID_ARG, "negative size (B=%lld D=%lld N=%lld L=%lld)",
+                    (long long)B, (long long)D, (long long)N, (long long)L);
+  if (N < 1 || N > 64)
+    return sw::fail(SW_ERR_UNSUPPORTED, "N=%lld outside [1, 64]", (long long)N);
+  if (train && N > 16)
+    return sw::fail(SW_ERR_UNSUPPORTED, "checkpoints need N <= 16 (got %lld)", (long long)N);
+  int64_t R, nx;
+  if (!sw::mul_ok(B, D, &R) || !sw::mul_ok(R, L, &nx) || !sw::mul_ok(nx, 4, &nx))
+    return sw::fail(SW_ERR_UNSUPPORTED, "sizes overflow");
+  if (B * ((D + 31) / 32) >= ((int64_t)1 << 24))
+    return sw::fail(SW_ERR_UNSUPPORTED, "B*ceil(D/32)=%lld workgroups exceed the launch limit",
+                    (long long)(B * ((D + 31) / 32)));
+  if (cus <= 0) {
+    int st = sw::device_cus(&cus);
+    if (st != SW_OK) return st;
+  }
+  // arrays as the library's own allocations would be: 16-byte aligned (the
+  // pointers stand in for them and are never dereferenced)
+  alignas(16) static const float stand_in[4] = {0.f, 0.f, 0.f, 0.f};
+  sw::SelArgs a = sw::sel_args(stand_in, stand_in, stand_in, stand_in, stand_in, nullptr,
+                               const_cast<float*>(stand_in), nullptr, B, D, N, L,
+                               in_dtype == SW_DTYPE_BF16);
+  a.y_bf16 = out_dtype == SW_DTYPE_BF16;
+  if (train) a.ckpt = const_cast<float*>(stand_in);
+  a.vec = L % 4 == 0;
+  const sw::SelPlan p = sw::selective_plan(a, cus);
+  *layout = p.layout;
+  *nseg = p.nseg;
+  *lseg = p.lseg;
+  *form = p.form;
+  return SW_OK;
+}
+
 SW_API int sw_selective_scan_fwd_train(const void* x, const void* delta, const float* A,
                                        const void* Bm, const void* Cm, const float* Dskip,
                                        const void* z, const float* delta_bias, const float* h0,

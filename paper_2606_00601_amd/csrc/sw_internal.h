@@ -76,6 +76,19 @@ struct SelArgs {
 };
 int selective_fwd(const SelArgs& a);
 int selective_blelloch_fwd(const SelArgs& a);
+// The kernels a forward call takes: layout 16 (one lane per state), 4 (four
+// lanes per row, four states each) or 8 (the 8-lane kernel of any N, which
+// chains its own sequence chunks); nseg segments of lseg steps (the last
+// the rest; 1 and L for whole rows); form 0 whole rows, 1 records, 2
+// correction.  Layout 0, nseg 0: nothing to launch (B*D or L zero).
+struct SelPlan {
+  int layout = 0;
+  int64_t nseg = 0, lseg = 0;
+  int form = 0;
+};
+// The plan of selective_fwd for `a` priced for `cus` compute units (the
+// pointers of `a` are only tested for alignment; nothing is launched).
+SelPlan selective_plan(const SelArgs& a, int cus);
 // The states of the forward walk without y: the 8-step checkpoints (a.ckpt,
 // required) and h_last if given, for a backward call without the forward's
 // checkpoints.  Enqueues (*taken = true) only where the forward takes its

@@ -109,6 +109,9 @@ SW_CALL(sw_selective_scan_fwd_train, "PPPPPPPPPPPPPLLLLIII", 20,
         sw_selective_scan_fwd_train(AP(0), AP(1), AP(2), AP(3), AP(4), AP(5), AP(6), AP(7), AP(8), AP(9),
                                     AP(10), AP(11), AP(12), AL(13), AL(14), AL(15), AL(16), AI(17),
                                     AI(18), AI(19)))
+SW_CALL(sw_selective_scan_plan, "LLLLIIIIPPPP", 12,
+        sw_selective_scan_plan(AL(0), AL(1), AL(2), AL(3), AI(4), AI(5), AI(6), AI(7), AP(8), AP(9),
+                               AP(10), AP(11)))
 SW_CALL(sw_selective_scan_bwd, "PPPPPPPPPPPPPPPPPPPPPPLLLLIII", 29,
         sw_selective_scan_bwd(AP(0), AP(1), AP(2), AP(3), AP(4), AP(5), AP(6), AP(7), AP(8), AP(9), AP(10),
                               AP(11), AP(12), AP(13), AP(14), AP(15), AP(16), AP(17), AP(18), AP(19),
@@ -177,6 +180,7 @@ static PyMethodDef methods[] = {
     FAST(sw_selective_scan_fwd_ex),
     FAST(sw_selective_scan_fwd_train),
     FAST(sw_selective_scan_bwd),
+    FAST(sw_selective_scan_plan),
     FAST(sw_set_stream),
     NOARG(sw_get_stream),
     FAST(sw_status_string),

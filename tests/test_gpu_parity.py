@@ -587,6 +587,49 @@ def test_planner_choices(sw, case):
     assert_gate(fp_gate(hg, o["h_last"], o["h_mag"], o["h_sens"]), f"planner h_last {(B, D, L)}")
 
 
+def _launch_plan(text):
+    """(layout, segments, steps, form) from sw_last_launch()'s text."""
+    import re
+    if text.startswith("selective_fwd_kernel"):
+        return (8, 1, None, "whole")
+    layout = 4 if text.startswith("selective_quad_kernel") else 16
+    m = re.search(r"(\d+) segments of (\d+) steps, (records|correction) form", text)
+    if m:
+        return (layout, int(m.group(1)), int(m.group(2)), m.group(3))
+    assert text.endswith("whole rows"), text
+    return (layout, 1, None, "whole")
+
+
+# (B, D, N, L), input dtype, bf16 y: the benched shapes, a narrow long call of
+# each layout, bf16 y (records form), an N the 16-lane layouts do not take
+_PLAN_VS_LAUNCH = [((1, 5120, 16, 65536), "f32", False), ((8, 1536, 16, 2048), "bf16", False),
+                   ((2, 256, 16, 512), "f32", False), ((1, 1280, 16, 16384), "f32", False),
+                   ((1, 2560, 16, 32768), "bf16", False), ((1, 1280, 16, 4096), "f32", True),
+                   ((1, 64, 8, 1000), "f32", False)]
+
+
+@pytest.mark.parametrize("case", _PLAN_VS_LAUNCH)
+def test_plan_query_matches_the_launch(sw, case):
+    """sw_selective_scan_plan for this device names the kernels, segments and
+    form the forward call then enqueues."""
+    (B, D, N, L), dtype, y_bf16 = case
+    _say("case plan vs launch", (B, D, N, L), dtype, "bf16 y" if y_bf16 else "")
+    p = sw.selective_scan_plan(B, D, N, L, dtype, "bf16" if y_bf16 else "f32")
+    inp = wl.selective_inputs(B, D, N, L, 9900 + D, dtype)
+    if dtype == "bf16":
+        x, dl = bf16_dev(inp["x_bf16"]), bf16_dev(inp["delta_bf16"])
+        Bm, Cm = bf16_dev(inp["Bm_bf16"]), bf16_dev(inp["Cm_bf16"])
+    else:
+        x, dl, Bm, Cm = (dev(inp[k]) for k in ("x", "delta", "Bm", "Cm"))
+    sw.selective_scan_fwd(x, dl, dev(inp["A"]), Bm, Cm, dev(inp["Dskip"]),
+                          y_dtype=torch.bfloat16 if y_bf16 else torch.float32)
+    torch.cuda.synchronize()
+    got = _launch_plan(sw.last_launch())
+    want = (p["layout"], p["segments"], p["segment_steps"] if p["segments"] > 1 else None,
+            p["form"])
+    assert got == want, (sw.last_launch(), p)
+
+
 # The quad layout (four lanes per row, four states per lane, 16 rows per
 # wavefront) taken by few-row, long calls; forced here on small shapes
 # (SW_SS_QUAD=1) with the segment count given: D not a multiple of 64 leaves
