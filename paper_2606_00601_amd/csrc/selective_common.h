@@ -23,6 +23,12 @@ struct Elt<uint16_t> {
   }
 };
 
+// Cache policy of a buffer access (the `aux` operand of the raw buffer
+// builtins): SW_NT marks it non-temporal -- for data a kernel reads or writes
+// once, so that it does not displace lines other workgroups read again (B and
+// C of a batch).
+constexpr int SW_NT = 2;
+
 // Raw registers for COUNT consecutive elements of type IN.
 template <typename IN, int COUNT>
 struct RawVec {
@@ -49,27 +55,28 @@ struct RawVec {
       }
     }
   }
-  // from a raw buffer resource at byte offset `off` (16- or 8-byte aligned);
-  // bytes outside the resource's range read as zero
+  // from a raw buffer resource at byte offset `off` (16- or 8-byte aligned),
+  // with cache policy POL; bytes outside the resource's range read as zero
+  template <int POL = 0>
   __device__ __forceinline__ void load_buf(__amdgpu_buffer_rsrc_t rs, int32_t off) {
     if constexpr (W % 4 == 0) {
 #pragma unroll
       for (int q = 0; q < W / 4; ++q) {
         const uint4 v =
-            __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 * q, 0, 0));
+            __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 * q, 0, POL));
         w[4 * q] = v.x;
         w[4 * q + 1] = v.y;
         w[4 * q + 2] = v.z;
         w[4 * q + 3] = v.w;
       }
     } else if constexpr (W == 1) {
-      w[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+      w[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, POL));
     } else {
       static_assert(W % 2 == 0, "8-byte granularity");
 #pragma unroll
       for (int q = 0; q < W / 2; ++q) {
         const uint2 v =
-            __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs, off + 8 * q, 0, 0));
+            __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs, off + 8 * q, 0, POL));
         w[2 * q] = v.x;
         w[2 * q + 1] = v.y;
       }

@@ -269,7 +269,9 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     // Ls is a multiple of V: a lane's V steps are all in or all out
     const int32_t t = (int32_t)(sup * ST) + V * n;
     const int32_t off = t < Ls32 ? lrow + t * ES : R16_OOB;
-    dlr.load_buf(rd, off);
+    // delta is read once (non-temporal); x is read again for the y of its
+    // tiles (fetch_yx), so this read keeps the default policy
+    dlr.template load_buf<SW_NT>(rd, off);
     xr.load_buf(rx, off);
   };
   auto widen_dx = [&](int64_t sup) {
@@ -300,8 +302,8 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   auto fetch_yx = [&](int64_t kt) {
     if constexpr (NOY) return;
     const int32_t off = lrow + (int32_t)((kt * R16_T + 4 * rq) * ES);
-    yxr.load_buf(rx, off);
-    if constexpr (OPT) yzr.load_buf(rz, off);
+    yxr.template load_buf<SW_NT>(rx, off);  // the last read of x
+    if constexpr (OPT) yzr.template load_buf<SW_NT>(rz, off);
   };
   float* const p_w = &sm.p[w][r * R16_PRS + n * R16_TS];
   const float* const p_r = &sm.p[w][r * R16_PRS + 8 * rh * R16_TS + 4 * rq];
@@ -309,7 +311,8 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
   // leave through buffer resources over the workgroup's rows from the
   // segment's start: a 32-bit offset per lane, and lanes with nothing to
   // store aim at the resource's end, where the hardware drops the store.
-  // Sizes fit 32 bits: 16 rows of L < 2^26 steps of at most 4 bytes.
+  // Sizes fit 32 bits: 16 rows of L < 2^26 steps of at most 4 bytes.  Both
+  // are written once, with the non-temporal policy.
   const uint32_t ys = ybf ? 2u : 4u;
   const uint32_t y_bytes = (uint32_t)((rows * L - ts) * ys);
   const __amdgpu_buffer_rsrc_t ry =
@@ -348,7 +351,7 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
         const uint32_t so = mine ? s_lrow + 4u * (uint32_t)t : s_bytes;
         __builtin_amdgcn_raw_buffer_store_b128(
             __builtin_bit_cast(sw_u32x4, make_float4(s4[0], s4[1], s4[2], s4[3])), rs, (int)so,
-            0, 0);
+            0, SW_NT);
       }
     }
 #pragma unroll
@@ -357,10 +360,11 @@ __global__ __launch_bounds__(256) void selective_row16_kernel(
     if (ybf)
       __builtin_amdgcn_raw_buffer_store_b64(
           __builtin_bit_cast(sw_u32x2, make_uint2(bf16x2_rne(s4[0], s4[1]), bf16x2_rne(s4[2], s4[3]))),
-          ry, (int)yo, 0, 0);
+          ry, (int)yo, 0, SW_NT);
     else
       __builtin_amdgcn_raw_buffer_store_b128(
-          __builtin_bit_cast(sw_u32x4, make_float4(s4[0], s4[1], s4[2], s4[3])), ry, (int)yo, 0, 0);
+          __builtin_bit_cast(sw_u32x4, make_float4(s4[0], s4[1], s4[2], s4[3])), ry, (int)yo, 0,
+          SW_NT);
   };
 
   auto read_ops = [&](R16Ops& o, int buf, int bi) {

@@ -20,7 +20,9 @@
 // reads back as 16-byte reads shared by the lanes of a quad (delta) or by all
 // lanes of a state group (B, C).  Global memory moves in 32-step tiles, 128
 // contiguous bytes of a row per 8 lanes (x, delta, z loaded a tile ahead; y
-// stored from a small LDS transpose by the lanes that hold its x and z).
+// stored from a small LDS transpose by the lanes that hold its x and z); what
+// is read or written once goes non-temporal, B and C (read by every row block
+// of the batch) do not.
 //
 // With four lanes per row the parallelism is a quarter of one lane per state,
 // so rows are cut into segments and walked in the correction form of
@@ -193,9 +195,11 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int32_t off = ioff[k] + kt * (Q_T * ES);
-      nx.d[k].load_buf(rd, off);
-      nx.x[k].load_buf(rx, off);
-      if constexpr (OPT) nx.z[k].load_buf(rz, off);
+      // x, delta and z are read once: non-temporal, so that they do not
+      // displace the B and C lines the other row blocks read
+      nx.d[k].template load_buf<SW_NT>(rd, off);
+      nx.x[k].template load_buf<SW_NT>(rx, off);
+      if constexpr (OPT) nx.z[k].template load_buf<SW_NT>(rz, off);
       const int32_t bo = boff + (kt * Q_T + 16 * k) * (Q_N * ES);
       nx.b[k].load_buf(rb, bo);
       nx.c[k].load_buf(rc, bo);
@@ -296,13 +300,14 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
       if constexpr (OPT) {
         if (s_out)
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(sw_u32x4, s), rso, (int)at, 0,
-                                                 0);
+                                                 SW_NT);
         s.x *= zc[k][0];
         s.y *= zc[k][1];
         s.z *= zc[k][2];
         s.w *= zc[k][3];
       }
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(sw_u32x4, s), ry, (int)at, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(sw_u32x4, s), ry, (int)at, 0,
+                                             SW_NT);
     }
   };
 
