@@ -20,9 +20,9 @@
 // reads back as 16-byte reads shared by the lanes of a quad (delta) or by all
 // lanes of a state group (B, C).  Global memory moves in 32-step tiles, 128
 // contiguous bytes of a row per 8 lanes (x, delta, z loaded a tile ahead; y
-// stored from a small LDS transpose by the lanes that hold its x and z); what
-// is read or written once goes non-temporal, B and C (read by every row block
-// of the batch) do not.
+// stored from a small LDS transpose by the lanes that hold its x and z); y
+// and fp32 x, delta, z, read or written once in whole lines, go non-temporal,
+// B and C (read by every row block of the batch) do not.
 //
 // With four lanes per row the parallelism is a quarter of one lane per state,
 // so rows are cut into segments and walked in the correction form of
@@ -110,6 +110,7 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
     uint32_t flags_in, float* __restrict__ s_out, int nseg, int Lseg) {
   constexpr bool CORR = MODE == Q_CORR;
   constexpr int ES = (int)sizeof(IN);
+  constexpr int XPOL = ES == 4 ? SW_NT : 0;  // cache policy of the x, delta, z loads
   const uint32_t flags = OPT ? flags_in : 0u;
   const bool gated = OPT && (flags & SEL_GATED);
   __shared__ __align__(16) QSmem sm;
@@ -195,11 +196,12 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int32_t off = ioff[k] + kt * (Q_T * ES);
-      // x, delta and z are read once: non-temporal, so that they do not
-      // displace the B and C lines the other row blocks read
-      nx.d[k].template load_buf<SW_NT>(rd, off);
-      nx.x[k].template load_buf<SW_NT>(rx, off);
-      if constexpr (OPT) nx.z[k].template load_buf<SW_NT>(rz, off);
+      // x, delta and z are read once: non-temporal in fp32, where a tile of a
+      // row is one whole 128-byte line (in bf16 it is half a line, whose other
+      // half the next tile reads: the default policy measured faster there)
+      nx.d[k].template load_buf<XPOL>(rd, off);
+      nx.x[k].template load_buf<XPOL>(rx, off);
+      if constexpr (OPT) nx.z[k].template load_buf<XPOL>(rz, off);
       const int32_t bo = boff + (kt * Q_T + 16 * k) * (Q_N * ES);
       nx.b[k].load_buf(rb, bo);
       nx.c[k].load_buf(rc, bo);
