@@ -26,7 +26,8 @@ struct Elt<uint16_t> {
 // Cache policy of a buffer access (the `aux` operand of the raw buffer
 // builtins): SW_NT marks it non-temporal -- for data a kernel reads or writes
 // once, so that it does not displace lines other workgroups read again (B and
-// C of a batch).
+// C of a batch).  Only where one instruction covers whole 128-byte lines: a
+// line read in parts by successive instructions measured slower with it.
 constexpr int SW_NT = 2;
 
 // Raw registers for COUNT consecutive elements of type IN.
