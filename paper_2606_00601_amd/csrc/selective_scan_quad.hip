@@ -190,7 +190,8 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
     RawVec<IN, 4> d[2], x[2], z[2], b[2], c[2];
   };
   Raw nx;                      // raw inputs of the next tile
-  float xc[2][4], zc[2][4];    // x and z of the current tile, for y
+  float xc[2][4], zc[2][4];    // x and z of the tile whose y is stored next
+  float xn[2][4], zn[2][4];    // the same of the tile staged last
   float dsum[2] = {0.f, 0.f};  // this lane's share of the sum of delta' of rows l/8, l/8+8
   auto load_tile = [&](int kt) {
 #pragma unroll
@@ -219,12 +220,12 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
         if constexpr (OPT) {
           dv += idb[k];
           if (flags & SEL_SOFTPLUS) dv = softplus_f32(dv);
-          zc[k][q] = gated ? silu_f32(nx.z[k].get(q)) : 1.0f;
+          zn[k][q] = gated ? silu_f32(nx.z[k].get(q)) : 1.0f;
         }
         dsum[k] += dv;
         dv4[q] = dv;
         dx4[q] = dv * xv;
-        xc[k][q] = xv;
+        xn[k][q] = xv;
       }
       const int o = qswz(ir + 8 * k, ij);
       *reinterpret_cast<float4*>(&tl.dl[o]) = make_float4(dv4[0], dv4[1], dv4[2], dv4[3]);
@@ -234,6 +235,16 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
       tl.bc[(lane >> 2) + 16 * k][lane & 3][1] =
           make_float4(nx.c[k].get(0), nx.c[k].get(1), nx.c[k].get(2), nx.c[k].get(3));
     }
+  };
+  // the staged tile's x and z become those of the next y store
+  auto take_next = [&]() {
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        xc[k][q] = xn[k][q];
+        if constexpr (OPT) zc[k][q] = zn[k][q];
+      }
   };
   // the sum of delta' of row r (over the staged tiles), in every lane of quad r
   auto row_dsum = [&]() {
@@ -316,12 +327,20 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
   // ---- prologue: tile 0 staged, tile 1 in flight
   load_tile(0);
   stage_tile();
+  take_next();
   load_tile(1);
   q_wave_order();
 
   // One tile: walk it, store its y, stage the next and load the one after.
   // (A second tile of loads in flight measured no faster and doubles the
-  // registers of the correction walk.)
+  // registers of the correction walk.)  In the plain walk from zero the next
+  // tile is staged before the y store: that ends the loaded registers' life
+  // before the y values are formed.  With the store first both were live at
+  // once, the compiler moved the loaded values at the loop's join, and each
+  // move waited for its load as soon as issued.  (The correction walk and the
+  // calls with options keep that order: the carried x and z of the staged
+  // tile would cost them a wavefront per SIMD.)
+  constexpr bool STAGE_FIRST = !CORR && !OPT;
   int kt_end = ntile;  // the correction walk lowers it once the carried part has faded
 #pragma unroll 1
   for (int kt = 0; kt < kt_end; ++kt) {
@@ -342,9 +361,12 @@ __global__ __launch_bounds__(256) void selective_quad_kernel(
       }
     }
     q_wave_order();  // the tile's reads are done and its y sums written
+    const bool more = kt + 1 < kt_end;
+    if (STAGE_FIRST && more) stage_tile();
     store_y(kt);
-    if (kt + 1 < kt_end) {
-      stage_tile();
+    if (more) {
+      if (!STAGE_FIRST) stage_tile();
+      take_next();
       load_tile(kt + 2);
     }
     q_wave_order();
