@@ -637,11 +637,12 @@ def test_plan_query_matches_the_launch(sw, case):
 # steps leaves the last segment the shortest (2048 / 3: 704, 704, 640; 8192 /
 # 7), and where that would leave it under 64 steps the length is rounded down
 # and the last segment is the longest (160 / 2: 64 + 96; 1056 / 16: 15 x 64 +
-# 96); one segment is the whole-row walk; L = 1040 (not whole 32-step tiles)
-# falls back to the 16-lane layout.  (B, D, L), segments.
+# 96); one segment is the whole-row walk, down to rows of one tile (L = 32);
+# L = 1040 (not whole 32-step tiles) falls back to the 16-lane layout.
+# (B, D, L), segments.
 _QUAD_CASES = [((1, 37, 1040), "2"), ((2, 100, 2048), "3"), ((1, 64, 4096), "4"),
                  ((1, 5, 16), "1"), ((3, 130, 512), "1"), ((1, 70, 8192), "7"),
-                 ((1, 37, 160), "2"), ((1, 37, 1056), "16")]
+                 ((1, 37, 160), "2"), ((1, 37, 1056), "16"), ((2, 70, 32), "1")]
 
 
 @pytest.mark.parametrize("case", _QUAD_CASES)
